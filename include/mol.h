@@ -1,0 +1,159 @@
+/*
+ * mol.h -- C ABI of the MI355X (gfx950) Mixture-of-Logits retrieval library.
+ *
+ * Problem (paper: "Retrieval with Learned Similarities", Section 2 Eq. 1-2,
+ * Section 3 Definition 1, Algorithm 2, Appendix A.3):
+ *
+ *   s_p(q,x)  = < f_pq(q), g_px(x) >,            p = pq * Px + px, P = Pq * Px
+ *   u_j       = b1[j] + sum_p W1[j][p] s_p        (j < H)
+ *   l_p       = a_q[q][p] + a_x[x][p] + b2[p] + sum_j W2[p][j] SiLU(u_j)
+ *   pi        = softmax_p(l)                      (sum_p pi_p = 1)
+ *   phi(q,x)  = sum_p pi_p s_p
+ *
+ * Memory: every array pointer below is a DEVICE pointer owned by the caller.
+ * The library allocates no device memory, keeps no pointer after a call
+ * returns, and holds no global state other than a per-thread last-error
+ * string.  Calls are asynchronous on `stream` (a hipStream_t passed as
+ * void*, NULL = the null stream); outputs are valid once the caller has
+ * synchronised that stream.  Calls on different streams may run
+ * concurrently as long as their outputs and workspaces do not overlap.
+ *
+ * Layouts (row-major, densely packed, element types by `dtype`):
+ *   Q   [B][Pq][d]   query component embeddings            (dtype)
+ *   X   [Px][N][d]   item component embeddings, component-major (dtype)
+ *   a_q [B][P]  a_x [N][P]  b1 [H]  b2 [P]                 (float32)
+ *   W1  [H][P]  W2  [P][H]                                 (dtype)
+ * Embeddings are used as given: Eq. 2's L2 normalisation is a
+ * precomputation and is never redone by the library.  Inputs must be finite.
+ *
+ * Ordering: every top-k output row is sorted by score descending, ties
+ * broken by item index ascending.  Where a row has fewer than k valid items
+ * (mol_rerank only) it is padded with index -1 and score -INFINITY.
+ *
+ * Errors: each entry point validates all arguments on the host before it
+ * launches anything.  On error it returns a nonzero mol_status, launches
+ * nothing, leaves outputs untouched, and records a message retrievable with
+ * mol_last_error() on the calling thread.  MOL_EHIP reports a HIP runtime
+ * failure at launch time (the message carries the HIP error string).
+ */
+#ifndef MOL_H_
+#define MOL_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  MOL_OK = 0,
+  MOL_EINVAL = 1,        /* null pointer, size out of range, bad k          */
+  MOL_EUNSUPPORTED = 2,  /* shape or dtype outside the kernel set           */
+  MOL_EWORKSPACE = 3,    /* workspace smaller than mol_workspace_size says  */
+  MOL_EHIP = 4           /* HIP runtime error on launch                     */
+} mol_status;
+
+typedef enum { MOL_F32 = 0, MOL_BF16 = 1 } mol_dtype;
+
+/* Operation codes for mol_workspace_size. */
+typedef enum {
+  MOL_OP_SCORE = 0,
+  MOL_OP_TOPK_EXACT = 1,
+  MOL_OP_TOPK_PER_EMBD = 2,
+  MOL_OP_RERANK = 3
+} mol_op;
+
+/* Limits of the kernel set. */
+#define MOL_MAX_P 64      /* Pq * Px                                        */
+#define MOL_MAX_H 256     /* gating MLP hidden width                         */
+#define MOL_MAX_D 1024    /* component embedding width                       */
+#define MOL_MAX_K 1024    /* k of every top-k output                         */
+#define MOL_MAX_C 16384   /* candidates per query handed to mol_rerank       */
+
+/* One retrieval problem: shapes, storage type and device pointers (the
+ * notation table of Section 2; gating parameters per Appendix A.3).
+ * Pointers not used by an entry point may be NULL (see each function). */
+typedef struct mol_problem {
+  int32_t B;      /* number of queries                                      */
+  int32_t N;      /* number of items                                        */
+  int32_t Pq;     /* query components                                       */
+  int32_t Px;     /* item components                                        */
+  int32_t d;      /* component embedding width d_P                          */
+  int32_t H;      /* gating MLP hidden width                                */
+  int32_t dtype;  /* mol_dtype of Q, X, W1, W2                              */
+  const void *Q;
+  const void *X;
+  const float *a_q;
+  const float *a_x;
+  const void *W1;
+  const float *b1;
+  const void *W2;
+  const float *b2;
+} mol_problem;
+
+/* Bytes of workspace an entry point needs for this problem (k, kprime and C
+ * as they will be passed; ignored where irrelevant).  Writes *bytes.
+ * Returns MOL_OK or the validation error the entry point would return. */
+int mol_workspace_size(const mol_problem *prob, int op, int32_t k,
+                       int32_t kprime, int32_t C, size_t *bytes);
+
+/* Dense MoL scores (Eq. 1 with the Appendix A.3 gating) of every query
+ * against items n_begin .. n_begin + n_count - 1:
+ *   phi[b][i] = phi(q_b, x_{n_begin + i}),   phi is float32 [B][n_count].
+ * Needs every problem pointer.  n_count == 0 is a no-op.  No workspace. */
+int mol_score(const mol_problem *prob, int32_t n_begin, int32_t n_count,
+              float *phi, void *stream);
+
+/* Exact top-k with MoL (Definition 1; the paper's brute-force baseline):
+ * for every query, the k items of the whole corpus with the largest phi.
+ * out_score float32 [B][k], out_idx int32 [B][k].  1 <= k <= min(N, 1024).
+ * Needs every problem pointer and mol_workspace_size(MOL_OP_TOPK_EXACT)
+ * bytes of workspace (any alignment of 256 bytes or more). */
+int mol_topk_exact(const mol_problem *prob, int32_t k, float *out_score,
+                   int32_t *out_idx, void *ws, size_t ws_bytes, void *stream);
+
+/* TopKPerEmbedding stage 1 (Algorithm 2, TopKDotProduct for every
+ * component): for every query b and component p = pq * Px + px, the k'
+ * items with the largest s_p = <f_pq(q_b), g_px(x)>.
+ * out_dot float32 [B][P][k'], out_idx int32 [B][P][k'].
+ * 1 <= kprime <= min(N, 1024).  Reads only Q and X (a_q, a_x, W1, b1, W2,
+ * b2 may be NULL; H is ignored).  TopKAvg (Section 3.2) is this call on the
+ * averaged problem: Pq = Px = 1, Q = q', X = x' from mol_avg_embed. */
+int mol_topk_per_embd(const mol_problem *prob, int32_t kprime, float *out_dot,
+                      int32_t *out_idx, void *ws, size_t ws_bytes,
+                      void *stream);
+
+/* Candidate union, deduplication and MoL rerank (Algorithm 2,
+ * BruteForceTopKMoL over the deduplicated candidate set G).
+ * cand int32 [B][C]: item ids, duplicates allowed, any negative id marks
+ * an empty slot; every non-negative id must be < N.  For each query the
+ * distinct ids are scored with full MoL and the top-k kept.
+ * out_score float32 [B][k], out_idx int32 [B][k] (padded with -INFINITY /
+ * -1 when a query has fewer than k distinct ids), out_n_unique int32 [B]
+ * (may be NULL).  1 <= C <= 16384, 1 <= k <= 1024.  Needs every problem
+ * pointer. */
+int mol_rerank(const mol_problem *prob, const int32_t *cand, int32_t C,
+               int32_t k, float *out_score, int32_t *out_idx,
+               int32_t *out_n_unique, void *ws, size_t ws_bytes, void *stream);
+
+/* TopKAvg materialisation (Section 3.2, Algorithm 2 TopKAvg):
+ *   q_avg[b][t] = round( sum_pq Q[b][pq][t] ),  [B][d]
+ *   x_avg[n][t] = round( sum_px X[px][n][t] ),  [N][d]
+ * each sum formed exactly (float64) and rounded once to dtype, nearest-even.
+ * The averaged dot product's 1/P factor does not change any ranking and is
+ * left out.  Either output pointer may be NULL to skip it.  No workspace. */
+int mol_avg_embed(const mol_problem *prob, void *q_avg, void *x_avg,
+                  void *stream);
+
+/* Static description of a status code. */
+const char *mol_status_str(int status);
+
+/* Message of the last failing call on this thread ("" if none). */
+const char *mol_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MOL_H_ */

@@ -1,0 +1,310 @@
+// Host side of the C ABI declared in include/mol.h: argument validation,
+// workspace planning and kernel sequencing on the caller's stream.
+#include <algorithm>
+#include <cstdarg>
+#include <cstdio>
+#include <string>
+
+#include "mol_kernels.h"
+
+using namespace mol;
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int status, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return status;
+}
+
+int hip_fail(hipError_t e, const char* where) {
+  return fail(MOL_EHIP, "%s: %s", where, hipGetErrorString(e));
+}
+
+#define MOL_TRY_HIP(expr, where)               \
+  do {                                         \
+    hipError_t e_ = (expr);                    \
+    if (e_ != hipSuccess) return hip_fail(e_, where); \
+  } while (0)
+
+constexpr size_t kAlign = 256;
+size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
+
+// Shape / pointer validation shared by every entry point.
+int check_problem(const mol_problem* p, bool gating) {
+  if (!p) return fail(MOL_EINVAL, "prob is NULL");
+  if (p->B < 1 || p->N < 1 || p->Pq < 1 || p->Px < 1 || p->d < 1)
+    return fail(MOL_EINVAL, "sizes must be positive (B=%d N=%d Pq=%d Px=%d d=%d)", p->B, p->N,
+                p->Pq, p->Px, p->d);
+  if (gating && p->H < 1) return fail(MOL_EINVAL, "H must be positive (H=%d)", p->H);
+  if (p->dtype != MOL_F32 && p->dtype != MOL_BF16)
+    return fail(MOL_EUNSUPPORTED, "dtype %d is not MOL_F32 or MOL_BF16", p->dtype);
+  if (p->Pq > MOL_MAX_P || p->Px > MOL_MAX_P || p->Pq * p->Px > MOL_MAX_P)
+    return fail(MOL_EUNSUPPORTED, "P = Pq*Px = %d*%d exceeds %d", p->Pq, p->Px, MOL_MAX_P);
+  if (p->d > MOL_MAX_D) return fail(MOL_EUNSUPPORTED, "d = %d exceeds %d", p->d, MOL_MAX_D);
+  if (gating && p->H > MOL_MAX_H) return fail(MOL_EUNSUPPORTED, "H = %d exceeds %d", p->H, MOL_MAX_H);
+  if (!p->Q || !p->X) return fail(MOL_EINVAL, "Q or X is NULL");
+  if (gating && (!p->a_q || !p->a_x || !p->W1 || !p->b1 || !p->W2 || !p->b2))
+    return fail(MOL_EINVAL, "a gating pointer (a_q, a_x, W1, b1, W2, b2) is NULL");
+  return MOL_OK;
+}
+
+DevProb dev_prob(const mol_problem* p) {
+  DevProb d;
+  d.B = p->B; d.N = p->N; d.Pq = p->Pq; d.Px = p->Px; d.P = p->Pq * p->Px;
+  d.d = p->d; d.H = p->H; d.dtype = p->dtype;
+  d.Q = p->Q; d.X = p->X; d.a_q = p->a_q; d.a_x = p->a_x;
+  d.W1 = p->W1; d.b1 = p->b1; d.W2 = p->W2; d.b2 = p->b2;
+  return d;
+}
+
+// ---------------------------------------------------------------------------
+// Streaming top-k over tiles of items (generic path).  For every row the
+// keys of one tile plus the running top-k are reduced by repeated segmented
+// sorts until k remain.
+// ---------------------------------------------------------------------------
+struct StreamPlan {
+  int rows = 0, k = 0, T = 0;
+  long strideA = 0, strideB = 0;
+  size_t offRun = 0, offA = 0, offB = 0, bytes = 0;
+};
+
+StreamPlan plan_stream(int rows, int N, int k) {
+  StreamPlan s;
+  s.rows = rows;
+  s.k = k;
+  const long budget = 256l << 20;  // bytes of tile keys
+  long T = budget / (8l * rows);
+  T = std::max(1024l, std::min(T, static_cast<long>(N)));
+  T = (T + 255) / 256 * 256;
+  s.T = static_cast<int>(T);
+  const long L0 = T + k;
+  const int S0 = segment_size_for(static_cast<int>(L0), k);
+  s.strideA = L0;
+  s.strideB = std::max<long>((L0 + S0 - 1) / S0 * k, k);
+  size_t off = 0;
+  s.offRun = off; off = align_up(off + 8ul * rows * k);
+  s.offA = off;   off = align_up(off + 8ul * rows * s.strideA);
+  s.offB = off;   off = align_up(off + 8ul * rows * s.strideB);
+  s.bytes = off;
+  return s;
+}
+
+// Reduce rows of `len` keys held in buffer A (stride strideA) to the top k,
+// written to `out` (stride out_stride).  Uses A and B as ping-pong buffers.
+int reduce_rows(const StreamPlan& s, char* ws, long len, uint64_t* out, long out_stride,
+                hipStream_t st) {
+  uint64_t* bufs[2] = {reinterpret_cast<uint64_t*>(ws + s.offA), reinterpret_cast<uint64_t*>(ws + s.offB)};
+  long strides[2] = {s.strideA, s.strideB};
+  int cur = 0;
+  for (;;) {
+    const int S = segment_size_for(static_cast<int>(len), s.k);
+    const long nseg = (len + S - 1) / S;
+    if (nseg == 1) {
+      MOL_TRY_HIP(launch_segment_topk(bufs[cur], strides[cur], s.rows, static_cast<int>(len), s.k,
+                                      out, out_stride, st), "segment top-k");
+      return MOL_OK;
+    }
+    const int nxt = 1 - cur;
+    if (nseg * s.k > strides[nxt]) return fail(MOL_EHIP, "internal: top-k buffer too small");
+    MOL_TRY_HIP(launch_segment_topk(bufs[cur], strides[cur], s.rows, static_cast<int>(len), s.k,
+                                    bufs[nxt], strides[nxt], st), "segment top-k");
+    len = nseg * s.k;
+    cur = nxt;
+  }
+}
+
+// Tile-by-tile exact selection; `score_tile` writes keys of items
+// [n0, n0+nt) into A (row stride strideA).
+template <typename F>
+int stream_topk(const StreamPlan& s, int N, char* ws, F score_tile, float* out_score,
+                int32_t* out_idx, hipStream_t st) {
+  uint64_t* run = reinterpret_cast<uint64_t*>(ws + s.offRun);
+  uint64_t* A = reinterpret_cast<uint64_t*>(ws + s.offA);
+  MOL_TRY_HIP(launch_fill(run, static_cast<long>(s.rows) * s.k, 0ull, st), "fill");
+  for (long n0 = 0; n0 < N; n0 += s.T) {
+    const int nt = static_cast<int>(std::min<long>(s.T, N - n0));
+    MOL_TRY_HIP(score_tile(static_cast<int>(n0), nt, A, s.strideA), "score tile");
+    MOL_TRY_HIP(launch_copy_rows(run, s.k, s.rows, s.k, A + nt, s.strideA, st), "copy rows");
+    int rc = reduce_rows(s, ws, nt + s.k, run, s.k, st);
+    if (rc != MOL_OK) return rc;
+  }
+  MOL_TRY_HIP(launch_decode(run, s.k, s.rows, s.k, out_score, out_idx, st), "decode");
+  return MOL_OK;
+}
+
+// Rerank workspace: uniq [B][C], n_unique [B], key rows A/B, final keys.
+struct RerankPlan {
+  StreamPlan s;
+  size_t offUniq = 0, offNu = 0, offFinal = 0, bytes = 0;
+};
+
+RerankPlan plan_rerank(int B, int C, int k) {
+  RerankPlan r;
+  StreamPlan& s = r.s;
+  s.rows = B;
+  s.k = k;
+  s.T = C;
+  const int S0 = segment_size_for(C, k);
+  s.strideA = std::max(C, k);
+  s.strideB = std::max<long>((C + S0 - 1) / S0 * k, k);
+  size_t off = 0;
+  s.offA = off;   off = align_up(off + 8ul * B * s.strideA);
+  s.offB = off;   off = align_up(off + 8ul * B * s.strideB);
+  r.offFinal = off; off = align_up(off + 8ul * B * k);
+  r.offUniq = off;  off = align_up(off + 4ul * B * C);
+  r.offNu = off;    off = align_up(off + 4ul * B);
+  r.bytes = off;
+  return r;
+}
+
+int check_ws(void* ws, size_t have, size_t need) {
+  if (need == 0) return MOL_OK;
+  if (!ws) return fail(MOL_EINVAL, "workspace is NULL (need %zu bytes)", need);
+  if (reinterpret_cast<uintptr_t>(ws) % kAlign)
+    return fail(MOL_EINVAL, "workspace must be %zu-byte aligned", kAlign);
+  if (have < need) return fail(MOL_EWORKSPACE, "workspace has %zu bytes, needs %zu", have, need);
+  return MOL_OK;
+}
+
+int check_k(int32_t k, int32_t N, const char* name) {
+  if (k < 1 || k > MOL_MAX_K) return fail(MOL_EINVAL, "%s = %d outside [1, %d]", name, k, MOL_MAX_K);
+  if (k > N) return fail(MOL_EINVAL, "%s = %d exceeds N = %d", name, k, N);
+  return MOL_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* mol_last_error(void) { return g_err.c_str(); }
+
+const char* mol_status_str(int status) {
+  switch (status) {
+    case MOL_OK: return "MOL_OK";
+    case MOL_EINVAL: return "MOL_EINVAL: invalid argument";
+    case MOL_EUNSUPPORTED: return "MOL_EUNSUPPORTED: shape or dtype not supported";
+    case MOL_EWORKSPACE: return "MOL_EWORKSPACE: workspace too small";
+    case MOL_EHIP: return "MOL_EHIP: HIP runtime error";
+    default: return "unknown mol_status";
+  }
+}
+
+int mol_workspace_size(const mol_problem* prob, int op, int32_t k, int32_t kprime, int32_t C,
+                       size_t* bytes) {
+  if (!bytes) return fail(MOL_EINVAL, "bytes is NULL");
+  int rc;
+  switch (op) {
+    case MOL_OP_SCORE:
+      if ((rc = check_problem(prob, true))) return rc;
+      *bytes = 0;
+      return MOL_OK;
+    case MOL_OP_TOPK_EXACT:
+      if ((rc = check_problem(prob, true))) return rc;
+      if ((rc = check_k(k, prob->N, "k"))) return rc;
+      *bytes = plan_stream(prob->B, prob->N, k).bytes;
+      return MOL_OK;
+    case MOL_OP_TOPK_PER_EMBD:
+      if ((rc = check_problem(prob, false))) return rc;
+      if ((rc = check_k(kprime, prob->N, "kprime"))) return rc;
+      *bytes = plan_stream(prob->B * prob->Pq * prob->Px, prob->N, kprime).bytes;
+      return MOL_OK;
+    case MOL_OP_RERANK:
+      if ((rc = check_problem(prob, true))) return rc;
+      if (k < 1 || k > MOL_MAX_K) return fail(MOL_EINVAL, "k = %d outside [1, %d]", k, MOL_MAX_K);
+      if (C < 1 || C > MOL_MAX_C) return fail(MOL_EINVAL, "C = %d outside [1, %d]", C, MOL_MAX_C);
+      *bytes = plan_rerank(prob->B, C, k).bytes;
+      return MOL_OK;
+    default:
+      return fail(MOL_EINVAL, "unknown op %d", op);
+  }
+}
+
+int mol_score(const mol_problem* prob, int32_t n_begin, int32_t n_count, float* phi, void* stream) {
+  int rc;
+  if ((rc = check_problem(prob, true))) return rc;
+  if (n_begin < 0 || n_count < 0 || static_cast<long>(n_begin) + n_count > prob->N)
+    return fail(MOL_EINVAL, "item range [%d, %d+%d) outside [0, %d)", n_begin, n_begin, n_count, prob->N);
+  if (n_count == 0) return MOL_OK;
+  if (!phi) return fail(MOL_EINVAL, "phi is NULL");
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const DevProb pr = dev_prob(prob);
+  MOL_TRY_HIP(launch_phi_generic(pr, n_begin, n_count, nullptr, nullptr, 0, phi, n_count, nullptr,
+                                 0, st), "mol_score");
+  return MOL_OK;
+}
+
+int mol_topk_exact(const mol_problem* prob, int32_t k, float* out_score, int32_t* out_idx, void* ws,
+                   size_t ws_bytes, void* stream) {
+  int rc;
+  if ((rc = check_problem(prob, true))) return rc;
+  if ((rc = check_k(k, prob->N, "k"))) return rc;
+  if (!out_score || !out_idx) return fail(MOL_EINVAL, "output pointer is NULL");
+  const StreamPlan s = plan_stream(prob->B, prob->N, k);
+  if ((rc = check_ws(ws, ws_bytes, s.bytes))) return rc;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const DevProb pr = dev_prob(prob);
+  auto tile = [&](int n0, int nt, uint64_t* A, long strideA) {
+    return launch_phi_generic(pr, n0, nt, nullptr, nullptr, 0, nullptr, 0, A, strideA, st);
+  };
+  return stream_topk(s, prob->N, static_cast<char*>(ws), tile, out_score, out_idx, st);
+}
+
+int mol_topk_per_embd(const mol_problem* prob, int32_t kprime, float* out_dot, int32_t* out_idx,
+                      void* ws, size_t ws_bytes, void* stream) {
+  int rc;
+  if ((rc = check_problem(prob, false))) return rc;
+  if ((rc = check_k(kprime, prob->N, "kprime"))) return rc;
+  if (!out_dot || !out_idx) return fail(MOL_EINVAL, "output pointer is NULL");
+  const int rows = prob->B * prob->Pq * prob->Px;
+  const StreamPlan s = plan_stream(rows, prob->N, kprime);
+  if ((rc = check_ws(ws, ws_bytes, s.bytes))) return rc;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const DevProb pr = dev_prob(prob);
+  auto tile = [&](int n0, int nt, uint64_t* A, long strideA) {
+    return launch_dots_generic(pr, n0, nt, A, strideA, st);
+  };
+  return stream_topk(s, prob->N, static_cast<char*>(ws), tile, out_dot, out_idx, st);
+}
+
+int mol_rerank(const mol_problem* prob, const int32_t* cand, int32_t C, int32_t k, float* out_score,
+               int32_t* out_idx, int32_t* out_n_unique, void* ws, size_t ws_bytes, void* stream) {
+  int rc;
+  if ((rc = check_problem(prob, true))) return rc;
+  if (k < 1 || k > MOL_MAX_K) return fail(MOL_EINVAL, "k = %d outside [1, %d]", k, MOL_MAX_K);
+  if (C < 1 || C > MOL_MAX_C) return fail(MOL_EINVAL, "C = %d outside [1, %d]", C, MOL_MAX_C);
+  if (!cand || !out_score || !out_idx) return fail(MOL_EINVAL, "cand or output pointer is NULL");
+  const RerankPlan r = plan_rerank(prob->B, C, k);
+  if ((rc = check_ws(ws, ws_bytes, r.bytes))) return rc;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  char* w = static_cast<char*>(ws);
+  const DevProb pr = dev_prob(prob);
+  int32_t* uniq = reinterpret_cast<int32_t*>(w + r.offUniq);
+  int32_t* nu = reinterpret_cast<int32_t*>(w + r.offNu);
+  uint64_t* A = reinterpret_cast<uint64_t*>(w + r.s.offA);
+  uint64_t* fin = reinterpret_cast<uint64_t*>(w + r.offFinal);
+  MOL_TRY_HIP(launch_dedup(cand, prob->B, C, prob->N, uniq, nu, st), "dedup");
+  MOL_TRY_HIP(launch_phi_generic(pr, 0, C, uniq, nu, C, nullptr, 0, A, r.s.strideA, st), "rerank score");
+  if ((rc = reduce_rows(r.s, w, C, fin, k, st))) return rc;
+  MOL_TRY_HIP(launch_decode(fin, k, prob->B, k, out_score, out_idx, st), "decode");
+  if (out_n_unique)
+    MOL_TRY_HIP(hipMemcpyAsync(out_n_unique, nu, sizeof(int32_t) * prob->B, hipMemcpyDeviceToDevice, st),
+                "copy n_unique");
+  return MOL_OK;
+}
+
+int mol_avg_embed(const mol_problem* prob, void* q_avg, void* x_avg, void* stream) {
+  int rc;
+  if ((rc = check_problem(prob, false))) return rc;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  MOL_TRY_HIP(launch_avg_embed(dev_prob(prob), q_avg, x_avg, st), "avg embed");
+  return MOL_OK;
+}
+
+}  // extern "C"

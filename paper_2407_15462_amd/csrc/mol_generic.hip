@@ -1,0 +1,390 @@
+// Generic gfx950 kernels of the MoL library: one thread per (query, item)
+// pair, float32 arithmetic, any supported shape and both storage types.
+// They serve the float32 problems and every shape the MFMA kernels do not
+// cover, and provide the selection machinery (segmented bitonic top-k,
+// key decoding), the candidate deduplication of the approximate path and
+// the TopKAvg materialisation.
+#include "mol_kernels.h"
+
+namespace mol {
+
+// ---------------------------------------------------------------------------
+// MoL score of one (query, item) pair, float32 (Eq. 1 with the two-layer
+// SiLU gating MLP of Appendix A.3).  Gating weights live in LDS as float32:
+// sW1 [H][P], sW2 [P][H], sb1 [H], sc [P] = a_q[b] + b2.
+// ---------------------------------------------------------------------------
+template <typename T, int PMAX>
+__device__ __forceinline__ void pair_dots(const DevProb& pr, int b, long n, float (&s)[PMAX]) {
+  const T* Qb = static_cast<const T*>(pr.Q) + static_cast<long>(b) * pr.Pq * pr.d;
+  const T* Xn = static_cast<const T*>(pr.X) + n * pr.d;
+  const long xstride = static_cast<long>(pr.N) * pr.d;
+#pragma unroll
+  for (int p = 0; p < PMAX; ++p) {
+    s[p] = 0.f;
+    if (p < pr.P) {
+      const int pq = p / pr.Px, px = p - (p / pr.Px) * pr.Px;
+      const T* q = Qb + pq * pr.d;
+      const T* x = Xn + px * xstride;
+      float acc = 0.f;
+      for (int t = 0; t < pr.d; ++t) acc = fmaf(to_f32(q[t]), to_f32(x[t]), acc);
+      s[p] = acc;
+    }
+  }
+}
+
+template <int PMAX>
+__device__ __forceinline__ float pair_phi(const DevProb& pr, long n, const float (&s)[PMAX],
+                                          const float* sW1, const float* sW2,
+                                          const float* sb1, const float* sc) {
+  const int P = pr.P, H = pr.H;
+  float l[PMAX];
+#pragma unroll
+  for (int p = 0; p < PMAX; ++p) l[p] = (p < P) ? sc[p] + pr.a_x[n * P + p] : 0.f;
+  for (int j = 0; j < H; ++j) {
+    float u = sb1[j];
+#pragma unroll
+    for (int p = 0; p < PMAX; ++p)
+      if (p < P) u = fmaf(sW1[j * P + p], s[p], u);
+    const float h = u / (1.f + expf(-u));
+#pragma unroll
+    for (int p = 0; p < PMAX; ++p)
+      if (p < P) l[p] = fmaf(sW2[p * H + j], h, l[p]);
+  }
+  float m = l[0];
+#pragma unroll
+  for (int p = 1; p < PMAX; ++p)
+    if (p < P) m = fmaxf(m, l[p]);
+  float den = 0.f, num = 0.f;
+#pragma unroll
+  for (int p = 0; p < PMAX; ++p) {
+    if (p < P) {
+      const float w = expf(l[p] - m);
+      den += w;
+      num = fmaf(w, s[p], num);
+    }
+  }
+  return num / den;
+}
+
+// Grid: x over items (256 per block), y over queries.  Items are either the
+// contiguous range n_begin .. n_begin+n_count-1 or, when `items` is given,
+// items[b*item_stride + i] for i < item_count[b].  Writes phi (float32) and/or
+// sort keys; key slots past a query's item count are cleared to 0 (empty).
+template <typename T, int PMAX>
+__global__ __launch_bounds__(256) void k_phi_generic(
+    DevProb pr, int n_begin, int n_count, const int32_t* __restrict__ items,
+    const int32_t* __restrict__ item_count, long item_stride, float* __restrict__ phi,
+    long phi_stride, uint64_t* __restrict__ keys, long key_stride) {
+  extern __shared__ float smem[];
+  const int P = pr.P, H = pr.H;
+  float* sW1 = smem;
+  float* sW2 = sW1 + H * P;
+  float* sb1 = sW2 + P * H;
+  float* sc = sb1 + H;
+  const int b = blockIdx.y;
+  for (int i = threadIdx.x; i < H * P; i += blockDim.x) {
+    sW1[i] = to_f32(static_cast<const T*>(pr.W1)[i]);
+    sW2[i] = to_f32(static_cast<const T*>(pr.W2)[i]);
+  }
+  for (int i = threadIdx.x; i < H; i += blockDim.x) sb1[i] = pr.b1[i];
+  for (int i = threadIdx.x; i < P; i += blockDim.x) sc[i] = pr.a_q[static_cast<long>(b) * P + i] + pr.b2[i];
+  __syncthreads();
+
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n_count) return;
+  const int cnt = items ? item_count[b] : n_count;
+  if (i >= cnt) {
+    if (keys) keys[b * key_stride + i] = 0;
+    return;
+  }
+  const long n = items ? static_cast<long>(items[b * item_stride + i]) : static_cast<long>(n_begin) + i;
+  float s[PMAX];
+  pair_dots<T, PMAX>(pr, b, n, s);
+  const float v = pair_phi<PMAX>(pr, n, s, sW1, sW2, sb1, sc);
+  if (phi) phi[b * phi_stride + i] = v;
+  if (keys) keys[b * key_stride + i] = make_key(v, static_cast<int32_t>(n));
+}
+
+// Per-component dot products as sort keys, rows r = b * P + p
+// (TopKDotProduct for every component).  Grid: x over items, y over queries.
+template <typename T, int PMAX>
+__global__ __launch_bounds__(256) void k_dots_generic(DevProb pr, int n_begin, int n_count,
+                                                      uint64_t* __restrict__ keys, long key_stride) {
+  const int b = blockIdx.y;
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n_count) return;
+  const long n = static_cast<long>(n_begin) + i;
+  float s[PMAX];
+  pair_dots<T, PMAX>(pr, b, n, s);
+#pragma unroll
+  for (int p = 0; p < PMAX; ++p)
+    if (p < pr.P) keys[(static_cast<long>(b) * pr.P + p) * key_stride + i] = make_key(s[p], static_cast<int32_t>(n));
+}
+
+// ---------------------------------------------------------------------------
+// Segmented top-k: block (seg, row) sorts keys in[row][seg*S .. seg*S+S) in
+// LDS (bitonic, descending; missing slots are empty keys) and writes the
+// first k to out[row][seg*k ..].
+// ---------------------------------------------------------------------------
+template <int S, int NT>
+__global__ __launch_bounds__(NT) void k_segment_topk(const uint64_t* __restrict__ in, long in_stride,
+                                                     int L, int k, uint64_t* __restrict__ out,
+                                                     long out_stride) {
+  __shared__ uint64_t sk[S];
+  const long row = blockIdx.y;
+  const long base = static_cast<long>(blockIdx.x) * S;
+  const uint64_t* src = in + row * in_stride + base;
+  const int len = static_cast<int>(min(static_cast<long>(S), static_cast<long>(L) - base));
+  for (int t = threadIdx.x; t < S; t += NT) sk[t] = t < len ? src[t] : 0ull;
+  __syncthreads();
+  for (int size = 2; size <= S; size <<= 1) {
+    for (int stride = size >> 1; stride > 0; stride >>= 1) {
+      for (int i = threadIdx.x; i < S / 2; i += NT) {
+        const int lo = 2 * i - (i & (stride - 1));
+        const int hi = lo + stride;
+        const bool desc = (lo & size) == 0;
+        const uint64_t a = sk[lo], c = sk[hi];
+        if ((a < c) == desc) {
+          sk[lo] = c;
+          sk[hi] = a;
+        }
+      }
+      __syncthreads();
+    }
+  }
+  uint64_t* dst = out + row * out_stride + static_cast<long>(blockIdx.x) * k;
+  for (int t = threadIdx.x; t < k; t += NT) dst[t] = sk[t];
+}
+
+__global__ void k_decode_keys(const uint64_t* __restrict__ keys, long key_stride, int rows, int k,
+                              float* __restrict__ score, int32_t* __restrict__ idx) {
+  const long i = static_cast<long>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (i >= static_cast<long>(rows) * k) return;
+  const long r = i / k, j = i - (i / k) * k;
+  const uint64_t key = keys[r * key_stride + j];
+  if (score) score[i] = key_score(key);
+  if (idx) idx[i] = key_item(key);
+}
+
+__global__ void k_fill_u64(uint64_t* __restrict__ p, long n, uint64_t v) {
+  const long i = static_cast<long>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (i < n) p[i] = v;
+}
+
+// Copy rows of k keys into a strided destination (the running top-k list is
+// appended to the next tile's keys).
+__global__ void k_copy_rows(const uint64_t* __restrict__ src, long src_stride, int rows, int k,
+                            uint64_t* __restrict__ dst, long dst_stride) {
+  const long i = static_cast<long>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (i >= static_cast<long>(rows) * k) return;
+  const long r = i / k, j = i - (i / k) * k;
+  dst[r * dst_stride + j] = src[r * src_stride + j];
+}
+
+// ---------------------------------------------------------------------------
+// Candidate union + dedup (the deduplicated set G of Algorithm 2): one block
+// per query inserts its C candidate ids into an LDS open-addressing hash set
+// (linear probing, capacity a power of two >= 1.5 C) and appends each id the
+// first time it is seen.  Ids outside [0, N) are empty slots.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(1024) void k_dedup(const int32_t* __restrict__ cand, int C, int N,
+                                                int cap_log2, int32_t* __restrict__ uniq,
+                                                int32_t* __restrict__ n_unique) {
+  extern __shared__ int32_t table[];
+  __shared__ int count;
+  const int cap = 1 << cap_log2;
+  const long b = blockIdx.x;
+  for (int i = threadIdx.x; i < cap; i += blockDim.x) table[i] = -1;
+  if (threadIdx.x == 0) count = 0;
+  __syncthreads();
+  for (int i = threadIdx.x; i < C; i += blockDim.x) {
+    const int32_t id = cand[b * C + i];
+    if (id < 0 || id >= N) continue;
+    uint32_t h = (static_cast<uint32_t>(id) * 0x9E3779B1u) >> (32 - cap_log2);
+    for (int probe = 0; probe < cap; ++probe) {
+      const int32_t prev = atomicCAS(&table[h], -1, id);
+      if (prev == -1) {
+        const int pos = atomicAdd(&count, 1);
+        uniq[b * C + pos] = id;
+        break;
+      }
+      if (prev == id) break;
+      h = (h + 1) & (cap - 1);
+    }
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) n_unique[b] = count;
+}
+
+// ---------------------------------------------------------------------------
+// TopKAvg materialisation: out[m][t] = round(sum_c in[c*sc + m*sm + t]),
+// summed in float64, rounded once (nearest-even).
+// ---------------------------------------------------------------------------
+template <typename T>
+__global__ void k_avg_embed(const T* __restrict__ in, long sc, long sm, int ncomp, long M, int d,
+                            T* __restrict__ out) {
+  const long i = static_cast<long>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (i >= M * d) return;
+  const long m = i / d, t = i - (i / d) * d;
+  double acc = 0.0;
+  for (int c = 0; c < ncomp; ++c) acc += static_cast<double>(to_f32(in[c * sc + m * sm + t]));
+  if constexpr (sizeof(T) == 2)
+    out[i] = f64_to_bf16_rne(acc);
+  else
+    out[i] = static_cast<float>(acc);
+}
+
+// ---------------------------------------------------------------------------
+// Host-side launchers.
+// ---------------------------------------------------------------------------
+static size_t phi_smem_bytes(const DevProb& pr) {
+  return sizeof(float) * (2 * static_cast<size_t>(pr.H) * pr.P + pr.H + pr.P);
+}
+
+template <typename T, int PMAX>
+static hipError_t launch_phi_t(const DevProb& pr, int n_begin, int n_count, const int32_t* items,
+                               const int32_t* item_count, long item_stride, float* phi,
+                               long phi_stride, uint64_t* keys, long key_stride, hipStream_t st) {
+  const size_t smem = phi_smem_bytes(pr);
+  if (smem > 65536) {
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_phi_generic<T, PMAX>),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize,
+                                       static_cast<int>(smem));
+    if (e != hipSuccess) return e;
+  }
+  dim3 grid((n_count + 255) / 256, pr.B);
+  hipLaunchKernelGGL((k_phi_generic<T, PMAX>), grid, dim3(256), smem, st, pr, n_begin, n_count,
+                     items, item_count, item_stride, phi, phi_stride, keys, key_stride);
+  return hipGetLastError();
+}
+
+template <typename T>
+static hipError_t launch_phi_p(const DevProb& pr, int n_begin, int n_count, const int32_t* items,
+                               const int32_t* item_count, long item_stride, float* phi,
+                               long phi_stride, uint64_t* keys, long key_stride, hipStream_t st) {
+  if (pr.P <= 4)
+    return launch_phi_t<T, 4>(pr, n_begin, n_count, items, item_count, item_stride, phi, phi_stride, keys, key_stride, st);
+  if (pr.P <= 16)
+    return launch_phi_t<T, 16>(pr, n_begin, n_count, items, item_count, item_stride, phi, phi_stride, keys, key_stride, st);
+  return launch_phi_t<T, 64>(pr, n_begin, n_count, items, item_count, item_stride, phi, phi_stride, keys, key_stride, st);
+}
+
+hipError_t launch_phi_generic(const DevProb& pr, int n_begin, int n_count, const int32_t* items,
+                              const int32_t* item_count, long item_stride, float* phi,
+                              long phi_stride, uint64_t* keys, long key_stride, hipStream_t st) {
+  if (n_count <= 0) return hipSuccess;
+  if (pr.dtype == MOL_BF16)
+    return launch_phi_p<bf16_t>(pr, n_begin, n_count, items, item_count, item_stride, phi, phi_stride, keys, key_stride, st);
+  return launch_phi_p<float>(pr, n_begin, n_count, items, item_count, item_stride, phi, phi_stride, keys, key_stride, st);
+}
+
+template <typename T>
+static hipError_t launch_dots_t(const DevProb& pr, int n_begin, int n_count, uint64_t* keys,
+                                long key_stride, hipStream_t st) {
+  dim3 grid((n_count + 255) / 256, pr.B);
+  if (pr.P <= 4)
+    hipLaunchKernelGGL((k_dots_generic<T, 4>), grid, dim3(256), 0, st, pr, n_begin, n_count, keys, key_stride);
+  else if (pr.P <= 16)
+    hipLaunchKernelGGL((k_dots_generic<T, 16>), grid, dim3(256), 0, st, pr, n_begin, n_count, keys, key_stride);
+  else
+    hipLaunchKernelGGL((k_dots_generic<T, 64>), grid, dim3(256), 0, st, pr, n_begin, n_count, keys, key_stride);
+  return hipGetLastError();
+}
+
+hipError_t launch_dots_generic(const DevProb& pr, int n_begin, int n_count, uint64_t* keys,
+                               long key_stride, hipStream_t st) {
+  if (n_count <= 0) return hipSuccess;
+  if (pr.dtype == MOL_BF16) return launch_dots_t<bf16_t>(pr, n_begin, n_count, keys, key_stride, st);
+  return launch_dots_t<float>(pr, n_begin, n_count, keys, key_stride, st);
+}
+
+int segment_size_for(int L, int k) {
+  // One segment when it fits, else the largest segment (always >= 4k so
+  // every pass shrinks the rows).
+  if (L <= 256 && k <= 256) return 256;
+  if (L <= 1024 && k <= 1024) return 1024;
+  return 4096;
+}
+
+hipError_t launch_segment_topk(const uint64_t* in, long in_stride, int rows, int L, int k,
+                               uint64_t* out, long out_stride, hipStream_t st) {
+  const int S = segment_size_for(L, k);
+  dim3 grid((L + S - 1) / S, rows);
+  if (S == 256)
+    hipLaunchKernelGGL((k_segment_topk<256, 128>), grid, dim3(128), 0, st, in, in_stride, L, k, out, out_stride);
+  else if (S == 1024)
+    hipLaunchKernelGGL((k_segment_topk<1024, 512>), grid, dim3(512), 0, st, in, in_stride, L, k, out, out_stride);
+  else
+    hipLaunchKernelGGL((k_segment_topk<4096, 1024>), grid, dim3(1024), 0, st, in, in_stride, L, k, out, out_stride);
+  return hipGetLastError();
+}
+
+hipError_t launch_decode(const uint64_t* keys, long key_stride, int rows, int k, float* score,
+                         int32_t* idx, hipStream_t st) {
+  const long n = static_cast<long>(rows) * k;
+  hipLaunchKernelGGL(k_decode_keys, dim3((n + 255) / 256), dim3(256), 0, st, keys, key_stride, rows, k, score, idx);
+  return hipGetLastError();
+}
+
+hipError_t launch_fill(uint64_t* p, long n, uint64_t v, hipStream_t st) {
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_fill_u64, dim3((n + 255) / 256), dim3(256), 0, st, p, n, v);
+  return hipGetLastError();
+}
+
+hipError_t launch_copy_rows(const uint64_t* src, long src_stride, int rows, int k, uint64_t* dst,
+                            long dst_stride, hipStream_t st) {
+  const long n = static_cast<long>(rows) * k;
+  hipLaunchKernelGGL(k_copy_rows, dim3((n + 255) / 256), dim3(256), 0, st, src, src_stride, rows, k, dst, dst_stride);
+  return hipGetLastError();
+}
+
+int dedup_cap_log2(int C) {
+  int lg = 1;
+  while ((1 << lg) < C + C / 2) ++lg;
+  return lg;
+}
+
+hipError_t launch_dedup(const int32_t* cand, int B, int C, int N, int32_t* uniq, int32_t* n_unique,
+                        hipStream_t st) {
+  const int lg = dedup_cap_log2(C);
+  const size_t smem = sizeof(int32_t) << lg;
+  if (smem > 65536) {
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_dedup),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize,
+                                       static_cast<int>(smem));
+    if (e != hipSuccess) return e;
+  }
+  hipLaunchKernelGGL(k_dedup, dim3(B), dim3(1024), smem, st, cand, C, N, lg, uniq, n_unique);
+  return hipGetLastError();
+}
+
+hipError_t launch_avg_embed(const DevProb& pr, void* q_avg, void* x_avg, hipStream_t st) {
+  const long nq = static_cast<long>(pr.B) * pr.d, nx = static_cast<long>(pr.N) * pr.d;
+  if (pr.dtype == MOL_BF16) {
+    if (q_avg)
+      hipLaunchKernelGGL((k_avg_embed<bf16_t>), dim3((nq + 255) / 256), dim3(256), 0, st,
+                         static_cast<const bf16_t*>(pr.Q), static_cast<long>(pr.d),
+                         static_cast<long>(pr.Pq) * pr.d, pr.Pq, static_cast<long>(pr.B), pr.d,
+                         static_cast<bf16_t*>(q_avg));
+    if (x_avg)
+      hipLaunchKernelGGL((k_avg_embed<bf16_t>), dim3((nx + 255) / 256), dim3(256), 0, st,
+                         static_cast<const bf16_t*>(pr.X), static_cast<long>(pr.N) * pr.d,
+                         static_cast<long>(pr.d), pr.Px, static_cast<long>(pr.N), pr.d,
+                         static_cast<bf16_t*>(x_avg));
+  } else {
+    if (q_avg)
+      hipLaunchKernelGGL((k_avg_embed<float>), dim3((nq + 255) / 256), dim3(256), 0, st,
+                         static_cast<const float*>(pr.Q), static_cast<long>(pr.d),
+                         static_cast<long>(pr.Pq) * pr.d, pr.Pq, static_cast<long>(pr.B), pr.d,
+                         static_cast<float*>(q_avg));
+    if (x_avg)
+      hipLaunchKernelGGL((k_avg_embed<float>), dim3((nx + 255) / 256), dim3(256), 0, st,
+                         static_cast<const float*>(pr.X), static_cast<long>(pr.N) * pr.d,
+                         static_cast<long>(pr.d), pr.Px, static_cast<long>(pr.N), pr.d,
+                         static_cast<float*>(x_avg));
+  }
+  return hipGetLastError();
+}
+
+}  // namespace mol

@@ -1,0 +1,31 @@
+// Host-side launchers of the gfx950 kernels (all asynchronous on `st`).
+#pragma once
+
+#include "mol_device.h"
+
+namespace mol {
+
+// Generic (one thread per pair, float32 arithmetic) kernels.
+hipError_t launch_phi_generic(const DevProb& pr, int n_begin, int n_count, const int32_t* items,
+                              const int32_t* item_count, long item_stride, float* phi,
+                              long phi_stride, uint64_t* keys, long key_stride, hipStream_t st);
+hipError_t launch_dots_generic(const DevProb& pr, int n_begin, int n_count, uint64_t* keys,
+                               long key_stride, hipStream_t st);
+
+// Selection machinery over 64-bit sort keys.
+int segment_size_for(int L, int k);
+hipError_t launch_segment_topk(const uint64_t* in, long in_stride, int rows, int L, int k,
+                               uint64_t* out, long out_stride, hipStream_t st);
+hipError_t launch_decode(const uint64_t* keys, long key_stride, int rows, int k, float* score,
+                         int32_t* idx, hipStream_t st);
+hipError_t launch_fill(uint64_t* p, long n, uint64_t v, hipStream_t st);
+hipError_t launch_copy_rows(const uint64_t* src, long src_stride, int rows, int k, uint64_t* dst,
+                            long dst_stride, hipStream_t st);
+
+// Approximate path helpers.
+int dedup_cap_log2(int C);
+hipError_t launch_dedup(const int32_t* cand, int B, int C, int N, int32_t* uniq, int32_t* n_unique,
+                        hipStream_t st);
+hipError_t launch_avg_embed(const DevProb& pr, void* q_avg, void* x_avg, hipStream_t st);
+
+}  // namespace mol

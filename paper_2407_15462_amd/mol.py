@@ -1,0 +1,217 @@
+"""ctypes binding of the MoL C ABI (include/mol.h).
+
+Argument marshalling only: every step of the retrieval path runs in the HIP
+kernels of libmol.so.  torch provides device memory and streams.  The
+functions carry the C names; the lower-case helpers at the bottom allocate
+outputs and workspace with torch and call them.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Tuple
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libmol.so")
+
+MOL_OK, MOL_EINVAL, MOL_EUNSUPPORTED, MOL_EWORKSPACE, MOL_EHIP = range(5)
+MOL_F32, MOL_BF16 = 0, 1
+MOL_OP_SCORE, MOL_OP_TOPK_EXACT, MOL_OP_TOPK_PER_EMBD, MOL_OP_RERANK = range(4)
+
+EXPORTS = ("mol_workspace_size", "mol_score", "mol_topk_exact", "mol_topk_per_embd",
+           "mol_rerank", "mol_avg_embed", "mol_status_str", "mol_last_error")
+
+
+class MolError(RuntimeError):
+    """A nonzero mol_status from the library."""
+
+    def __init__(self, status: int, message: str):
+        super().__init__(message)
+        self.status = status
+
+
+class MolProblemC(ctypes.Structure):
+    _fields_ = [("B", ctypes.c_int32), ("N", ctypes.c_int32), ("Pq", ctypes.c_int32),
+                ("Px", ctypes.c_int32), ("d", ctypes.c_int32), ("H", ctypes.c_int32),
+                ("dtype", ctypes.c_int32),
+                ("Q", ctypes.c_void_p), ("X", ctypes.c_void_p),
+                ("a_q", ctypes.c_void_p), ("a_x", ctypes.c_void_p),
+                ("W1", ctypes.c_void_p), ("b1", ctypes.c_void_p),
+                ("W2", ctypes.c_void_p), ("b2", ctypes.c_void_p)]
+
+
+_lib: Optional[ctypes.CDLL] = None
+
+
+def load(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Load libmol.so; raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is missing: build it with "
+                           "`python -m paper_2407_15462_amd.build` (there is no fallback)")
+    lib = ctypes.CDLL(path)
+    P = ctypes.POINTER(MolProblemC)
+    vp, i32, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_size_t
+    sig = {
+        "mol_workspace_size": [P, ctypes.c_int, i32, i32, i32, ctypes.POINTER(sz)],
+        "mol_score": [P, i32, i32, vp, vp],
+        "mol_topk_exact": [P, i32, vp, vp, vp, sz, vp],
+        "mol_topk_per_embd": [P, i32, vp, vp, vp, sz, vp],
+        "mol_rerank": [P, vp, i32, i32, vp, vp, vp, vp, sz, vp],
+        "mol_avg_embed": [P, vp, vp, vp],
+    }
+    for name, args in sig.items():
+        fn = getattr(lib, name)
+        fn.argtypes = args
+        fn.restype = ctypes.c_int
+    lib.mol_status_str.argtypes = [ctypes.c_int]
+    lib.mol_status_str.restype = ctypes.c_char_p
+    lib.mol_last_error.argtypes = []
+    lib.mol_last_error.restype = ctypes.c_char_p
+    _lib = lib
+    return lib
+
+
+def _check(status: int) -> None:
+    if status != MOL_OK:
+        lib = load()
+        raise MolError(status, f"{lib.mol_status_str(status).decode()}: "
+                               f"{lib.mol_last_error().decode()}")
+
+
+def _ptr(t: Optional[torch.Tensor]) -> Optional[int]:
+    if t is None:
+        return None
+    if not t.is_contiguous():
+        raise ValueError("tensors handed to the MoL library must be contiguous")
+    return t.data_ptr()
+
+
+def _stream(stream) -> Optional[int]:
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream
+    return stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+
+
+class Problem:
+    """A mol_problem built from torch tensors (kept alive by this object).
+
+    Q [B][Pq][d], X [Px][N][d] in bfloat16 or float32; a_q [B][P], a_x [N][P],
+    b1 [H], b2 [P] float32; W1 [H][P], W2 [P][H] in the embedding dtype.
+    Gating tensors may be None for mol_topk_per_embd.
+    """
+
+    def __init__(self, Q, X, a_q=None, a_x=None, W1=None, b1=None, W2=None, b2=None):
+        self.tensors = (Q, X, a_q, a_x, W1, b1, W2, b2)
+        if Q.dtype == torch.bfloat16:
+            dtype = MOL_BF16
+        elif Q.dtype == torch.float32:
+            dtype = MOL_F32
+        else:
+            raise ValueError(f"unsupported embedding dtype {Q.dtype}")
+        B, Pq, d = Q.shape
+        Px, N, d2 = X.shape
+        H = W1.shape[0] if W1 is not None else 1
+        self.c = MolProblemC(B, N, Pq, Px, d if d == d2 else -1, H, dtype,
+                             _ptr(Q), _ptr(X), _ptr(a_q), _ptr(a_x), _ptr(W1), _ptr(b1),
+                             _ptr(W2), _ptr(b2))
+        self.B, self.N, self.Pq, self.Px, self.d, self.H = B, N, Pq, Px, d, H
+        self.P = Pq * Px
+        self.device = Q.device
+
+    @classmethod
+    def from_inputs(cls, inp) -> "Problem":
+        return cls(inp.Q, inp.X, inp.a_q, inp.a_x, inp.W1, inp.b1, inp.W2, inp.b2)
+
+    @property
+    def ref(self):
+        return ctypes.byref(self.c)
+
+
+# ---------------------------------------------------------------- C entry points
+def mol_workspace_size(prob: Problem, op: int, k: int = 0, kprime: int = 0, C: int = 0) -> int:
+    out = ctypes.c_size_t(0)
+    _check(load().mol_workspace_size(prob.ref, op, k, kprime, C, ctypes.byref(out)))
+    return out.value
+
+
+def mol_score(prob: Problem, n_begin: int, n_count: int, phi: torch.Tensor, stream=None) -> None:
+    _check(load().mol_score(prob.ref, n_begin, n_count, _ptr(phi), _stream(stream)))
+
+
+def mol_topk_exact(prob: Problem, k: int, out_score, out_idx, ws, stream=None) -> None:
+    _check(load().mol_topk_exact(prob.ref, k, _ptr(out_score), _ptr(out_idx), _ptr(ws),
+                                 ws.numel() if ws is not None else 0, _stream(stream)))
+
+
+def mol_topk_per_embd(prob: Problem, kprime: int, out_dot, out_idx, ws, stream=None) -> None:
+    _check(load().mol_topk_per_embd(prob.ref, kprime, _ptr(out_dot), _ptr(out_idx), _ptr(ws),
+                                    ws.numel() if ws is not None else 0, _stream(stream)))
+
+
+def mol_rerank(prob: Problem, cand, C: int, k: int, out_score, out_idx, out_n_unique, ws,
+               stream=None) -> None:
+    _check(load().mol_rerank(prob.ref, _ptr(cand), C, k, _ptr(out_score), _ptr(out_idx),
+                             _ptr(out_n_unique), _ptr(ws), ws.numel() if ws is not None else 0,
+                             _stream(stream)))
+
+
+def mol_avg_embed(prob: Problem, q_avg, x_avg, stream=None) -> None:
+    _check(load().mol_avg_embed(prob.ref, _ptr(q_avg), _ptr(x_avg), _stream(stream)))
+
+
+# ------------------------------------------------- torch-allocating conveniences
+def workspace(prob: Problem, op: int, k: int = 0, kprime: int = 0, C: int = 0) -> torch.Tensor:
+    """A uint8 device buffer of the size the library asks for (>= 1 byte)."""
+    n = mol_workspace_size(prob, op, k, kprime, C)
+    return torch.empty(max(n, 1), dtype=torch.uint8, device=prob.device)
+
+
+def score(prob: Problem, n_begin: int = 0, n_count: Optional[int] = None, stream=None):
+    n_count = prob.N - n_begin if n_count is None else n_count
+    phi = torch.empty((prob.B, n_count), dtype=torch.float32, device=prob.device)
+    mol_score(prob, n_begin, n_count, phi, stream)
+    return phi
+
+
+def topk_exact(prob: Problem, k: int, ws=None, stream=None) -> Tuple[torch.Tensor, torch.Tensor]:
+    ws = workspace(prob, MOL_OP_TOPK_EXACT, k=k) if ws is None else ws
+    s = torch.empty((prob.B, k), dtype=torch.float32, device=prob.device)
+    i = torch.empty((prob.B, k), dtype=torch.int32, device=prob.device)
+    mol_topk_exact(prob, k, s, i, ws, stream)
+    return s, i
+
+
+def topk_per_embd(prob: Problem, kprime: int, ws=None, stream=None):
+    ws = workspace(prob, MOL_OP_TOPK_PER_EMBD, kprime=kprime) if ws is None else ws
+    s = torch.empty((prob.B, prob.P, kprime), dtype=torch.float32, device=prob.device)
+    i = torch.empty((prob.B, prob.P, kprime), dtype=torch.int32, device=prob.device)
+    mol_topk_per_embd(prob, kprime, s, i, ws, stream)
+    return s, i
+
+
+def rerank(prob: Problem, cand: torch.Tensor, k: int, ws=None, stream=None):
+    C = cand.shape[1]
+    ws = workspace(prob, MOL_OP_RERANK, k=k, C=C) if ws is None else ws
+    s = torch.empty((prob.B, k), dtype=torch.float32, device=prob.device)
+    i = torch.empty((prob.B, k), dtype=torch.int32, device=prob.device)
+    nu = torch.empty((prob.B,), dtype=torch.int32, device=prob.device)
+    mol_rerank(prob, cand, C, k, s, i, nu, ws, stream)
+    return s, i, nu
+
+
+def avg_embed(prob: Problem, stream=None) -> Tuple[torch.Tensor, torch.Tensor]:
+    dt = torch.bfloat16 if prob.c.dtype == MOL_BF16 else torch.float32
+    q = torch.empty((prob.B, prob.d), dtype=dt, device=prob.device)
+    x = torch.empty((prob.N, prob.d), dtype=dt, device=prob.device)
+    mol_avg_embed(prob, q, x, stream)
+    return q, x
+
+
+def averaged_problem(prob: Problem, q_avg: torch.Tensor, x_avg: torch.Tensor) -> Problem:
+    """The P = 1 problem TopKAvg runs on (Q = q', X = x')."""
+    return Problem(q_avg.view(prob.B, 1, prob.d), x_avg.view(1, prob.N, prob.d))

@@ -1,0 +1,49 @@
+"""Shared helpers for the GPU-vs-oracle parity tests."""
+from __future__ import annotations
+
+import sys
+
+import numpy as np
+import torch
+
+import synth
+from oracle import mol_oracle as mo
+
+TAU = 1e-4          # score tolerance and tie window (absolute)
+
+
+def log(msg: str) -> None:
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def oracle_problem(inp: synth.MolInputs) -> mo.Problem:
+    return mo.Problem.from_arrays(synth.to_numpy(inp))
+
+
+def check_scores(got: np.ndarray, want: np.ndarray, tol: float = TAU, what: str = "phi") -> None:
+    err = np.abs(got.astype(np.float64) - want)
+    i = np.unravel_index(np.argmax(err), err.shape)
+    assert err.max() <= tol, f"{what}: max |err| {err.max():.3e} at {i} (got {got[i]}, want {want[i]})"
+
+
+def check_topk_row(scores_all: np.ndarray, got_ids: np.ndarray, got_scores: np.ndarray, k: int,
+                   what: str) -> None:
+    """tau rule on ids, plus returned scores within TAU of the exact ones and
+    returned order (score desc, id asc)."""
+    ok, msg = mo.valid_topk(scores_all, got_ids, k, TAU)
+    assert ok, f"{what}: {msg}"
+    check_scores(got_scores, scores_all[got_ids], what=f"{what} scores")
+    s = got_scores.astype(np.float64)
+    for j in range(k - 1):
+        assert s[j] > s[j + 1] or (s[j] == s[j + 1] and got_ids[j] < got_ids[j + 1]), \
+            f"{what}: order broken at rank {j}"
+
+
+def recall(got_ids: np.ndarray, exact_ids: np.ndarray) -> float:
+    hits = sum(len(set(g.tolist()) & set(e.tolist())) for g, e in zip(got_ids, exact_ids))
+    return hits / exact_ids.size
+
+
+def cuda_inputs(spec: synth.Workload, seed: int = 0) -> synth.MolInputs:
+    return synth.generate(spec, seed=seed, device="cuda")

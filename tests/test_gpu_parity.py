@@ -1,0 +1,187 @@
+"""GPU parity: every entry point of the C ABI against the FP64 oracle on the
+same seeded inputs (MI355X only)."""
+import numpy as np
+import pytest
+import torch
+
+import synth
+from oracle import mol_oracle as mo
+from paper_2407_15462_amd import mol
+from parity_helpers import (TAU, check_scores, check_topk_row, cuda_inputs, log, oracle_problem,
+                            recall)
+
+pytestmark = pytest.mark.gpu
+
+W = synth.WORKLOADS
+
+
+def _cases_small():
+    # sizes the oracle finishes in seconds, spanning several tiles with a
+    # ragged tail
+    return [
+        ("tiny_exact_f32", W["tiny_exact_f32"]),
+        ("exact_32k_ragged", W["exact_32k"].scaled(B=37, N=5003, clusters=64)),
+        ("exact_1m_shape_ragged", W["exact_1m"].scaled(B=20, N=4099, clusters=64)),
+        ("hybrid_8m_shape_ragged", W["hybrid_8m"].scaled(B=9, N=3001, clusters=64)),
+    ]
+
+
+@pytest.mark.parametrize("name,spec", _cases_small(), ids=[c[0] for c in _cases_small()])
+def test_score_matches_oracle(name, spec):
+    log(f"[score] {name} B={spec.B} N={spec.N} P={spec.P} d={spec.d} H={spec.H} {spec.dtype}")
+    inp = cuda_inputs(spec, seed=11)
+    prob = mol.Problem.from_inputs(inp)
+    phi = mol.score(prob)
+    torch.cuda.synchronize()
+    want = mo.mol_scores(oracle_problem(inp), list(range(spec.B)))
+    check_scores(phi.cpu().numpy(), want)
+    # a sub-range of items
+    phi2 = mol.score(prob, n_begin=1001, n_count=777)
+    torch.cuda.synchronize()
+    check_scores(phi2.cpu().numpy(), want[:, 1001:1778])
+
+
+@pytest.mark.parametrize("name,spec", _cases_small(), ids=[c[0] for c in _cases_small()])
+def test_topk_exact_matches_oracle(name, spec):
+    k = min(spec.k, 100)
+    log(f"[topk_exact] {name} B={spec.B} N={spec.N} k={k}")
+    inp = cuda_inputs(spec, seed=12)
+    prob = mol.Problem.from_inputs(inp)
+    s, i = mol.topk_exact(prob, k)
+    torch.cuda.synchronize()
+    want = mo.mol_scores(oracle_problem(inp), list(range(spec.B)))
+    s, i = s.cpu().numpy(), i.cpu().numpy()
+    for b in range(spec.B):
+        check_topk_row(want[b], i[b], s[b], k, f"{name} query {b}")
+
+
+def test_topk_exact_full_32k_workload():
+    spec = W["exact_32k"]
+    log(f"[topk_exact] exact_32k full B={spec.B} N={spec.N}")
+    inp = cuda_inputs(spec, seed=0)
+    prob = mol.Problem.from_inputs(inp)
+    s, i = mol.topk_exact(prob, spec.k)
+    torch.cuda.synchronize()
+    queries = list(range(0, spec.B, 97))
+    want = mo.mol_scores(oracle_problem(inp), queries)
+    s, i = s.cpu().numpy(), i.cpu().numpy()
+    for r, b in enumerate(queries):
+        check_topk_row(want[r], i[b], s[b], spec.k, f"exact_32k query {b}")
+
+
+def test_topk_exact_k_equals_n_and_single_query():
+    spec = W["exact_32k"].scaled(B=1, N=300, clusters=8)
+    inp = cuda_inputs(spec, seed=13)
+    prob = mol.Problem.from_inputs(inp)
+    s, i = mol.topk_exact(prob, 300)
+    torch.cuda.synchronize()
+    want = mo.mol_scores(oracle_problem(inp), [0])[0]
+    check_topk_row(want, i.cpu().numpy()[0], s.cpu().numpy()[0], 300, "k=N")
+
+
+def test_duplicate_items_tie_to_lower_index():
+    spec = W["exact_32k"].scaled(B=3, N=2000, clusters=8)
+    inp = cuda_inputs(spec, seed=14)
+    # item 1500 becomes an exact copy of item 17 (embeddings and logits)
+    inp.X[:, 1500] = inp.X[:, 17]
+    inp.a_x[1500] = inp.a_x[17]
+    # make them the best item for query 0: copy query 0 from item 17
+    inp.Q[0] = inp.X[torch.arange(spec.Pq, device="cuda") % spec.Px, 17]
+    prob = mol.Problem.from_inputs(inp)
+    s, i = mol.topk_exact(prob, 10)
+    phi = mol.score(prob)
+    torch.cuda.synchronize()
+    row = i.cpu().numpy()[0].tolist()
+    assert 17 in row and 1500 in row
+    assert row.index(17) + 1 == row.index(1500)
+    assert phi[0, 17].item() == phi[0, 1500].item()
+
+
+@pytest.mark.parametrize("name,spec,kp", [
+    ("small_p32", W["exact_32k"].scaled(B=5, N=5003, clusters=32), 128),
+    ("small_p64", W["exact_1m"].scaled(B=3, N=4099, clusters=32), 128),
+    ("small_d128", W["hybrid_8m"].scaled(B=3, N=3001, clusters=32), 256),
+    ("f32", W["tiny_exact_f32"].scaled(B=4, N=2000), 50),
+])
+def test_topk_per_embd_matches_oracle(name, spec, kp):
+    log(f"[per_embd] {name} B={spec.B} N={spec.N} P={spec.P} k'={kp}")
+    inp = cuda_inputs(spec, seed=15)
+    prob = mol.Problem(inp.Q, inp.X)
+    dots, ids = mol.topk_per_embd(prob, kp)
+    torch.cuda.synchronize()
+    op = oracle_problem(inp)
+    dots, ids = dots.cpu().numpy(), ids.cpu().numpy()
+    for b in range(spec.B):
+        s = mo.all_dots(op, b)
+        for p in range(spec.P):
+            check_topk_row(s[:, p], ids[b, p], dots[b, p], kp, f"{name} b={b} p={p}")
+
+
+def test_avg_embed_bit_exact_and_topk_avg():
+    spec = W["hybrid_8m"].scaled(B=6, N=5000, clusters=32)
+    inp = cuda_inputs(spec, seed=16)
+    prob = mol.Problem.from_inputs(inp)
+    q, x = mol.avg_embed(prob)
+    torch.cuda.synchronize()
+    op = oracle_problem(inp)
+    qbar, xbar = mo.averaged_embeddings(op)
+    assert np.array_equal(q.view(torch.int16).cpu().numpy().view(np.uint16), qbar)
+    assert np.array_equal(x.view(torch.int16).cpu().numpy().view(np.uint16), xbar)
+    avg = mol.averaged_problem(prob, q, x)
+    dots, ids = mol.topk_per_embd(avg, 300)
+    torch.cuda.synchronize()
+    oavg = mo.averaged_problem(op)
+    for b in range(spec.B):
+        s = mo.all_dots(oavg, b)[:, 0]
+        check_topk_row(s, ids.cpu().numpy()[b, 0], dots.cpu().numpy()[b, 0], 300, f"avg b={b}")
+
+
+@pytest.mark.parametrize("C,k", [(700, 100), (64, 100), (4096, 100)])
+def test_rerank_matches_oracle(C, k):
+    spec = W["exact_1m"].scaled(B=7, N=3000, clusters=32)
+    log(f"[rerank] C={C} k={k}")
+    inp = cuda_inputs(spec, seed=17)
+    prob = mol.Problem.from_inputs(inp)
+    g = torch.Generator(device="cuda").manual_seed(5)
+    cand = torch.randint(-1, spec.N, (spec.B, C), device="cuda", generator=g, dtype=torch.int32)
+    cand[1] = 42                      # every slot the same id
+    cand[2, : C // 2] = -1            # half empty
+    cand[3, 0] = spec.N + 5           # out of range: treated as empty
+    s, i, nu = mol.rerank(prob, cand, k)
+    torch.cuda.synchronize()
+    op = oracle_problem(inp)
+    cand_np = cand.cpu().numpy().astype(np.int64)
+    cand_np[cand_np >= spec.N] = -1
+    s, i, nu = s.cpu().numpy(), i.cpu().numpy(), nu.cpu().numpy()
+    for b in range(spec.B):
+        uniq = mo.union_dedup([cand_np[b]])
+        assert nu[b] == len(uniq), f"n_unique query {b}: {nu[b]} vs {len(uniq)}"
+        _, _, phi = mo.mol_terms(op, b, uniq)
+        kk = min(k, len(uniq))
+        full = np.full(spec.N, -np.inf)
+        full[uniq] = phi
+        check_topk_row(full, i[b, :kk], s[b, :kk], kk, f"rerank query {b}")
+        assert np.all(i[b, kk:] == -1) and np.all(np.isneginf(s[b, kk:]))
+
+
+def test_worked_example_through_the_abi():
+    """Appendix B's example run through the library: exact top-2 {a, d},
+    TopKPerEmbedding(2) candidates {a, b, c}, rerank of those -> {a, b}."""
+    from test_oracle_pins import worked_example_problem
+    op, names, rows, expect = worked_example_problem()
+    dev = "cuda"
+    t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+    prob = mol.Problem(t(op.Qraw), t(op.X), t(op.a_q.astype(np.float32)), t(op.a_x),
+                       t(op.W1.astype(np.float32)), t(op.b1.astype(np.float32)),
+                       t(op.W2.astype(np.float32)), t(op.b2.astype(np.float32)))
+    s, i = mol.topk_exact(prob, 2)
+    dots, ids = mol.topk_per_embd(mol.Problem(prob.tensors[0], prob.tensors[1]), 2)
+    cand = ids.reshape(1, -1).contiguous()
+    rs, ri, nu = mol.rerank(prob, cand, 2)
+    torch.cuda.synchronize()
+    assert [names[j] for j in i.cpu().numpy()[0]] == expect["exact top-2"]
+    got_cand = sorted(set(ids.cpu().numpy().ravel().tolist()))
+    assert [names[j] for j in got_cand] == expect["TopKPerEmbedding(K'=2) candidates"]
+    assert nu.item() == 3
+    assert [names[j] for j in ri.cpu().numpy()[0]] == ["a", "b"]
+    assert abs(rs[0, 1].item() - float(expect["Theorem 2 S_K"][0])) < 1e-6
