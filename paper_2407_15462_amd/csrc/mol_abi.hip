@@ -164,6 +164,36 @@ RerankPlan plan_rerank(int B, int C, int k) {
   return r;
 }
 
+// Exact top-k through the fused kernel: partial lists [B][R][k] are reduced
+// to [B][k] by segmented sorts.
+struct FusedExactPlan {
+  StreamPlan s;  // offA = partial lists (stride R*k), offB = ping-pong
+  int R = 0, range_len = 0, G = 0;
+  size_t offFinal = 0, bytes = 0;
+};
+
+FusedExactPlan plan_fused_exact(const DevProb& pr, int k) {
+  FusedExactPlan f;
+  fused_grid(pr, pr.N, f.R, f.range_len, f.G);
+  StreamPlan& s = f.s;
+  s.rows = pr.B;
+  s.k = k;
+  const long L0 = static_cast<long>(f.R) * k;
+  const int S0 = segment_size_for(static_cast<int>(L0), k);
+  s.strideA = L0;
+  s.strideB = std::max<long>((L0 + S0 - 1) / S0 * k, k);
+  size_t off = 0;
+  s.offA = off;     off = align_up(off + 8ul * pr.B * s.strideA);
+  s.offB = off;     off = align_up(off + 8ul * pr.B * s.strideB);
+  f.offFinal = off; off = align_up(off + 8ul * pr.B * k);
+  f.bytes = off;
+  return f;
+}
+
+size_t exact_ws_bytes(const DevProb& pr, int k) {
+  return fused_supported(pr, k) ? plan_fused_exact(pr, k).bytes : plan_stream(pr.B, pr.N, k).bytes;
+}
+
 int check_ws(void* ws, size_t have, size_t need) {
   if (need == 0) return MOL_OK;
   if (!ws) return fail(MOL_EINVAL, "workspace is NULL (need %zu bytes)", need);
@@ -208,7 +238,7 @@ int mol_workspace_size(const mol_problem* prob, int op, int32_t k, int32_t kprim
     case MOL_OP_TOPK_EXACT:
       if ((rc = check_problem(prob, true))) return rc;
       if ((rc = check_k(k, prob->N, "k"))) return rc;
-      *bytes = plan_stream(prob->B, prob->N, k).bytes;
+      *bytes = exact_ws_bytes(dev_prob(prob), k);
       return MOL_OK;
     case MOL_OP_TOPK_PER_EMBD:
       if ((rc = check_problem(prob, false))) return rc;
@@ -235,6 +265,10 @@ int mol_score(const mol_problem* prob, int32_t n_begin, int32_t n_count, float* 
   if (!phi) return fail(MOL_EINVAL, "phi is NULL");
   hipStream_t st = static_cast<hipStream_t>(stream);
   const DevProb pr = dev_prob(prob);
+  if (fused_supported(pr, 1)) {
+    MOL_TRY_HIP(launch_fused_dense(pr, n_begin, n_count, phi, st), "mol_score (fused)");
+    return MOL_OK;
+  }
   MOL_TRY_HIP(launch_phi_generic(pr, n_begin, n_count, nullptr, nullptr, 0, phi, n_count, nullptr,
                                  0, st), "mol_score");
   return MOL_OK;
@@ -246,10 +280,21 @@ int mol_topk_exact(const mol_problem* prob, int32_t k, float* out_score, int32_t
   if ((rc = check_problem(prob, true))) return rc;
   if ((rc = check_k(k, prob->N, "k"))) return rc;
   if (!out_score || !out_idx) return fail(MOL_EINVAL, "output pointer is NULL");
-  const StreamPlan s = plan_stream(prob->B, prob->N, k);
-  if ((rc = check_ws(ws, ws_bytes, s.bytes))) return rc;
   hipStream_t st = static_cast<hipStream_t>(stream);
   const DevProb pr = dev_prob(prob);
+  if (fused_supported(pr, k)) {
+    const FusedExactPlan f = plan_fused_exact(pr, k);
+    if ((rc = check_ws(ws, ws_bytes, f.bytes))) return rc;
+    char* w = static_cast<char*>(ws);
+    uint64_t* partial = reinterpret_cast<uint64_t*>(w + f.s.offA);
+    uint64_t* fin = reinterpret_cast<uint64_t*>(w + f.offFinal);
+    MOL_TRY_HIP(launch_fused_topk(pr, k, f.R, f.range_len, f.G, partial, st), "fused MoL top-k");
+    if ((rc = reduce_rows(f.s, w, static_cast<long>(f.R) * k, fin, k, st))) return rc;
+    MOL_TRY_HIP(launch_decode(fin, k, prob->B, k, out_score, out_idx, st), "decode");
+    return MOL_OK;
+  }
+  const StreamPlan s = plan_stream(prob->B, prob->N, k);
+  if ((rc = check_ws(ws, ws_bytes, s.bytes))) return rc;
   auto tile = [&](int n0, int nt, uint64_t* A, long strideA) {
     return launch_phi_generic(pr, n0, nt, nullptr, nullptr, 0, nullptr, 0, A, strideA, st);
   };

@@ -29,3 +29,15 @@ hipError_t launch_dedup(const int32_t* cand, int B, int C, int N, int32_t* uniq,
 hipError_t launch_avg_embed(const DevProb& pr, void* q_avg, void* x_avg, hipStream_t st);
 
 }  // namespace mol
+
+namespace mol {
+
+// Fused MFMA scoring (bf16, Pq = 8; (Px, d, H) in {(8,64,64), (4,64,64), (4,128,128)}).
+bool fused_supported(const DevProb& pr, int k);
+void fused_grid(const DevProb& pr, int n_count, int& R, int& range_len, int& G);
+hipError_t launch_fused_topk(const DevProb& pr, int k, int R, int range_len, int G,
+                             uint64_t* partial, hipStream_t st);
+hipError_t launch_fused_dense(const DevProb& pr, int n_begin, int n_count, float* phi,
+                              hipStream_t st);
+
+}  // namespace mol

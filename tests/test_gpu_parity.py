@@ -1,5 +1,7 @@
 """GPU parity: every entry point of the C ABI against the FP64 oracle on the
 same seeded inputs (MI355X only)."""
+import dataclasses
+
 import numpy as np
 import pytest
 import torch
@@ -23,6 +25,8 @@ def _cases_small():
         ("exact_32k_ragged", W["exact_32k"].scaled(B=37, N=5003, clusters=64)),
         ("exact_1m_shape_ragged", W["exact_1m"].scaled(B=20, N=4099, clusters=64)),
         ("hybrid_8m_shape_ragged", W["hybrid_8m"].scaled(B=9, N=3001, clusters=64)),
+        # bf16 with P_q = 4: served by the generic kernels
+        ("bf16_pq4_generic", dataclasses.replace(W["exact_32k"], Pq=4, B=11, N=2100, clusters=16)),
     ]
 
 
@@ -85,8 +89,11 @@ def test_duplicate_items_tie_to_lower_index():
     # item 1500 becomes an exact copy of item 17 (embeddings and logits)
     inp.X[:, 1500] = inp.X[:, 17]
     inp.a_x[1500] = inp.a_x[17]
-    # make them the best item for query 0: copy query 0 from item 17
+    # make them the best item for query 0: copy query 0 from item 17 and give
+    # the matching components (px == pq mod Px) a large item gating logit
     inp.Q[0] = inp.X[torch.arange(spec.Pq, device="cuda") % spec.Px, 17]
+    for pq in range(spec.Pq):
+        inp.a_x[[17, 1500], pq * spec.Px + pq % spec.Px] = 4.0
     prob = mol.Problem.from_inputs(inp)
     s, i = mol.topk_exact(prob, 10)
     phi = mol.score(prob)
