@@ -145,15 +145,22 @@ struct RerankPlan {
   size_t offUniq = 0, offNu = 0, offFinal = 0, bytes = 0;
 };
 
-RerankPlan plan_rerank(int B, int C, int k) {
+RerankPlan plan_rerank(const DevProb& pr, int C, int k) {
+  const int B = pr.B;
   RerankPlan r;
   StreamPlan& s = r.s;
   s.rows = B;
   s.k = k;
   s.T = C;
-  const int S0 = segment_size_for(C, k);
-  s.strideA = std::max(C, k);
-  s.strideB = std::max<long>((C + S0 - 1) / S0 * k, k);
+  // generic path: keys of every candidate; fused path: per-chunk top-k lists
+  long L0 = C;
+  if (rerank_supported(pr, k)) {
+    const int chunk = rerank_chunk(C);
+    L0 = static_cast<long>((C + chunk - 1) / chunk) * k;
+  }
+  const int S0 = segment_size_for(static_cast<int>(L0), k);
+  s.strideA = std::max<long>(L0, k);
+  s.strideB = std::max<long>((L0 + S0 - 1) / S0 * k, k);
   size_t off = 0;
   s.offA = off;   off = align_up(off + 8ul * B * s.strideA);
   s.offB = off;   off = align_up(off + 8ul * B * s.strideB);
@@ -188,6 +195,39 @@ FusedExactPlan plan_fused_exact(const DevProb& pr, int k) {
   f.offFinal = off; off = align_up(off + 8ul * pr.B * k);
   f.bytes = off;
   return f;
+}
+
+// Per-component top-k' through the MFMA kernel: lists [P*B rows][R][KL]
+// are reduced to [rows][k'] by segmented sorts.
+struct PerEmbdPlan {
+  StreamPlan s;
+  int R = 0, range_len = 0, G = 0, KL = 0;
+  size_t offFinal = 0, offStg = 0, bytes = 0;
+};
+
+PerEmbdPlan plan_per_embd(const DevProb& pr, int kp) {
+  PerEmbdPlan f;
+  per_embd_grid(pr, f.R, f.range_len, f.G);
+  f.KL = per_embd_list_cap(kp);
+  StreamPlan& s = f.s;
+  s.rows = pr.B * pr.P;
+  s.k = kp;
+  const long L0 = static_cast<long>(f.R) * f.KL;
+  const int S0 = segment_size_for(static_cast<int>(L0), kp);
+  s.strideA = L0;
+  s.strideB = std::max<long>((L0 + S0 - 1) / S0 * kp, kp);
+  size_t off = 0;
+  s.offA = off;     off = align_up(off + 8ul * s.rows * s.strideA);
+  s.offB = off;     off = align_up(off + 8ul * s.rows * s.strideB);
+  f.offFinal = off; off = align_up(off + 8ul * s.rows * kp);
+  f.offStg = off;   off = align_up(off + 8ul * s.rows * f.R * per_embd_stage_cap());
+  f.bytes = off;
+  return f;
+}
+
+size_t per_embd_ws_bytes(const DevProb& pr, int kp) {
+  return per_embd_supported(pr, kp) ? plan_per_embd(pr, kp).bytes
+                                    : plan_stream(pr.B * pr.P, pr.N, kp).bytes;
 }
 
 size_t exact_ws_bytes(const DevProb& pr, int k) {
@@ -243,13 +283,13 @@ int mol_workspace_size(const mol_problem* prob, int op, int32_t k, int32_t kprim
     case MOL_OP_TOPK_PER_EMBD:
       if ((rc = check_problem(prob, false))) return rc;
       if ((rc = check_k(kprime, prob->N, "kprime"))) return rc;
-      *bytes = plan_stream(prob->B * prob->Pq * prob->Px, prob->N, kprime).bytes;
+      *bytes = per_embd_ws_bytes(dev_prob(prob), kprime);
       return MOL_OK;
     case MOL_OP_RERANK:
       if ((rc = check_problem(prob, true))) return rc;
       if (k < 1 || k > MOL_MAX_K) return fail(MOL_EINVAL, "k = %d outside [1, %d]", k, MOL_MAX_K);
       if (C < 1 || C > MOL_MAX_C) return fail(MOL_EINVAL, "C = %d outside [1, %d]", C, MOL_MAX_C);
-      *bytes = plan_rerank(prob->B, C, k).bytes;
+      *bytes = plan_rerank(dev_prob(prob), C, k).bytes;
       return MOL_OK;
     default:
       return fail(MOL_EINVAL, "unknown op %d", op);
@@ -308,10 +348,22 @@ int mol_topk_per_embd(const mol_problem* prob, int32_t kprime, float* out_dot, i
   if ((rc = check_k(kprime, prob->N, "kprime"))) return rc;
   if (!out_dot || !out_idx) return fail(MOL_EINVAL, "output pointer is NULL");
   const int rows = prob->B * prob->Pq * prob->Px;
-  const StreamPlan s = plan_stream(rows, prob->N, kprime);
-  if ((rc = check_ws(ws, ws_bytes, s.bytes))) return rc;
   hipStream_t st = static_cast<hipStream_t>(stream);
   const DevProb pr = dev_prob(prob);
+  if (per_embd_supported(pr, kprime)) {
+    const PerEmbdPlan f = plan_per_embd(pr, kprime);
+    if ((rc = check_ws(ws, ws_bytes, f.bytes))) return rc;
+    char* w = static_cast<char*>(ws);
+    uint64_t* lists = reinterpret_cast<uint64_t*>(w + f.s.offA);
+    uint64_t* fin = reinterpret_cast<uint64_t*>(w + f.offFinal);
+    uint64_t* stg = reinterpret_cast<uint64_t*>(w + f.offStg);
+    MOL_TRY_HIP(launch_per_embd(pr, kprime, f.R, f.range_len, f.G, lists, stg, st), "per-component top-k'");
+    if ((rc = reduce_rows(f.s, w, static_cast<long>(f.R) * f.KL, fin, kprime, st))) return rc;
+    MOL_TRY_HIP(launch_decode(fin, kprime, rows, kprime, out_dot, out_idx, st), "decode");
+    return MOL_OK;
+  }
+  const StreamPlan s = plan_stream(rows, prob->N, kprime);
+  if ((rc = check_ws(ws, ws_bytes, s.bytes))) return rc;
   auto tile = [&](int n0, int nt, uint64_t* A, long strideA) {
     return launch_dots_generic(pr, n0, nt, A, strideA, st);
   };
@@ -325,18 +377,25 @@ int mol_rerank(const mol_problem* prob, const int32_t* cand, int32_t C, int32_t 
   if (k < 1 || k > MOL_MAX_K) return fail(MOL_EINVAL, "k = %d outside [1, %d]", k, MOL_MAX_K);
   if (C < 1 || C > MOL_MAX_C) return fail(MOL_EINVAL, "C = %d outside [1, %d]", C, MOL_MAX_C);
   if (!cand || !out_score || !out_idx) return fail(MOL_EINVAL, "cand or output pointer is NULL");
-  const RerankPlan r = plan_rerank(prob->B, C, k);
+  const DevProb pr = dev_prob(prob);
+  const RerankPlan r = plan_rerank(pr, C, k);
   if ((rc = check_ws(ws, ws_bytes, r.bytes))) return rc;
   hipStream_t st = static_cast<hipStream_t>(stream);
   char* w = static_cast<char*>(ws);
-  const DevProb pr = dev_prob(prob);
   int32_t* uniq = reinterpret_cast<int32_t*>(w + r.offUniq);
   int32_t* nu = reinterpret_cast<int32_t*>(w + r.offNu);
   uint64_t* A = reinterpret_cast<uint64_t*>(w + r.s.offA);
   uint64_t* fin = reinterpret_cast<uint64_t*>(w + r.offFinal);
   MOL_TRY_HIP(launch_dedup(cand, prob->B, C, prob->N, uniq, nu, st), "dedup");
-  MOL_TRY_HIP(launch_phi_generic(pr, 0, C, uniq, nu, C, nullptr, 0, A, r.s.strideA, st), "rerank score");
-  if ((rc = reduce_rows(r.s, w, C, fin, k, st))) return rc;
+  if (rerank_supported(pr, k)) {
+    const int chunk = rerank_chunk(C);
+    const long L0 = static_cast<long>((C + chunk - 1) / chunk) * k;
+    MOL_TRY_HIP(launch_rerank(pr, uniq, nu, C, k, A, st), "fused rerank");
+    if ((rc = reduce_rows(r.s, w, L0, fin, k, st))) return rc;
+  } else {
+    MOL_TRY_HIP(launch_phi_generic(pr, 0, C, uniq, nu, C, nullptr, 0, A, r.s.strideA, st), "rerank score");
+    if ((rc = reduce_rows(r.s, w, C, fin, k, st))) return rc;
+  }
   MOL_TRY_HIP(launch_decode(fin, k, prob->B, k, out_score, out_idx, st), "decode");
   if (out_n_unique)
     MOL_TRY_HIP(hipMemcpyAsync(out_n_unique, nu, sizeof(int32_t) * prob->B, hipMemcpyDeviceToDevice, st),

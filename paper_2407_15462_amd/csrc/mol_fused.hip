@@ -1,144 +1,56 @@
 // Fused MoL scoring on gfx950 matrix cores (bf16 embeddings, P_q = 8).
 //
-// One wave scores 2 queries against 16 items per step through three chained
-// 16x16x32 MFMA products whose register layouts line up, so no accumulator
-// is re-laid-out through LDS (lane l: item column c = l % 16, group
-// g = l / 16):
+// One wave scores 2 queries against 16 items per step.  GEMM1 (bf16
+// 16x16x32) forms S[(q, pq)][item] = Q[q][pq] . X[px][item] for every px with
+// rows 8 q + pq, so a lane of group g = lane / 16 holds query g / 2 and
+// pq in {4 (g%2) .. 4 (g%2) + 3}.  One permlane32 swap per register pair then
+// hands each query's 64 dot products to all 64 lanes in the run layout of
+// mol_tile.h, whose chained f16 MFMAs evaluate the gating MLP, the softmax
+// and phi (Eq. 1 / Eq. 2 with the SiLU gating MLP of Appendix A.3) without
+// any LDS re-layout.
 //
-//   GEMM1 (bf16)  S[(q,pq)][item] = Q[q][pq] . X[px][item], one per px.
-//                 Rows 8 q + pq: a lane of group g holds query g/2, pq in
-//                 {4(g%2) .. 4(g%2)+3}, all px.  One permlane32 swap per
-//                 register pair then gives each query's 64 p values to all
-//                 64 lanes: lane (c, g) holds the contiguous run
-//                 p = base(g) + mu, mu < 2 Px, base(g) = (4(g%2) + 2(g/2)) Px.
-//   GEMM2 (f16)   U^T[j][item] = W1'[j][:] . s[:, item] + b1'[j]; the run
-//                 above is the B operand (K slot 8g + e <-> p = base(g)+8m+e).
-//   SiLU          h'_j = u'_j / (1 + 2^{u'_j}),  u' = -log2(e) u.
-//   GEMM3 (f16)   l'^T[p][item] = -W2[p][:] . h'[:, item]
-//                                 + log2(e) (a_x[item][p] + a_q[q][p] + b2[p]);
-//                 GEMM2's accumulators are the B operand up to a fixed
-//                 permutation of K (folded into the staged W2), and W2's
-//                 rows are ordered so each lane's logits are the p values
-//                 of its own s run.  a_x is the accumulator input; a_q + b2
-//                 enters as one extra K block split into f16 hi + lo.
-//   softmax, phi  w_p = 2^{l'_p}, phi = sum w_p s_p / sum w_p, s in f32,
-//                 summed over the 4 lanes of an item with two xor shuffles.
-//
-// (Eq. 1 / Eq. 2 of the paper with the two-layer SiLU gating MLP of its
-// Appendix A.3.)  Epilogues: a running per-query top-k (Definition 1) kept
-// in LDS with threshold rejection, or a dense phi store.
+// Epilogues: a running per-query top-k (Definition 1) kept in LDS with
+// threshold rejection, or a dense phi store.
 //
 // Workgroup: 8 waves (2 per SIMD) = 16 queries sharing an LDS-staged,
 // double-buffered stream of 32-item tiles loaded with direct global->LDS
 // copies.
-#include "mol_kernels.h"
+#include "mol_tile.h"
 
 namespace mol {
 
-typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
-typedef _Float16 f16x8_t __attribute__((ext_vector_type(8)));
-typedef float f32x4_t __attribute__((ext_vector_type(4)));
-typedef __attribute__((address_space(3))) void lds_void_t;
-typedef __attribute__((address_space(1))) void glb_void_t;
+using namespace tile;
 
-constexpr float kLog2e = 1.4426950408889634f;
-constexpr int kTopkList = 128;   // list capacity per query (k <= 128)
-constexpr int kTopkStage = 128;  // staging slots per query
+namespace {
+
 constexpr int kWaves = 8;
 constexpr int kQueriesPerWG = 2 * kWaves;
 constexpr int kTile = 32;        // items per LDS stage (two 16-item steps)
-
-__device__ __forceinline__ f32x4_t mfma_bf16(uint4 a, uint4 b, f32x4_t c) {
-  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a),
-                                                 __builtin_bit_cast(bf16x8_t, b), c, 0, 0, 0);
-}
-__device__ __forceinline__ f32x4_t mfma_f16(uint4 a, uint4 b, f32x4_t c) {
-  return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8_t, a),
-                                                __builtin_bit_cast(f16x8_t, b), c, 0, 0, 0);
-}
-__device__ __forceinline__ uint32_t pack_f16(float a, float b) {
-  return static_cast<uint32_t>(__builtin_bit_cast(uint16_t, static_cast<_Float16>(a))) |
-         (static_cast<uint32_t>(__builtin_bit_cast(uint16_t, static_cast<_Float16>(b))) << 16);
-}
-__device__ __forceinline__ uint32_t neg_bf16_to_f16_bits(bf16_t w, float scale) {
-  // f16 bits of -scale * w (sign flipped on the integer side)
-  const float v = scale * to_f32(static_cast<bf16_t>(w ^ 0x8000u));
-  return static_cast<uint32_t>(__builtin_bit_cast(uint16_t, static_cast<_Float16>(v)));
-}
-
-// Sum of x over the 4 lanes {c, c+16, c+32, c+48} (the 4 groups holding one
-// item), returned in all of them; VALU lane permutes only.
-__device__ __forceinline__ float sum_groups(float x) {
-  const uint32_t u = __float_as_uint(x);
-  auto a = __builtin_amdgcn_permlane16_swap(u, u, false, false);
-  const float y = __uint_as_float(a[0]) + __uint_as_float(a[1]);
-  const uint32_t v = __float_as_uint(y);
-  auto b = __builtin_amdgcn_permlane32_swap(v, v, false, false);
-  return __uint_as_float(b[0]) + __uint_as_float(b[1]);
-}
-__device__ __forceinline__ float max_groups(float x) {
-  const uint32_t u = __float_as_uint(x);
-  auto a = __builtin_amdgcn_permlane16_swap(u, u, false, false);
-  const float y = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
-  const uint32_t v = __float_as_uint(y);
-  auto b = __builtin_amdgcn_permlane32_swap(v, v, false, false);
-  return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
-}
-
-// LDS fence for exchanges between lanes of one wave.
-__device__ __forceinline__ void wave_lds_sync() {
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
-  __builtin_amdgcn_wave_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
-}
-
-// Bitonic sort (descending) of 256 keys held in LDS by one wave.
-__device__ __noinline__ void wave_sort256(uint64_t* r, int lane) {
-  for (int size = 2; size <= 256; size <<= 1) {
-    for (int stride = size >> 1; stride > 0; stride >>= 1) {
-#pragma unroll
-      for (int t = 0; t < 2; ++t) {
-        const int i = lane + 64 * t;
-        const int lo = 2 * i - (i & (stride - 1));
-        const int hi = lo + stride;
-        const bool desc = (lo & size) == 0;
-        const uint64_t a = r[lo], c = r[hi];
-        if ((a < c) == desc) {
-          r[lo] = c;
-          r[hi] = a;
-        }
-      }
-      wave_lds_sync();
-    }
-  }
-}
+constexpr int kRing = 3;         // item stages in flight
+constexpr int kTopkRegion = WaveTopk::kList + WaveTopk::kStage;
 
 template <int PX, int D, int H>
 struct FusedShape {
-  static constexpr int PQ = 8;
-  static constexpr int P = PQ * PX;
+  static constexpr int P = 8 * PX;
   static constexpr int RUN = 2 * PX;     // s values per lane per query
   static constexpr int KD = D / 32;      // K blocks of GEMM1
-  static constexpr int KP = P / 32;      // K blocks of GEMM2
-  static constexpr int JT = H / 16;      // output tiles of GEMM2
-  static constexpr int KH = H / 32;      // K blocks of GEMM3
   static constexpr int PT = P / 16;      // output tiles of GEMM3
   static constexpr int XROWCH = D / 8;   // 16-byte chunks per X row
   static constexpr int AROWCH = P / 4;   // 16-byte chunks per a_x row
   static constexpr int XSTAGE = PX * kTile * D * 2;   // bytes of one X stage
   static constexpr int ASTAGE = kTile * P * 4;        // bytes of one a_x stage
-  static constexpr int LDS_X = 2 * XSTAGE;
-  static constexpr int LDS_AX = 2 * ASTAGE;
+  static constexpr int LDS_X = kRing * XSTAGE;
+  static constexpr int LDS_AX = kRing * ASTAGE;
   static constexpr int LDS_CB = kQueriesPerWG * P * 4;
-  static constexpr int LDS_TOPK = kQueriesPerWG * (kTopkList + kTopkStage) * 8;
+  static constexpr int LDS_TOPK = kQueriesPerWG * kTopkRegion * 8;
   static constexpr int LDS_TOTAL = LDS_X + LDS_AX + LDS_CB + LDS_TOPK;
   // 16-byte global->LDS copies per stage, in 1 KB blocks of one wave each
   static constexpr int XBLOCKS = XSTAGE / 1024;
   static constexpr int ABLOCKS = ASTAGE / 1024;
   static_assert(XBLOCKS % kWaves == 0, "X stage must split evenly over the waves");
+  // fewest copies any wave issues per stage (a_x blocks may not split evenly)
+  static constexpr int LOADS = XBLOCKS / kWaves + ABLOCKS / kWaves;
 };
-
-__device__ __forceinline__ int lane_base(int g, int PX) { return (4 * (g & 1) + 2 * (g >> 1)) * PX; }
 
 // WG -> (item range, query group); WGs on one XCD (WG id mod 8) share item
 // ranges so that the corpus streams through each XCD's L2 once.
@@ -153,11 +65,14 @@ __device__ __forceinline__ void wg_coords(int g, int R, int G, int& r, int& qg) 
   }
 }
 
+}  // namespace
+
 template <int PX, int D, int H, bool DENSE>
 __global__ __launch_bounds__(64 * kWaves, 1) void k_mol_fused(
     DevProb pr, int k, int R, int range_len, int G, int n_begin, int n_end,
     uint64_t* __restrict__ partial, float* __restrict__ phi_out, long phi_stride) {
   using S = FusedShape<PX, D, H>;
+  using Mlp = MolMlp<PX, H>;
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   unsigned char* sX = smem;
   unsigned char* sAx = smem + S::LDS_X;
@@ -179,8 +94,6 @@ __global__ __launch_bounds__(64 * kWaves, 1) void k_mol_fused(
 
   const bf16_t* X = static_cast<const bf16_t*>(pr.X);
   const bf16_t* Q = static_cast<const bf16_t*>(pr.Q);
-  const bf16_t* W1 = static_cast<const bf16_t*>(pr.W1);
-  const bf16_t* W2 = static_cast<const bf16_t*>(pr.W2);
 
   // ---- stage tile t into LDS buffer buf with direct global->LDS copies ----
   // X stage layout [px][item][16-byte chunk ^ (item % XROWCH)], a_x stage
@@ -213,58 +126,20 @@ __global__ __launch_bounds__(64 * kWaves, 1) void k_mol_fused(
       __builtin_amdgcn_global_load_lds((glb_void_t*)src, (lds_void_t*)dst, 16, 0, 0);
     }
   };
-  if (ntiles > 0) stage(0, 0);
+  for (int t = 0; t < kRing - 1 && t < ntiles; ++t) stage(t, t);
 
   // ---- per-workgroup constants ----
   for (int i = tid; i < kQueriesPerWG * P; i += 64 * kWaves) {
     const int qi = i / P, p = i % P, b = qwg + qi;
-    const float v = b < pr.B ? kLog2e * (pr.a_q[static_cast<long>(b) * P + p] + pr.b2[p]) : 0.f;
-    const float hi = static_cast<float>(static_cast<_Float16>(v));
-    sCb[i] = pack_f16(hi, v - hi);
+    sCb[i] = split_f16(b < pr.B ? kLog2e * (pr.a_q[static_cast<long>(b) * P + p] + pr.b2[p]) : 0.f);
   }
-  uint64_t* myTop = sTop + wave * 2 * (kTopkList + kTopkStage);
-  if (!DENSE)
-    for (int i = lane; i < 2 * (kTopkList + kTopkStage); i += 64) myTop[i] = 0ull;
-
-  // W1' = -log2(e) W1 as GEMM2 A operands: row j, K slot 8g+e <-> p = base(g)+8m+e
-  uint4 w1op[S::JT][S::KP];
-#pragma unroll
-  for (int jt = 0; jt < S::JT; ++jt)
-#pragma unroll
-    for (int m = 0; m < S::KP; ++m) {
-      const bf16_t* src = W1 + (16 * jt + c) * P + base + 8 * m;
-      uint32_t w[4];
-#pragma unroll
-      for (int e = 0; e < 4; ++e)
-        w[e] = neg_bf16_to_f16_bits(src[2 * e], kLog2e) |
-               (neg_bf16_to_f16_bits(src[2 * e + 1], kLog2e) << 16);
-      w1op[jt][m] = make_uint4(w[0], w[1], w[2], w[3]);
-    }
-  // -W2 as GEMM3 A operands: row rho = 16 pt + c <-> p = base(c/4) + 4 pt + c%4;
-  // K slot 8g+e <-> j = 32 m + 16 (e/4) + 4 g + e%4
-  uint4 w2op[S::PT][S::KH];
-#pragma unroll
-  for (int pt = 0; pt < S::PT; ++pt)
-#pragma unroll
-    for (int m = 0; m < S::KH; ++m) {
-      const int p = lane_base(c >> 2, PX) + 4 * pt + (c & 3);
-      uint32_t w[4];
-#pragma unroll
-      for (int e2 = 0; e2 < 4; ++e2) {
-        const int e0 = 2 * e2, e1 = 2 * e2 + 1;
-        const int j0 = 32 * m + 16 * (e0 >> 2) + 4 * g + (e0 & 3);
-        const int j1 = 32 * m + 16 * (e1 >> 2) + 4 * g + (e1 & 3);
-        w[e2] = neg_bf16_to_f16_bits(W2[p * H + j0], 1.f) |
-                (neg_bf16_to_f16_bits(W2[p * H + j1], 1.f) << 16);
-      }
-      w2op[pt][m] = make_uint4(w[0], w[1], w[2], w[3]);
-    }
-  // b1' in the GEMM2 accumulator layout (row j = 16 jt + 4 g + i)
-  f32x4_t b1acc[S::JT];
-#pragma unroll
-  for (int jt = 0; jt < S::JT; ++jt)
-#pragma unroll
-    for (int i = 0; i < 4; ++i) b1acc[jt][i] = -kLog2e * pr.b1[16 * jt + 4 * g + i];
+  WaveTopk top[2];
+  if (!DENSE) {
+    top[0].init(sTop + (2 * wave + 0) * kTopkRegion, k, lane);
+    top[1].init(sTop + (2 * wave + 1) * kTopkRegion, k, lane);
+  }
+  Mlp mlp;
+  mlp.load(pr, c, g);
   // Q as GEMM1 A operands: row c = 8 q + pq, K slot 8g+e <-> d = 32 kk + 8 g + e
   uint4 qop[S::KD];
   {
@@ -275,28 +150,14 @@ __global__ __launch_bounds__(64 * kWaves, 1) void k_mol_fused(
                     ? *reinterpret_cast<const uint4*>(Q + (static_cast<long>(b) * 8 + pq) * D + 32 * kk + 8 * g)
                     : make_uint4(0, 0, 0, 0);
   }
-  // constant B operand of the a_q + b2 K block: ones in K slots 0 and 1
-  const uint4 ones = make_uint4(g == 0 ? 0x3C003C00u : 0u, 0u, 0u, 0u);
 
-  // running top-k state of the wave's 2 queries (wave-uniform)
-  uint64_t theta[2] = {0ull, 0ull};
-  int stg[2] = {0, 0};
-  auto merge = [&](int qb) {
-    uint64_t* reg = myTop + qb * (kTopkList + kTopkStage);
-    wave_lds_sync();
-    wave_sort256(reg, lane);
-    for (int i = kTopkList + lane; i < kTopkList + kTopkStage; i += 64) reg[i] = 0ull;
-    wave_lds_sync();
-    theta[qb] = reg[k - 1];
-    stg[qb] = 0;
-  };
-
-  __builtin_amdgcn_s_waitcnt(0);
+  // stage 0 complete; later stages' copies may still be in flight
+  if (ntiles >= kRing - 1) __builtin_amdgcn_s_waitcnt(waitcnt_vm((kRing - 2) * S::LOADS));
+  else __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
 
   for (int t = 0; t < ntiles; ++t) {
-    const int buf = t & 1;
-    if (t + 1 < ntiles) stage(t + 1, buf ^ 1);
+    const int buf = t % kRing;
     const unsigned char* xs = sX + buf * S::XSTAGE;
     const unsigned char* as = sAx + buf * S::ASTAGE;
 
@@ -342,107 +203,37 @@ __global__ __launch_bounds__(64 * kWaves, 1) void k_mol_fused(
         float s[S::RUN];
 #pragma unroll
         for (int mu = 0; mu < S::RUN; ++mu) s[mu] = qb == 0 ? s0[mu] : s1[mu];
-        // GEMM2
-        uint4 sop[S::KP];
-#pragma unroll
-        for (int m = 0; m < S::KP; ++m)
-          sop[m] = make_uint4(pack_f16(s[8 * m + 0], s[8 * m + 1]), pack_f16(s[8 * m + 2], s[8 * m + 3]),
-                              pack_f16(s[8 * m + 4], s[8 * m + 5]), pack_f16(s[8 * m + 6], s[8 * m + 7]));
-        f32x4_t u[S::JT];
-#pragma unroll
-        for (int jt = 0; jt < S::JT; ++jt) {
-          u[jt] = b1acc[jt];
-#pragma unroll
-          for (int m = 0; m < S::KP; ++m) u[jt] = mfma_f16(w1op[jt][m], sop[m], u[jt]);
-        }
-        // SiLU, packed as GEMM3 B operands: K slot 8g+e of block m <-> (jt, i) = (2m + e/4, e%4)
-        uint4 hop[S::KH];
-#pragma unroll
-        for (int m = 0; m < S::KH; ++m) {
-          float hv[8];
-#pragma unroll
-          for (int e = 0; e < 8; ++e) {
-            const float x = u[2 * m + (e >> 2)][e & 3];
-            hv[e] = x * __builtin_amdgcn_rcpf(1.f + __builtin_amdgcn_exp2f(x));
-          }
-          hop[m] = make_uint4(pack_f16(hv[0], hv[1]), pack_f16(hv[2], hv[3]), pack_f16(hv[4], hv[5]),
-                              pack_f16(hv[6], hv[7]));
-        }
-        // GEMM3 with the a_q + b2 block
-        f32x4_t lg[S::PT];
-#pragma unroll
-        for (int pt = 0; pt < S::PT; ++pt) {
-          const int p = lane_base(c >> 2, PX) + 4 * pt + (c & 3);
-          const uint32_t cb = g == 0 ? sCb[(2 * wave + qb) * P + p] : 0u;
-          lg[pt] = mfma_f16(make_uint4(cb, 0u, 0u, 0u), ones, axr[pt]);
-#pragma unroll
-          for (int m = 0; m < S::KH; ++m) lg[pt] = mfma_f16(w2op[pt][m], hop[m], lg[pt]);
-        }
-        // softmax over p and phi
-        float den = 0.f, num = 0.f;
+        uint32_t cb[S::PT];
 #pragma unroll
         for (int pt = 0; pt < S::PT; ++pt)
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const float w = __builtin_amdgcn_exp2f(lg[pt][i]);
-            den += w;
-            num = fmaf(w, s[4 * pt + i], num);
-          }
-        den = sum_groups(den);
-        num = sum_groups(num);
-        if (!__all(den >= 0x1p-60f && den <= 0x1p60f)) {
-          // logits far from zero: subtract the row maximum first
-          float mx = -__builtin_inff();
-#pragma unroll
-          for (int pt = 0; pt < S::PT; ++pt)
-#pragma unroll
-            for (int i = 0; i < 4; ++i) mx = fmaxf(mx, lg[pt][i]);
-          mx = max_groups(mx);
-          den = 0.f;
-          num = 0.f;
-#pragma unroll
-          for (int pt = 0; pt < S::PT; ++pt)
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-              const float w = __builtin_amdgcn_exp2f(lg[pt][i] - mx);
-              den += w;
-              num = fmaf(w, s[4 * pt + i], num);
-            }
-          den = sum_groups(den);
-          num = sum_groups(num);
-        }
-        const float phi = num * __builtin_amdgcn_rcpf(den);
+          cb[pt] = g == 0 ? sCb[(2 * wave + qb) * P + Mlp::aug_p(c, pt)] : 0u;
+        const float phi = mlp.phi(s, axr, cb);
         const int b = qwv + qb;
-
         if constexpr (DENSE) {
           if (g == 0 && item_ok && b < pr.B) phi_out[b * phi_stride + (item - n_begin)] = phi;
         } else {
-          const uint64_t key = (g == 0 && item_ok) ? make_key(phi, item) : 0ull;
-          const bool pass = key > theta[qb];
-          const uint64_t mask = __ballot(pass);
-          if (mask) {
-            uint64_t* reg = myTop + qb * (kTopkList + kTopkStage);
-            const int below = __popcll(mask & ((1ull << lane) - 1ull));
-            if (pass) reg[kTopkList + stg[qb] + below] = key;
-            stg[qb] += __popcll(mask);
-            if (stg[qb] > kTopkStage - 16) merge(qb);
-          }
+          top[qb].offer((g == 0 && item_ok) ? make_key(phi, item) : 0ull, lane);
         }
       }
     }
-    __builtin_amdgcn_s_waitcnt(0);
+    // refill the buffer read in iteration t-1, then wait for stage t+1
+    if (t + kRing - 1 < ntiles) {
+      stage(t + kRing - 1, (t + kRing - 1) % kRing);
+      __builtin_amdgcn_s_waitcnt(waitcnt_vm((kRing - 2) * S::LOADS));
+    } else {
+      __builtin_amdgcn_s_waitcnt(0);
+    }
     __syncthreads();
   }
 
   if constexpr (!DENSE) {
 #pragma unroll
     for (int qb = 0; qb < 2; ++qb) {
-      if (stg[qb] > 0) merge(qb);
+      top[qb].flush(lane);
       const int b = qwv + qb;
       if (b < pr.B) {
-        const uint64_t* reg = myTop + qb * (kTopkList + kTopkStage);
         uint64_t* dst = partial + (static_cast<long>(b) * R + r) * k;
-        for (int i = lane; i < k; i += 64) dst[i] = reg[i];
+        for (int i = lane; i < k; i += 64) dst[i] = top[qb].reg[i];
       }
     }
   }
@@ -454,7 +245,7 @@ bool fused_supported(const DevProb& pr, int k) {
   if (!((pr.Px == 4 && pr.d == 128 && pr.H == 128) || (pr.Px == 4 && pr.d == 64 && pr.H == 64) ||
         (pr.Px == 8 && pr.d == 64 && pr.H == 64)))
     return false;
-  return k <= kTopkList;
+  return k <= WaveTopk::kList;
 }
 
 void fused_grid(const DevProb& pr, int n_count, int& R, int& range_len, int& G) {

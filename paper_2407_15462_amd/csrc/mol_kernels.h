@@ -41,3 +41,26 @@ hipError_t launch_fused_dense(const DevProb& pr, int n_begin, int n_count, float
                               hipStream_t st);
 
 }  // namespace mol
+
+namespace mol {
+
+// Per-component top-k' with MFMA dots and LDS-staged threshold selection
+// (bf16, d in {64, 128}, k' <= 256).
+bool per_embd_supported(const DevProb& pr, int kp);
+int per_embd_list_cap(int kp);
+int per_embd_stage_cap();
+void per_embd_grid(const DevProb& pr, int& R, int& range_len, int& G);
+hipError_t launch_per_embd(const DevProb& pr, int kp, int R, int range_len, int G, uint64_t* lists,
+                           uint64_t* stg, hipStream_t st);
+
+}  // namespace mol
+
+namespace mol {
+
+// Fused MFMA rerank of deduplicated candidates (same shapes as the fused scorer).
+bool rerank_supported(const DevProb& pr, int k);
+int rerank_chunk(int C);
+hipError_t launch_rerank(const DevProb& pr, const int32_t* uniq, const int32_t* n_unique, int C, int k,
+                         uint64_t* partial, hipStream_t st);
+
+}  // namespace mol

@@ -1,0 +1,290 @@
+// MFMA building blocks shared by the fused MoL kernels (scoring, rerank):
+// the gating MLP + softmax + weighted sum for 16 items of one query held in
+// the 16x16x32 register layout described below.
+//
+// Lane l of a wave: item column c = l % 16, group g = l / 16.  For one query
+// the lane holds the component dot products s_p for the contiguous run
+// p = base(g) + mu, mu < 2 Px, base(g) = (4 (g%2) + 2 (g/2)) Px.  This is the
+// layout a 16x16x32 GEMM over rows (query, pq) produces after one permlane32
+// swap (see mol_fused.hip).
+//
+//   GEMM2 (f16)   U^T[j][item] = W1'[j][:] . s[:, item] + b1'[j]
+//                 s is the B operand: K slot 8g + e <-> p = base(g) + 8m + e.
+//   SiLU          h'_j = u'_j / (1 + 2^{u'_j}),  u' = -log2(e) u
+//   GEMM3 (f16)   l'^T[p][item] = -W2[p][:] . h'[:, item]
+//                                 + log2(e) (a_x[item][p] + a_q[q][p] + b2[p])
+//                 GEMM2's accumulators (row j = 16 jt + 4 g + i) are the B
+//                 operand with K slot 8g + e of block m <-> j = 32 m +
+//                 16 (e/4) + 4 g + e%4; W2's rows are ordered so that output
+//                 row 16 pt + 4 g + i is p = base(g) + 4 pt + i, the lane's
+//                 own s value.  a_x enters as the accumulator input; a_q + b2
+//                 as one extra K block holding it split into f16 hi + lo.
+//   softmax, phi  w_p = 2^{l'_p}, phi = sum w_p s_p / sum w_p (s in f32),
+//                 reduced over the 4 lanes of an item with permlane swaps.
+// (Eq. 1 / Eq. 2 with the two-layer SiLU gating MLP of Appendix A.3.)
+#pragma once
+
+#include "mol_kernels.h"
+
+namespace mol {
+namespace tile {
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) void lds_void_t;
+typedef __attribute__((address_space(1))) void glb_void_t;
+
+constexpr float kLog2e = 1.4426950408889634f;
+
+__device__ __forceinline__ f32x4_t mfma_bf16(uint4 a, uint4 b, f32x4_t c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a),
+                                                 __builtin_bit_cast(bf16x8_t, b), c, 0, 0, 0);
+}
+__device__ __forceinline__ f32x4_t mfma_f16(uint4 a, uint4 b, f32x4_t c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8_t, a),
+                                                __builtin_bit_cast(f16x8_t, b), c, 0, 0, 0);
+}
+__device__ __forceinline__ uint32_t pack_f16(float a, float b) {
+  return static_cast<uint32_t>(__builtin_bit_cast(uint16_t, static_cast<_Float16>(a))) |
+         (static_cast<uint32_t>(__builtin_bit_cast(uint16_t, static_cast<_Float16>(b))) << 16);
+}
+// f16 bits of -scale * w (sign flipped on the integer side)
+__device__ __forceinline__ uint32_t neg_bf16_to_f16_bits(bf16_t w, float scale) {
+  const float v = scale * to_f32(static_cast<bf16_t>(w ^ 0x8000u));
+  return static_cast<uint32_t>(__builtin_bit_cast(uint16_t, static_cast<_Float16>(v)));
+}
+// f16 hi + lo split of v, packed (hi in the low half)
+__device__ __forceinline__ uint32_t split_f16(float v) {
+  const float hi = static_cast<float>(static_cast<_Float16>(v));
+  return pack_f16(hi, v - hi);
+}
+
+// Sum / max of x over the 4 lanes {c, c+16, c+32, c+48}, in all of them.
+__device__ __forceinline__ float sum_groups(float x) {
+  const uint32_t u = __float_as_uint(x);
+  auto a = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+  const float y = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+  const uint32_t v = __float_as_uint(y);
+  auto b = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+  return __uint_as_float(b[0]) + __uint_as_float(b[1]);
+}
+__device__ __forceinline__ float max_groups(float x) {
+  const uint32_t u = __float_as_uint(x);
+  auto a = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+  const float y = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+  const uint32_t v = __float_as_uint(y);
+  auto b = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+  return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+}
+
+__device__ __forceinline__ int lane_base(int g, int PX) { return (4 * (g & 1) + 2 * (g >> 1)) * PX; }
+
+// s_waitcnt immediate that waits until at most n vector-memory operations
+// of this wave are outstanding (expcnt and lgkmcnt left unconstrained).
+// Vector-memory loads complete in issue order, so after issuing the loads
+// of later stages, vmcnt <= (their count) means every older load is done.
+constexpr int waitcnt_vm(int n) { return (n & 0xF) | ((n >> 4) << 14) | (0x7 << 4) | (0xF << 8); }
+
+// LDS fence for exchanges between lanes of one wave.
+__device__ __forceinline__ void wave_lds_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+}
+
+typedef __attribute__((address_space(3))) uint64_t lds_u64_t;
+
+// Bitonic sort (descending) of SORT keys in LDS by one wave.
+template <int SORT>
+__device__ __noinline__ void wave_sort(lds_u64_t* r, int lane) {
+  for (int size = 2; size <= SORT; size <<= 1) {
+    for (int stride = size >> 1; stride > 0; stride >>= 1) {
+#pragma unroll
+      for (int t = 0; t < SORT / 128; ++t) {
+        const int i = lane + 64 * t;
+        const int lo = 2 * i - (i & (stride - 1));
+        const int hi = lo + stride;
+        const bool desc = (lo & size) == 0;
+        const uint64_t a = r[lo], c = r[hi];
+        if ((a < c) == desc) {
+          r[lo] = c;
+          r[hi] = a;
+        }
+      }
+      wave_lds_sync();
+    }
+  }
+}
+
+// Running top-k of one query kept by one wave in LDS: list [0, 128) sorted
+// descending, staging [128, 256); keys below the threshold are rejected.
+struct WaveTopk {
+  static constexpr int kList = 128;
+  static constexpr int kStage = 128;
+  uint64_t* reg;
+  uint64_t theta;
+  int stg;
+  int k;
+  __device__ void init(uint64_t* region, int k_, int lane) {
+    reg = region;
+    theta = 0ull;
+    stg = 0;
+    k = k_;
+    for (int i = lane; i < kList + kStage; i += 64) reg[i] = 0ull;
+  }
+  __device__ void merge(int lane) {
+    wave_lds_sync();
+    wave_sort<kList + kStage>((lds_u64_t*)reg, lane);
+    for (int i = kList + lane; i < kList + kStage; i += 64) reg[i] = 0ull;
+    wave_lds_sync();
+    theta = reg[k - 1];
+    stg = 0;
+  }
+  // offer one key per lane (0 = none); at most 16 lanes offer per call
+  __device__ void offer(uint64_t key, int lane) {
+    const bool pass = key > theta;
+    const uint64_t mask = __ballot(pass);
+    if (mask) {
+      const int below = __popcll(mask & ((1ull << lane) - 1ull));
+      if (pass) reg[kList + stg + below] = key;
+      stg += __popcll(mask);
+      if (stg > kStage - 16) merge(lane);
+    }
+  }
+  __device__ void flush(int lane) {
+    if (stg > 0) merge(lane);
+  }
+};
+
+// Per-wave constants of the gating MLP in MFMA operand layouts.
+template <int PX, int H>
+struct MolMlp {
+  static constexpr int P = 8 * PX;
+  static constexpr int RUN = 2 * PX;
+  static constexpr int KP = P / 32;   // K blocks of GEMM2
+  static constexpr int JT = H / 16;   // output tiles of GEMM2
+  static constexpr int KH = H / 32;   // K blocks of GEMM3
+  static constexpr int PT = P / 16;   // output tiles of GEMM3
+  uint4 w1op[JT][KP];
+  uint4 w2op[PT][KH];
+  f32x4_t b1acc[JT];
+  uint4 ones;
+
+  __device__ void load(const DevProb& pr, int c, int g) {
+    const bf16_t* W1 = static_cast<const bf16_t*>(pr.W1);
+    const bf16_t* W2 = static_cast<const bf16_t*>(pr.W2);
+    const int base = lane_base(g, PX);
+    // W1' = -log2(e) W1: row j, K slot 8g+e <-> p = base(g) + 8m + e
+#pragma unroll
+    for (int jt = 0; jt < JT; ++jt)
+#pragma unroll
+      for (int m = 0; m < KP; ++m) {
+        const bf16_t* src = W1 + (16 * jt + c) * P + base + 8 * m;
+        uint32_t w[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          w[e] = neg_bf16_to_f16_bits(src[2 * e], kLog2e) |
+                 (neg_bf16_to_f16_bits(src[2 * e + 1], kLog2e) << 16);
+        w1op[jt][m] = make_uint4(w[0], w[1], w[2], w[3]);
+      }
+    // -W2: row 16 pt + c <-> p = base(c/4) + 4 pt + c%4; K slot 8g+e <-> j
+#pragma unroll
+    for (int pt = 0; pt < PT; ++pt)
+#pragma unroll
+      for (int m = 0; m < KH; ++m) {
+        const int p = lane_base(c >> 2, PX) + 4 * pt + (c & 3);
+        uint32_t w[4];
+#pragma unroll
+        for (int e2 = 0; e2 < 4; ++e2) {
+          const int e0 = 2 * e2, e1 = 2 * e2 + 1;
+          const int j0 = 32 * m + 16 * (e0 >> 2) + 4 * g + (e0 & 3);
+          const int j1 = 32 * m + 16 * (e1 >> 2) + 4 * g + (e1 & 3);
+          w[e2] = neg_bf16_to_f16_bits(W2[p * H + j0], 1.f) |
+                  (neg_bf16_to_f16_bits(W2[p * H + j1], 1.f) << 16);
+        }
+        w2op[pt][m] = make_uint4(w[0], w[1], w[2], w[3]);
+      }
+#pragma unroll
+    for (int jt = 0; jt < JT; ++jt)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) b1acc[jt][i] = -kLog2e * pr.b1[16 * jt + 4 * g + i];
+    ones = make_uint4(g == 0 ? 0x3C003C00u : 0u, 0u, 0u, 0u);
+  }
+
+  // p of GEMM3 A-operand row 16 pt + c (the a_q + b2 block's rows)
+  __device__ static int aug_p(int c, int pt) { return lane_base(c >> 2, PX) + 4 * pt + (c & 3); }
+
+  // phi for the lane's item.  s: the lane's run of s values; axr: log2(e) a_x
+  // in the GEMM3 accumulator layout; cb[pt]: packed f16 hi/lo of
+  // log2(e) (a_q + b2) at p = aug_p(c, pt) for group-0 lanes, 0 elsewhere.
+  __device__ float phi(const float (&s)[RUN], const f32x4_t (&axr)[PT], const uint32_t (&cb)[PT]) const {
+    uint4 sop[KP];
+#pragma unroll
+    for (int m = 0; m < KP; ++m)
+      sop[m] = make_uint4(pack_f16(s[8 * m + 0], s[8 * m + 1]), pack_f16(s[8 * m + 2], s[8 * m + 3]),
+                          pack_f16(s[8 * m + 4], s[8 * m + 5]), pack_f16(s[8 * m + 6], s[8 * m + 7]));
+    f32x4_t u[JT];
+#pragma unroll
+    for (int jt = 0; jt < JT; ++jt) {
+      u[jt] = b1acc[jt];
+#pragma unroll
+      for (int m = 0; m < KP; ++m) u[jt] = mfma_f16(w1op[jt][m], sop[m], u[jt]);
+    }
+    uint4 hop[KH];
+#pragma unroll
+    for (int m = 0; m < KH; ++m) {
+      float hv[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float x = u[2 * m + (e >> 2)][e & 3];
+        hv[e] = x * __builtin_amdgcn_rcpf(1.f + __builtin_amdgcn_exp2f(x));
+      }
+      hop[m] = make_uint4(pack_f16(hv[0], hv[1]), pack_f16(hv[2], hv[3]), pack_f16(hv[4], hv[5]),
+                          pack_f16(hv[6], hv[7]));
+    }
+    f32x4_t lg[PT];
+#pragma unroll
+    for (int pt = 0; pt < PT; ++pt) {
+      lg[pt] = mfma_f16(make_uint4(cb[pt], 0u, 0u, 0u), ones, axr[pt]);
+#pragma unroll
+      for (int m = 0; m < KH; ++m) lg[pt] = mfma_f16(w2op[pt][m], hop[m], lg[pt]);
+    }
+    float den = 0.f, num = 0.f;
+#pragma unroll
+    for (int pt = 0; pt < PT; ++pt)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float w = __builtin_amdgcn_exp2f(lg[pt][i]);
+        den += w;
+        num = fmaf(w, s[4 * pt + i], num);
+      }
+    den = sum_groups(den);
+    num = sum_groups(num);
+    if (!__all(den >= 0x1p-60f && den <= 0x1p60f)) {
+      // logits far from zero: subtract the row maximum first
+      float mx = -__builtin_inff();
+#pragma unroll
+      for (int pt = 0; pt < PT; ++pt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) mx = fmaxf(mx, lg[pt][i]);
+      mx = max_groups(mx);
+      den = 0.f;
+      num = 0.f;
+#pragma unroll
+      for (int pt = 0; pt < PT; ++pt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const float w = __builtin_amdgcn_exp2f(lg[pt][i] - mx);
+          den += w;
+          num = fmaf(w, s[4 * pt + i], num);
+        }
+      den = sum_groups(den);
+      num = sum_groups(num);
+    }
+    return num * __builtin_amdgcn_rcpf(den);
+  }
+};
+
+}  // namespace tile
+}  // namespace mol
