@@ -13,8 +13,9 @@
  * Memory: every array pointer below is a DEVICE pointer owned by the caller.
  * The library allocates no device memory, keeps no pointer after a call
  * returns, and holds no global state other than a per-thread last-error
- * string.  Calls are asynchronous on `stream` (a hipStream_t passed as
- * void*, NULL = the null stream); outputs are valid once the caller has
+ * string and the optional kernel-timing records (mol_timing_enable).
+ * Calls are asynchronous on `stream` (a hipStream_t passed as void*,
+ * NULL = the null stream); outputs are valid once the caller has
  * synchronised that stream.  Calls on different streams may run
  * concurrently as long as their outputs and workspaces do not overlap.
  *
@@ -126,8 +127,8 @@ int mol_topk_per_embd(const mol_problem *prob, int32_t kprime, float *out_dot,
 
 /* Candidate union, deduplication and MoL rerank (Algorithm 2,
  * BruteForceTopKMoL over the deduplicated candidate set G).
- * cand int32 [B][C]: item ids, duplicates allowed, any negative id marks
- * an empty slot; every non-negative id must be < N.  For each query the
+ * cand int32 [B][C]: item ids, duplicates allowed; an id outside [0, N)
+ * (e.g. -1) marks an empty slot and is skipped.  For each query the
  * distinct ids are scored with full MoL and the top-k kept.
  * out_score float32 [B][k], out_idx int32 [B][k] (padded with -INFINITY /
  * -1 when a query has fewer than k distinct ids), out_n_unique int32 [B]
@@ -145,6 +146,22 @@ int mol_rerank(const mol_problem *prob, const int32_t *cand, int32_t C,
  * left out.  Either output pointer may be NULL to skip it.  No workspace. */
 int mol_avg_embed(const mol_problem *prob, void *q_avg, void *x_avg,
                   void *stream);
+
+/* Kernel timing, a diagnostic for throughput measurements.
+ * mol_timing_enable(1) makes every later call record a pair of HIP events on
+ * its stream around its main kernel: the fused scoring kernel of mol_score,
+ * the scoring + per-range top-k scan of mol_topk_exact, the per-component
+ * scan of mol_topk_per_embd and the candidate scoring of mol_rerank
+ * (validation, merges of partial lists and decoding are outside the pair).
+ * mol_timing_enable(0) stops recording; records already taken stay.
+ * mol_timing_read(op, &ms, &n) waits for the recorded events of operation
+ * `op` (a mol_op code), writes their summed duration in milliseconds and
+ * their count, and clears them.  Process-wide and thread-safe; events are
+ * created on first use and reused, never freed; every recorded stream must
+ * belong to the device that is current when reading.  Returns MOL_EINVAL
+ * for an unknown op or NULL output, MOL_EHIP if an event wait fails. */
+int mol_timing_enable(int on);
+int mol_timing_read(int op, double *total_ms, int32_t *launches);
 
 /* Static description of a status code. */
 const char *mol_status_str(int status);

@@ -3,7 +3,10 @@
 #include <algorithm>
 #include <cstdarg>
 #include <cstdio>
+#include <mutex>
 #include <string>
+#include <utility>
+#include <vector>
 
 #include "mol_kernels.h"
 
@@ -31,6 +34,67 @@ int hip_fail(hipError_t e, const char* where) {
   do {                                         \
     hipError_t e_ = (expr);                    \
     if (e_ != hipSuccess) return hip_fail(e_, where); \
+  } while (0)
+
+// ---------------------------------------------------------------------------
+// Kernel timing: while enabled, event pairs recorded on the caller's stream
+// around each entry point's main kernel; read (and recycled) by
+// mol_timing_read.
+constexpr int kTimedOps = 4;                  // mol_op codes 0..3
+
+struct EvPair {
+  hipEvent_t a = nullptr, b = nullptr;
+};
+
+struct TimingLog {
+  std::mutex mu;
+  bool on = false;
+  std::vector<EvPair> rec[kTimedOps];
+  std::vector<EvPair> spare;
+};
+
+TimingLog& timing_log() {
+  static TimingLog t;
+  return t;
+}
+
+EvPair timing_start(hipStream_t st) {
+  TimingLog& t = timing_log();
+  std::lock_guard<std::mutex> g(t.mu);
+  EvPair p;
+  if (!t.on) return p;
+  if (!t.spare.empty()) {
+    p = t.spare.back();
+    t.spare.pop_back();
+  } else {
+    if (hipEventCreate(&p.a) != hipSuccess) return EvPair{};
+    if (hipEventCreate(&p.b) != hipSuccess) {
+      (void)hipEventDestroy(p.a);
+      return EvPair{};
+    }
+  }
+  if (hipEventRecord(p.a, st) != hipSuccess) {
+    t.spare.push_back(p);
+    return EvPair{};
+  }
+  return p;
+}
+
+void timing_stop(int op, const EvPair& p, hipStream_t st, bool launched) {
+  if (!p.a) return;
+  TimingLog& t = timing_log();
+  const bool ok = launched && hipEventRecord(p.b, st) == hipSuccess;
+  std::lock_guard<std::mutex> g(t.mu);
+  (ok ? t.rec[op] : t.spare).push_back(p);
+}
+
+// Launch `expr` (a hipError_t expression) between the events of `op`.
+#define MOL_TIMED_LAUNCH(op, st, expr, where)              \
+  do {                                                     \
+    const EvPair tp_ = timing_start(st);                   \
+    const hipError_t te_ = (expr);                         \
+    timing_stop((op), tp_, (st), te_ == hipSuccess);       \
+    MOL_TRY_HIP(te_, where);                               \
   } while (0)
 
 constexpr size_t kAlign = 256;
@@ -306,11 +370,12 @@ int mol_score(const mol_problem* prob, int32_t n_begin, int32_t n_count, float* 
   hipStream_t st = static_cast<hipStream_t>(stream);
   const DevProb pr = dev_prob(prob);
   if (fused_supported(pr, 1)) {
-    MOL_TRY_HIP(launch_fused_dense(pr, n_begin, n_count, phi, st), "mol_score (fused)");
+    MOL_TIMED_LAUNCH(MOL_OP_SCORE, st, launch_fused_dense(pr, n_begin, n_count, phi, st), "mol_score (fused)");
     return MOL_OK;
   }
-  MOL_TRY_HIP(launch_phi_generic(pr, n_begin, n_count, nullptr, nullptr, 0, phi, n_count, nullptr,
-                                 0, st), "mol_score");
+  MOL_TIMED_LAUNCH(MOL_OP_SCORE, st,
+                   launch_phi_generic(pr, n_begin, n_count, nullptr, nullptr, 0, phi, n_count, nullptr, 0, st),
+                   "mol_score");
   return MOL_OK;
 }
 
@@ -328,7 +393,8 @@ int mol_topk_exact(const mol_problem* prob, int32_t k, float* out_score, int32_t
     char* w = static_cast<char*>(ws);
     uint64_t* partial = reinterpret_cast<uint64_t*>(w + f.s.offA);
     uint64_t* fin = reinterpret_cast<uint64_t*>(w + f.offFinal);
-    MOL_TRY_HIP(launch_fused_topk(pr, k, f.R, f.range_len, f.G, partial, st), "fused MoL top-k");
+    MOL_TIMED_LAUNCH(MOL_OP_TOPK_EXACT, st, launch_fused_topk(pr, k, f.R, f.range_len, f.G, partial, st),
+                     "fused MoL top-k");
     if ((rc = reduce_rows(f.s, w, static_cast<long>(f.R) * k, fin, k, st))) return rc;
     MOL_TRY_HIP(launch_decode(fin, k, prob->B, k, out_score, out_idx, st), "decode");
     return MOL_OK;
@@ -357,7 +423,8 @@ int mol_topk_per_embd(const mol_problem* prob, int32_t kprime, float* out_dot, i
     uint64_t* lists = reinterpret_cast<uint64_t*>(w + f.s.offA);
     uint64_t* fin = reinterpret_cast<uint64_t*>(w + f.offFinal);
     uint64_t* stg = reinterpret_cast<uint64_t*>(w + f.offStg);
-    MOL_TRY_HIP(launch_per_embd(pr, kprime, f.R, f.range_len, f.G, lists, stg, st), "per-component top-k'");
+    MOL_TIMED_LAUNCH(MOL_OP_TOPK_PER_EMBD, st,
+                     launch_per_embd(pr, kprime, f.R, f.range_len, f.G, lists, stg, st), "per-component top-k'");
     if ((rc = reduce_rows(f.s, w, static_cast<long>(f.R) * f.KL, fin, kprime, st))) return rc;
     MOL_TRY_HIP(launch_decode(fin, kprime, rows, kprime, out_dot, out_idx, st), "decode");
     return MOL_OK;
@@ -390,10 +457,11 @@ int mol_rerank(const mol_problem* prob, const int32_t* cand, int32_t C, int32_t 
   if (rerank_supported(pr, k)) {
     const int chunk = rerank_chunk(C);
     const long L0 = static_cast<long>((C + chunk - 1) / chunk) * k;
-    MOL_TRY_HIP(launch_rerank(pr, uniq, nu, C, k, A, st), "fused rerank");
+    MOL_TIMED_LAUNCH(MOL_OP_RERANK, st, launch_rerank(pr, uniq, nu, C, k, A, st), "fused rerank");
     if ((rc = reduce_rows(r.s, w, L0, fin, k, st))) return rc;
   } else {
-    MOL_TRY_HIP(launch_phi_generic(pr, 0, C, uniq, nu, C, nullptr, 0, A, r.s.strideA, st), "rerank score");
+    MOL_TIMED_LAUNCH(MOL_OP_RERANK, st, launch_phi_generic(pr, 0, C, uniq, nu, C, nullptr, 0, A, r.s.strideA, st),
+                     "rerank score");
     if ((rc = reduce_rows(r.s, w, C, fin, k, st))) return rc;
   }
   MOL_TRY_HIP(launch_decode(fin, k, prob->B, k, out_score, out_idx, st), "decode");
@@ -408,6 +476,36 @@ int mol_avg_embed(const mol_problem* prob, void* q_avg, void* x_avg, void* strea
   if ((rc = check_problem(prob, false))) return rc;
   hipStream_t st = static_cast<hipStream_t>(stream);
   MOL_TRY_HIP(launch_avg_embed(dev_prob(prob), q_avg, x_avg, st), "avg embed");
+  return MOL_OK;
+}
+
+int mol_timing_enable(int on) {
+  TimingLog& t = timing_log();
+  std::lock_guard<std::mutex> g(t.mu);
+  t.on = on != 0;
+  return MOL_OK;
+}
+
+int mol_timing_read(int op, double* total_ms, int32_t* launches) {
+  if (op < 0 || op >= kTimedOps) return fail(MOL_EINVAL, "unknown op %d", op);
+  if (!total_ms || !launches) return fail(MOL_EINVAL, "output pointer is NULL");
+  TimingLog& t = timing_log();
+  std::lock_guard<std::mutex> g(t.mu);
+  double sum = 0.0;
+  int32_t n = 0;
+  hipError_t err = hipSuccess;
+  for (const EvPair& p : t.rec[op]) {
+    float ms = 0.f;
+    if (err == hipSuccess) err = hipEventSynchronize(p.b);
+    if (err == hipSuccess) err = hipEventElapsedTime(&ms, p.a, p.b);
+    sum += ms;
+    ++n;
+    t.spare.push_back(p);
+  }
+  t.rec[op].clear();
+  if (err != hipSuccess) return hip_fail(err, "mol_timing_read");
+  *total_ms = sum;
+  *launches = n;
   return MOL_OK;
 }
 

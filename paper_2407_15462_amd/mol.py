@@ -21,7 +21,8 @@ MOL_F32, MOL_BF16 = 0, 1
 MOL_OP_SCORE, MOL_OP_TOPK_EXACT, MOL_OP_TOPK_PER_EMBD, MOL_OP_RERANK = range(4)
 
 EXPORTS = ("mol_workspace_size", "mol_score", "mol_topk_exact", "mol_topk_per_embd",
-           "mol_rerank", "mol_avg_embed", "mol_status_str", "mol_last_error")
+           "mol_rerank", "mol_avg_embed", "mol_timing_enable", "mol_timing_read",
+           "mol_status_str", "mol_last_error")
 
 
 class MolError(RuntimeError):
@@ -63,6 +64,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "mol_topk_per_embd": [P, i32, vp, vp, vp, sz, vp],
         "mol_rerank": [P, vp, i32, i32, vp, vp, vp, vp, sz, vp],
         "mol_avg_embed": [P, vp, vp, vp],
+        "mol_timing_enable": [ctypes.c_int],
+        "mol_timing_read": [ctypes.c_int, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(i32)],
     }
     for name, args in sig.items():
         fn = getattr(lib, name)
@@ -162,6 +165,18 @@ def mol_rerank(prob: Problem, cand, C: int, k: int, out_score, out_idx, out_n_un
 
 def mol_avg_embed(prob: Problem, q_avg, x_avg, stream=None) -> None:
     _check(load().mol_avg_embed(prob.ref, _ptr(q_avg), _ptr(x_avg), _stream(stream)))
+
+
+def mol_timing_enable(on: bool) -> None:
+    _check(load().mol_timing_enable(1 if on else 0))
+
+
+def mol_timing_read(op: int) -> Tuple[float, int]:
+    """(summed milliseconds, launch count) of the main kernel of ``op`` since
+    the last read; waits for the recorded events."""
+    ms, n = ctypes.c_double(0.0), ctypes.c_int32(0)
+    _check(load().mol_timing_read(op, ctypes.byref(ms), ctypes.byref(n)))
+    return ms.value, n.value
 
 
 # ------------------------------------------------- torch-allocating conveniences

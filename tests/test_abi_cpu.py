@@ -96,3 +96,22 @@ def test_entry_points_reject_before_launch():
     rc = lib.mol_rerank(ctypes.byref(c), None, 8, 5, 256, 256, None, ws, 1 << 40, None)
     assert rc == mol.MOL_EINVAL
     assert lib.mol_topk_exact(None, 10, 256, 256, ws, 1 << 40, None) == mol.MOL_EINVAL
+
+
+def test_timing_records_are_empty_and_validated():
+    lib = mol.load()
+    ms, n = ctypes.c_double(-1.0), ctypes.c_int32(-1)
+    assert lib.mol_timing_enable(0) == mol.MOL_OK
+    assert lib.mol_timing_read(mol.MOL_OP_TOPK_EXACT, ctypes.byref(ms), ctypes.byref(n)) == mol.MOL_OK
+    assert (ms.value, n.value) == (0.0, 0)
+    assert lib.mol_timing_read(4, ctypes.byref(ms), ctypes.byref(n)) == mol.MOL_EINVAL
+    assert lib.mol_timing_read(-1, ctypes.byref(ms), ctypes.byref(n)) == mol.MOL_EINVAL
+    assert lib.mol_timing_read(0, None, ctypes.byref(n)) == mol.MOL_EINVAL
+    # a call rejected before launch records nothing
+    c = _problem()
+    assert lib.mol_timing_enable(1) == mol.MOL_OK
+    assert lib.mol_topk_exact(ctypes.byref(c), 10, 256, 256, ctypes.c_void_p(256), 16, None) \
+        == mol.MOL_EWORKSPACE
+    assert lib.mol_timing_enable(0) == mol.MOL_OK
+    assert lib.mol_timing_read(mol.MOL_OP_TOPK_EXACT, ctypes.byref(ms), ctypes.byref(n)) == mol.MOL_OK
+    assert n.value == 0
