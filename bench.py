@@ -47,11 +47,17 @@ def parse():
 
 
 def source_digest(names=FUSED_SOURCES) -> str:
+    """sha256 of the kernel sources with comments and whitespace removed, so
+    that only a change of the code itself marks a measurement as stale."""
     import hashlib
+    import re
     h = hashlib.sha256()
     for n in names:
-        with open(os.path.join(CSRC, n), "rb") as f:
-            h.update(f.read())
+        with open(os.path.join(CSRC, n)) as f:
+            text = f.read()
+        text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+        text = re.sub(r"//[^\n]*", " ", text)
+        h.update(" ".join(text.split()).encode())
     return h.hexdigest()
 
 

@@ -12,9 +12,9 @@
 // Epilogues: a running per-query top-k (Definition 1) kept in LDS with
 // threshold rejection, or a dense phi store.
 //
-// Workgroup: 8 waves (2 per SIMD) = 16 queries sharing an LDS-staged,
-// double-buffered stream of 32-item tiles loaded with direct global->LDS
-// copies.
+// Workgroup: 8 waves (2 per SIMD) = 16 queries sharing an LDS-staged
+// stream of 32-item tiles (a three-deep ring) loaded with direct
+// global->LDS copies.
 #include "mol_tile.h"
 
 namespace mol {

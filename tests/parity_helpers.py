@@ -10,6 +10,7 @@ import synth
 from oracle import mol_oracle as mo
 
 TAU = 1e-4          # score tolerance and tie window (absolute)
+MAX_ERR = {}        # largest |gpu - oracle| seen per check label (reported at session end)
 
 
 def log(msg: str) -> None:
@@ -23,7 +24,11 @@ def oracle_problem(inp: synth.MolInputs) -> mo.Problem:
 
 def check_scores(got: np.ndarray, want: np.ndarray, tol: float = TAU, what: str = "phi") -> None:
     err = np.abs(got.astype(np.float64) - want)
+    if err.size == 0:
+        return
     i = np.unravel_index(np.argmax(err), err.shape)
+    label = what.split(" ")[0]
+    MAX_ERR[label] = max(MAX_ERR.get(label, 0.0), float(err.max()))
     assert err.max() <= tol, f"{what}: max |err| {err.max():.3e} at {i} (got {got[i]}, want {want[i]})"
 
 
