@@ -150,8 +150,9 @@ int mol_avg_embed(const mol_problem *prob, void *q_avg, void *x_avg,
 /* Kernel timing, a diagnostic for throughput measurements.
  * mol_timing_enable(1) makes every later call record a pair of HIP events on
  * its stream around its main kernel: the fused scoring kernel of mol_score,
- * the scoring + per-range top-k scan of mol_topk_exact, the per-component
- * scan of mol_topk_per_embd and the candidate scoring of mol_rerank
+ * the scoring + per-range top-k scan of mol_topk_exact, the two
+ * per-component scans (with the threshold selection between them) of
+ * mol_topk_per_embd and the candidate scoring of mol_rerank
  * (validation, merges of partial lists and decoding are outside the pair).
  * mol_timing_enable(0) stops recording; records already taken stay.
  * mol_timing_read(op, &ms, &n) waits for the recorded events of operation

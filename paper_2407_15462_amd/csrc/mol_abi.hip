@@ -265,18 +265,19 @@ FusedExactPlan plan_fused_exact(const DevProb& pr, int k) {
 // are reduced to [rows][k'] by segmented sorts.
 struct PerEmbdPlan {
   StreamPlan s;
-  int R = 0, range_len = 0, G = 0, KL = 0;
-  size_t offFinal = 0, offStg = 0, bytes = 0;
+  PerEmbdGrid g;
+  int KL = 0;
+  size_t offFinal = 0, offStg = 0, offBmax = 0, offThr = 0, bytes = 0;
 };
 
 PerEmbdPlan plan_per_embd(const DevProb& pr, int kp) {
   PerEmbdPlan f;
-  per_embd_grid(pr, f.R, f.range_len, f.G);
+  per_embd_grid(pr, f.g);
   f.KL = per_embd_list_cap(kp);
   StreamPlan& s = f.s;
   s.rows = pr.B * pr.P;
   s.k = kp;
-  const long L0 = static_cast<long>(f.R) * f.KL;
+  const long L0 = static_cast<long>(f.g.R) * f.KL;
   const int S0 = segment_size_for(static_cast<int>(L0), kp);
   s.strideA = L0;
   s.strideB = std::max<long>((L0 + S0 - 1) / S0 * kp, kp);
@@ -284,7 +285,9 @@ PerEmbdPlan plan_per_embd(const DevProb& pr, int kp) {
   s.offA = off;     off = align_up(off + 8ul * s.rows * s.strideA);
   s.offB = off;     off = align_up(off + 8ul * s.rows * s.strideB);
   f.offFinal = off; off = align_up(off + 8ul * s.rows * kp);
-  f.offStg = off;   off = align_up(off + 8ul * s.rows * f.R * per_embd_stage_cap());
+  f.offStg = off;   off = align_up(off + 8ul * s.rows * f.g.R * per_embd_stage_cap());
+  f.offBmax = off;  off = align_up(off + 4ul * s.rows * f.g.R * 2 * f.g.nbk);
+  f.offThr = off;   off = align_up(off + 4ul * s.rows);
   f.bytes = off;
   return f;
 }
@@ -423,9 +426,11 @@ int mol_topk_per_embd(const mol_problem* prob, int32_t kprime, float* out_dot, i
     uint64_t* lists = reinterpret_cast<uint64_t*>(w + f.s.offA);
     uint64_t* fin = reinterpret_cast<uint64_t*>(w + f.offFinal);
     uint64_t* stg = reinterpret_cast<uint64_t*>(w + f.offStg);
-    MOL_TIMED_LAUNCH(MOL_OP_TOPK_PER_EMBD, st,
-                     launch_per_embd(pr, kprime, f.R, f.range_len, f.G, lists, stg, st), "per-component top-k'");
-    if ((rc = reduce_rows(f.s, w, static_cast<long>(f.R) * f.KL, fin, kprime, st))) return rc;
+    float* bmax = reinterpret_cast<float*>(w + f.offBmax);
+    float* thr = reinterpret_cast<float*>(w + f.offThr);
+    MOL_TIMED_LAUNCH(MOL_OP_TOPK_PER_EMBD, st, launch_per_embd(pr, kprime, f.g, bmax, thr, lists, stg, st),
+                     "per-component top-k'");
+    if ((rc = reduce_rows(f.s, w, static_cast<long>(f.g.R) * f.KL, fin, kprime, st))) return rc;
     MOL_TRY_HIP(launch_decode(fin, kprime, rows, kprime, out_dot, out_idx, st), "decode");
     return MOL_OK;
   }

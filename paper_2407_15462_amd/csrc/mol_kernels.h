@@ -44,14 +44,21 @@ hipError_t launch_fused_dense(const DevProb& pr, int n_begin, int n_count, float
 
 namespace mol {
 
-// Per-component top-k' with MFMA dots and LDS-staged threshold selection
+// Per-component top-k' with MFMA dots: a bucket-maximum scan, a per-list
+// starting threshold, and a threshold scan with staged merges
 // (bf16, d in {64, 128}, k' <= 256).
+struct PerEmbdGrid {
+  int R = 0, range_len = 0, G = 0;   // item ranges, items per range, vector groups
+  int bucket_tiles = 0, nbk = 0;     // 32-item tiles per bucket, buckets per (range, half)
+};
 bool per_embd_supported(const DevProb& pr, int kp);
 int per_embd_list_cap(int kp);
 int per_embd_stage_cap();
-void per_embd_grid(const DevProb& pr, int& R, int& range_len, int& G);
-hipError_t launch_per_embd(const DevProb& pr, int kp, int R, int range_len, int G, uint64_t* lists,
-                           uint64_t* stg, hipStream_t st);
+void per_embd_grid(const DevProb& pr, PerEmbdGrid& g);
+// bmax: [B*Pq*Px][R][2][nbk] floats; thr: [B*Pq*Px] floats;
+// lists: [B*Pq*Px][R][KL] keys; stg: [B*Pq*Px][R][stage_cap] keys.
+hipError_t launch_per_embd(const DevProb& pr, int kp, const PerEmbdGrid& g, float* bmax, float* thr,
+                           uint64_t* lists, uint64_t* stg, hipStream_t st);
 
 }  // namespace mol
 

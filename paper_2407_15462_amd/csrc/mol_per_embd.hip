@@ -9,13 +9,21 @@
 // (B operands, in registers) on 32x32x16 bf16 MFMAs.  In the result
 // D[item][query vector] lane (c = lane % 32, h = lane / 32) holds, per
 // block, 16 items' scores for the single list of query vector c: every
-// list is owned by two lanes, each seeing half of the items.  A lane keeps
-// its list's running threshold (the k'-th best key merged so far) and
-// appends the scores that reach it to its own staging region in the
-// workspace; about k' (1 + ln(n / k')) keys per list survive over n items.
-// A full staging region is merged into the list (also in the workspace) by
-// a wave-wide bitonic sort in LDS.  Lists of several item ranges are merged
-// afterwards by segmented sorts.
+// list is owned by two lanes, each seeing half of the items.
+//
+// Two scans of the same dot products:
+//  1. every lane keeps the maximum of its scores over buckets of
+//     `bucket_tiles` tiles and stores the bucket maxima;
+//  2. the k'-th largest bucket maximum of a list is a lower bound of the
+//     list's k'-th largest score (k' disjoint buckets each hold an item at
+//     least that large), so the second scan starts every list at that
+//     threshold.  Scores that reach the threshold are appended to the
+//     lane's staging region in the workspace; a full staging region is
+//     merged into the list by a wave-wide bitonic sort in LDS, and the
+//     threshold rises to the list's k'-th key.
+// Both scans evaluate bit-identical dot products (same instructions, same
+// accumulation order), so the bound is exact.  Lists of several item ranges
+// are merged afterwards by segmented sorts.
 #include "mol_tile.h"
 
 namespace mol {
@@ -34,6 +42,7 @@ constexpr int kStageBytes = 16384;           // bytes of one LDS item stage
 constexpr int kRing = 4;                     // item stages in flight
 constexpr int kSortKeys = 512;               // keys of one wave's merge sort
 constexpr int kSGMax = (kSortKeys - 128) / 2;  // largest staging region per lane half
+constexpr int kMaxBuckets = 2048;            // bucket maxima per list (all ranges, both halves)
 
 __device__ __forceinline__ f32x16_t mfma32_bf16(uint4 a, uint4 b, f32x16_t c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, a),
@@ -59,10 +68,13 @@ struct EmbdShape {
 
 // Grid: WG -> (vector group, px, range).  WGs sharing (px, range) are placed
 // on the same XCD (WG id mod 8) when the grid allows it.
-// lists: [nvec * Px][R][KL] keys; stg: [nvec * Px][R][2][SG] keys.
-template <int D, int KL>
+// bmax: [nvec * Px][R][2][nbk] bucket maxima (scan 1 writes, scan 2 unused);
+// thr: [nvec * Px] starting thresholds (scan 2 reads);
+// lists: [nvec * Px][R][KL] keys; stg: [nvec * Px][R][2][SG] keys (scan 2).
+template <int D, int KL, bool SCAN2>
 __global__ __launch_bounds__(64 * kWaves, 1) void k_topk_per_embd(
-    DevProb pr, int kp, int R, int range_len, int G, uint64_t* __restrict__ lists,
+    DevProb pr, int kp, int R, int range_len, int G, int bucket_tiles, int nbk,
+    float* __restrict__ bmax, const float* __restrict__ thr, uint64_t* __restrict__ lists,
     uint64_t* __restrict__ stg) {
   using S = EmbdShape<D, KL>;
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
@@ -113,19 +125,32 @@ __global__ __launch_bounds__(64 * kWaves, 1) void k_topk_per_embd(
   // list of (block nb, column c): query vector vwave + 32 nb + c, component px, range r
   auto list_idx = [&](int nb, int c) { return (static_cast<long>(vwave + 32 * nb + c) * Px + px) * R + r; };
   auto stg_ptr = [&](int nb, int c, int h) { return stg + (list_idx(nb, c) * 2 + h) * S::SG; };
-  // per-lane list state: threshold (float score of the k'-th key) and staging count
-  float th[kNB];
+  // per-lane state.  Scan 1: running bucket maximum.  Scan 2: threshold
+  // (float score every appended key reaches), staging count, and whether the
+  // list has been merged into (it is empty otherwise).
+  bool vok[kNB];
+  float th[kNB], bm[kNB];
   int cnt[kNB];
+  bool merged[kNB];
 #pragma unroll
   for (int nb = 0; nb < kNB; ++nb) {
-    const bool vok = vwave + 32 * nb + col < nvec;
-    th[nb] = vok ? -__builtin_inff() : __builtin_inff();   // invalid vectors never pass
+    vok[nb] = vwave + 32 * nb + col < nvec;
+    bm[nb] = -__builtin_inff();
     cnt[nb] = 0;
-    if (vok && half == 0) {
-      uint64_t* lp = lists + list_idx(nb, col) * KL;
-      for (int i = 0; i < KL; ++i) lp[i] = 0ull;
+    merged[nb] = false;
+    th[nb] = __builtin_inff();                      // invalid vectors never pass
+    if (SCAN2 && vok[nb]) {
+      th[nb] = thr[static_cast<long>(vwave + 32 * nb + col) * Px + px];
+      if (half == 0) {
+        uint64_t* lp = lists + list_idx(nb, col) * KL;
+        for (int i = 0; i < KL; ++i) lp[i] = 0ull;
+      }
     }
   }
+  auto bucket_ptr = [&](int nb) {
+    return bmax + ((static_cast<long>(vwave + 32 * nb + col) * Px + px) * R + r) * 2 * nbk +
+           static_cast<long>(half) * nbk;
+  };
   // merge the staged keys of list (nb, c) into it; nb and c are wave-uniform
   auto merge = [&](int nb, int c) {
     // staged keys were written by other lanes of this wave: make them visible
@@ -158,8 +183,9 @@ __global__ __launch_bounds__(64 * kWaves, 1) void k_topk_per_embd(
     const float nth = key_score(mySort[kp - 1]);
     wave_lds_sync();
     if (col == c) {
-      th[nb] = nth;
+      th[nb] = fmaxf(th[nb], nth);
       cnt[nb] = 0;
+      merged[nb] = true;
     }
   };
 
@@ -169,12 +195,13 @@ __global__ __launch_bounds__(64 * kWaves, 1) void k_topk_per_embd(
   else __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
 
+  int tile = 0;                                   // tile index within the range
   for (int t = 0; t < nstages; ++t) {
     const int buf = t % kRing;
     const unsigned char* xs = sX + buf * kStageBytes;
-    for (int tt = 0; tt < S::ST / 32; ++tt) {
+    for (int tt = 0; tt < S::ST / 32; ++tt, ++tile) {
       const int n = 32 * tt + col;                    // A-operand row = item
-      const int n0 = nr0 + S::ST * t + 32 * tt;       // first item of the tile
+      const int n0 = nr0 + 32 * tile;                 // first item of the tile
       f32x16_t acc[kNB];
 #pragma unroll
       for (int nb = 0; nb < kNB; ++nb) acc[nb] = f32x16_t{};
@@ -185,31 +212,59 @@ __global__ __launch_bounds__(64 * kWaves, 1) void k_topk_per_embd(
 #pragma unroll
         for (int nb = 0; nb < kNB; ++nb) acc[nb] = mfma32_bf16(xa, qop[nb][kk], acc[nb]);
       }
-      // lane (c, h) register v holds item n0 + (v/4)*8 + 4h + v%4 of list c
-      if (n0 + 32 > nr1) {
+      // lane (c, h) register v holds item n0 + (v/4)*8 + 4h + v%4 of list c;
+      // items past the range end (last tile only) become -inf
+      const bool ragged = n0 + 32 > nr1;
+      uint32_t vmask = 0xFFFFu;
+      if (ragged) {
+        vmask = 0u;
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
           const bool ok = n0 + (v >> 2) * 8 + 4 * half + (v & 3) < nr1;
+          vmask |= ok ? (1u << v) : 0u;
 #pragma unroll
-          for (int nb = 0; nb < kNB; ++nb) acc[nb][v] = ok ? acc[nb][v] : __builtin_nanf("");  // never passes
+          for (int nb = 0; nb < kNB; ++nb) acc[nb][v] = ok ? acc[nb][v] : -__builtin_inff();
         }
       }
-      uint64_t any = 0ull;
+      float m[kNB];
 #pragma unroll
-      for (int nb = 0; nb < kNB; ++nb)
+      for (int nb = 0; nb < kNB; ++nb) {
+        float a0 = fmaxf(fmaxf(acc[nb][0], acc[nb][1]), acc[nb][2]);
+        float a1 = fmaxf(fmaxf(acc[nb][3], acc[nb][4]), acc[nb][5]);
+        float a2 = fmaxf(fmaxf(acc[nb][6], acc[nb][7]), acc[nb][8]);
+        float a3 = fmaxf(fmaxf(acc[nb][9], acc[nb][10]), acc[nb][11]);
+        float a4 = fmaxf(fmaxf(acc[nb][12], acc[nb][13]), acc[nb][14]);
+        m[nb] = fmaxf(fmaxf(fmaxf(a0, a1), a2), fmaxf(fmaxf(a3, a4), acc[nb][15]));
+      }
+      if (!SCAN2) {
 #pragma unroll
-        for (int v = 0; v < 16; ++v) any |= __ballot(acc[nb][v] >= th[nb]);
-      if (any == 0ull) continue;
+        for (int nb = 0; nb < kNB; ++nb) bm[nb] = fmaxf(bm[nb], m[nb]);
+        if ((tile + 1) % bucket_tiles == 0) {
+          const int bk = tile / bucket_tiles;
+#pragma unroll
+          for (int nb = 0; nb < kNB; ++nb) {
+            if (vok[nb]) bucket_ptr(nb)[bk] = bm[nb];
+            bm[nb] = -__builtin_inff();
+          }
+        }
+        continue;
+      }
+      bool hit = false;
+#pragma unroll
+      for (int nb = 0; nb < kNB; ++nb) hit = hit || m[nb] >= th[nb];
+      if (__ballot(hit) == 0ull) continue;
       // append survivors to the lane's own staging region
 #pragma unroll
       for (int nb = 0; nb < kNB; ++nb) {
-        uint64_t* sp = stg_ptr(nb, col, half);
+        if (m[nb] >= th[nb]) {
+          uint64_t* sp = stg_ptr(nb, col, half);
 #pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          if (acc[nb][v] >= th[nb]) {
-            const int item = n0 + (v >> 2) * 8 + 4 * half + (v & 3);
-            sp[cnt[nb]] = make_key(acc[nb][v], item);
-            ++cnt[nb];
+          for (int v = 0; v < 16; ++v) {
+            if (acc[nb][v] >= th[nb] && ((vmask >> v) & 1u)) {
+              const int item = n0 + (v >> 2) * 8 + 4 * half + (v & 3);
+              sp[cnt[nb]] = make_key(acc[nb][v], item);
+              ++cnt[nb];
+            }
           }
         }
       }
@@ -234,7 +289,35 @@ __global__ __launch_bounds__(64 * kWaves, 1) void k_topk_per_embd(
     }
     __syncthreads();
   }
-  // flush the remaining staged keys
+  if (!SCAN2) {
+    // the last partial bucket, then -inf for buckets past the range end
+    const int ntiles = tile;
+    const int done = ntiles / bucket_tiles;
+#pragma unroll
+    for (int nb = 0; nb < kNB; ++nb) {
+      if (!vok[nb]) continue;
+      float* bp = bucket_ptr(nb);
+      int bk = done;
+      if (ntiles % bucket_tiles != 0) bp[bk++] = bm[nb];
+      for (; bk < nbk; ++bk) bp[bk] = -__builtin_inff();
+    }
+    return;
+  }
+  // staged keys of lists never merged into go straight into the (empty)
+  // list when they fit; the others are merged
+  __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "agent");
+#pragma unroll
+  for (int nb = 0; nb < kNB; ++nb) {
+    const int other = __shfl_xor(cnt[nb], 32);
+    const int c0 = half == 0 ? cnt[nb] : other;
+    const int c1 = half == 0 ? other : cnt[nb];
+    if (vok[nb] && !merged[nb] && c0 + c1 <= KL) {
+      uint64_t* lp = lists + list_idx(nb, col) * KL + (half == 0 ? 0 : c0);
+      const uint64_t* sp = stg_ptr(nb, col, half);
+      for (int i = 0; i < cnt[nb]; ++i) lp[i] = sp[i];
+      cnt[nb] = 0;
+    }
+  }
 #pragma unroll
   for (int nb = 0; nb < kNB; ++nb) {
     uint64_t need = __ballot(cnt[nb] > 0);
@@ -244,6 +327,35 @@ __global__ __launch_bounds__(64 * kWaves, 1) void k_topk_per_embd(
       merge(nb, c);
     }
   }
+}
+
+// k'-th largest bucket maximum of every list (one wave per list): the
+// starting threshold of the second scan.  Bitwise search over the
+// order-preserving 32-bit image of the scores; fewer than k' finite
+// maxima give -inf (no filtering).
+__global__ __launch_bounds__(256) void k_bucket_threshold(const float* __restrict__ bmax, int nlists,
+                                                         int per_list, int kp, float* __restrict__ thr) {
+  const int lane = threadIdx.x & 63;
+  const long list = static_cast<long>(blockIdx.x) * 4 + (threadIdx.x >> 6);
+  if (list >= nlists) return;                    // whole wave exits
+  const float* row = bmax + list * per_list;
+  uint32_t v[kMaxBuckets / 64];
+#pragma unroll
+  for (int j = 0; j < kMaxBuckets / 64; ++j) {
+    const int i = lane + 64 * j;
+    v[j] = i < per_list ? float_to_ordered(row[i]) : 0u;
+  }
+  uint32_t t = 0u;
+  for (int bit = 31; bit >= 0; --bit) {
+    const uint32_t c = t | (1u << bit);
+    int n = 0;
+#pragma unroll
+    for (int j = 0; j < kMaxBuckets / 64; ++j) n += __popcll(__ballot(v[j] >= c));
+    if (n >= kp) t = c;
+  }
+  // t is the k'-th largest image; images below that of -inf mean "none"
+  const float f = t >= float_to_ordered(-__builtin_inff()) ? ordered_to_float(t) : -__builtin_inff();
+  if (lane == 0) thr[list] = f;
 }
 
 // ---------------------------------------------------------------------------
@@ -256,38 +368,59 @@ bool per_embd_supported(const DevProb& pr, int kp) {
 int per_embd_list_cap(int kp) { return kp <= 128 ? 128 : 256; }
 int per_embd_stage_cap() { return 2 * kSGMax; }
 
-void per_embd_grid(const DevProb& pr, int& R, int& range_len, int& G) {
+void per_embd_grid(const DevProb& pr, PerEmbdGrid& g) {
   const int nvec = pr.B * pr.Pq;
-  G = (nvec + kVecPerWG - 1) / kVecPerWG;
-  const int units = G * pr.Px;
-  R = std::max(1, (256 + units - 1) / units);
+  g.G = (nvec + kVecPerWG - 1) / kVecPerWG;
+  const int units = g.G * pr.Px;
+  int R = std::max(1, (256 + units - 1) / units);
   R = std::min(R, std::max(1, pr.N / 4096));
-  range_len = (pr.N + R - 1) / R;
-  range_len = (range_len + 127) / 128 * 128;
-  R = (pr.N + range_len - 1) / range_len;
+  g.range_len = (pr.N + R - 1) / R;
+  g.range_len = (g.range_len + 127) / 128 * 128;
+  g.R = (pr.N + g.range_len - 1) / g.range_len;
+  // buckets: as many as fit kMaxBuckets per list over all ranges and halves
+  const int ntiles = g.range_len / 32;
+  g.bucket_tiles = std::max(1, (2 * g.R * ntiles + kMaxBuckets - 1) / kMaxBuckets);
+  g.nbk = (ntiles + g.bucket_tiles - 1) / g.bucket_tiles;
+  while (2 * g.R * g.nbk > kMaxBuckets) {
+    ++g.bucket_tiles;
+    g.nbk = (ntiles + g.bucket_tiles - 1) / g.bucket_tiles;
+  }
 }
 
-template <int D, int KL>
-static hipError_t launch_pe_t(const DevProb& pr, int kp, int R, int range_len, int G, uint64_t* lists,
-                              uint64_t* stg, hipStream_t st) {
+template <int D, int KL, bool SCAN2>
+static hipError_t launch_pe_t(const DevProb& pr, int kp, const PerEmbdGrid& g, float* bmax, const float* thr,
+                              uint64_t* lists, uint64_t* stg, hipStream_t st) {
   using S = EmbdShape<D, KL>;
-  auto kern = &k_topk_per_embd<D, KL>;
+  auto kern = &k_topk_per_embd<D, KL, SCAN2>;
   hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                      hipFuncAttributeMaxDynamicSharedMemorySize, S::LDS_TOTAL);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(kern, dim3(G * pr.Px * R), dim3(64 * kWaves), S::LDS_TOTAL, st, pr, kp, R,
-                     range_len, G, lists, stg);
+  hipLaunchKernelGGL(kern, dim3(g.G * pr.Px * g.R), dim3(64 * kWaves), S::LDS_TOTAL, st, pr, kp, g.R,
+                     g.range_len, g.G, g.bucket_tiles, g.nbk, bmax, thr, lists, stg);
   return hipGetLastError();
 }
 
-hipError_t launch_per_embd(const DevProb& pr, int kp, int R, int range_len, int G, uint64_t* lists,
-                           uint64_t* stg, hipStream_t st) {
+template <int D, int KL>
+static hipError_t launch_pe_d(const DevProb& pr, int kp, const PerEmbdGrid& g, float* bmax, float* thr,
+                              uint64_t* lists, uint64_t* stg, hipStream_t st) {
+  hipError_t e = launch_pe_t<D, KL, false>(pr, kp, g, bmax, thr, lists, stg, st);
+  if (e != hipSuccess) return e;
+  const int nlists = pr.B * pr.Pq * pr.Px;
+  hipLaunchKernelGGL(k_bucket_threshold, dim3((nlists + 3) / 4), dim3(256), 0, st, bmax, nlists,
+                     2 * g.R * g.nbk, kp, thr);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  return launch_pe_t<D, KL, true>(pr, kp, g, bmax, thr, lists, stg, st);
+}
+
+hipError_t launch_per_embd(const DevProb& pr, int kp, const PerEmbdGrid& g, float* bmax, float* thr,
+                           uint64_t* lists, uint64_t* stg, hipStream_t st) {
   const int KL = per_embd_list_cap(kp);
   if (pr.d == 64)
-    return KL == 128 ? launch_pe_t<64, 128>(pr, kp, R, range_len, G, lists, stg, st)
-                     : launch_pe_t<64, 256>(pr, kp, R, range_len, G, lists, stg, st);
-  return KL == 128 ? launch_pe_t<128, 128>(pr, kp, R, range_len, G, lists, stg, st)
-                   : launch_pe_t<128, 256>(pr, kp, R, range_len, G, lists, stg, st);
+    return KL == 128 ? launch_pe_d<64, 128>(pr, kp, g, bmax, thr, lists, stg, st)
+                     : launch_pe_d<64, 256>(pr, kp, g, bmax, thr, lists, stg, st);
+  return KL == 128 ? launch_pe_d<128, 128>(pr, kp, g, bmax, thr, lists, stg, st)
+                   : launch_pe_d<128, 256>(pr, kp, g, bmax, thr, lists, stg, st);
 }
 
 }  // namespace mol

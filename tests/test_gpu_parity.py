@@ -124,6 +124,36 @@ def test_topk_per_embd_matches_oracle(name, spec, kp):
             check_topk_row(s[:, p], ids[b, p], dots[b, p], kp, f"{name} b={b} p={p}")
 
 
+def test_topk_per_embd_adversarial_order_and_ties():
+    """Lists whose best items are contiguous (one block of identical items)
+    or all tied (a zero query vector): the bucket-maximum threshold is then
+    loose, staging overflows and the merge path runs; ties resolve to the
+    lowest item indices."""
+    spec = W["exact_1m"].scaled(B=3, N=12000, clusters=32)
+    kp = 128
+    inp = cuda_inputs(spec, seed=21)
+    blk0, blk1 = 2000, 5000
+    inp.X[0, blk0:blk1, :] = inp.Q[1, 0, :]          # list (b=1, pq=0, px=0): a tied block on top
+    inp.Q[2, 3, :] = 0                                # lists (b=2, pq=3, *): every dot is 0
+    log(f"[per_embd adversarial] B={spec.B} N={spec.N} k'={kp}")
+    prob = mol.Problem(inp.Q, inp.X)
+    dots, ids = mol.topk_per_embd(prob, kp)
+    torch.cuda.synchronize()
+    dots, ids = dots.cpu().numpy(), ids.cpu().numpy()
+    Px = spec.Px
+    assert ids[1, 0].tolist() == list(range(blk0, blk0 + kp))
+    assert np.all(dots[1, 0] == dots[1, 0, 0])
+    for px in range(Px):
+        p = 3 * Px + px
+        assert ids[2, p].tolist() == list(range(kp)), f"zero query, component {p}"
+        assert np.all(dots[2, p] == 0.0)
+    op = oracle_problem(inp)
+    for b in range(spec.B):
+        s_all = mo.all_dots(op, b)
+        for p in range(spec.P):
+            check_topk_row(s_all[:, p], ids[b, p], dots[b, p], kp, f"adversarial b={b} p={p}")
+
+
 def test_avg_embed_bit_exact_and_topk_avg():
     spec = W["hybrid_8m"].scaled(B=6, N=5000, clusters=32)
     inp = cuda_inputs(spec, seed=16)
