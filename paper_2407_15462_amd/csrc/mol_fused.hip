@@ -152,9 +152,8 @@ __global__ __launch_bounds__(64 * kWaves, 1) void k_mol_fused(
   }
 
   // stage 0 complete; later stages' copies may still be in flight
-  if (ntiles >= kRing - 1) __builtin_amdgcn_s_waitcnt(waitcnt_vm((kRing - 2) * S::LOADS));
-  else __builtin_amdgcn_s_waitcnt(0);
-  __syncthreads();
+  if (ntiles >= kRing - 1) ring_barrier<(kRing - 2) * S::LOADS>();
+  else ring_barrier<0>();
 
   for (int t = 0; t < ntiles; ++t) {
     const int buf = t % kRing;
@@ -219,11 +218,10 @@ __global__ __launch_bounds__(64 * kWaves, 1) void k_mol_fused(
     // refill the buffer read in iteration t-1, then wait for stage t+1
     if (t + kRing - 1 < ntiles) {
       stage(t + kRing - 1, (t + kRing - 1) % kRing);
-      __builtin_amdgcn_s_waitcnt(waitcnt_vm((kRing - 2) * S::LOADS));
+      ring_barrier<(kRing - 2) * S::LOADS>();
     } else {
-      __builtin_amdgcn_s_waitcnt(0);
+      ring_barrier<0>();
     }
-    __syncthreads();
   }
 
   if constexpr (!DENSE) {

@@ -35,9 +35,9 @@ namespace {
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
 constexpr int kWaves = 8;
-constexpr int kNB = 2;                       // query-vector blocks per wave
-constexpr int kVecPerWave = 32 * kNB;
-constexpr int kVecPerWG = kWaves * kVecPerWave;
+// query-vector blocks of 32 per wave: 4 at d = 64, 2 at d = 128 (B operands
+// stay in registers)
+constexpr int nb_for(int d) { return d >= 128 ? 2 : 4; }
 constexpr int kStageBytes = 16384;           // bytes of one LDS item stage
 constexpr int kRing = 4;                     // item stages in flight
 constexpr int kSortKeys = 512;               // keys of one wave's merge sort
@@ -52,7 +52,14 @@ __device__ __forceinline__ f32x16_t mfma32_bf16(uint4 a, uint4 b, f32x16_t c) {
 template <int D, int KL>
 struct EmbdShape {
   static constexpr int KD = D / 16;                    // K blocks (32x32x16)
+  static constexpr int NB = nb_for(D);
+  static constexpr int VEC_WAVE = 32 * NB;             // query vectors per wave
+  static constexpr int VEC_WG = kWaves * VEC_WAVE;
   static constexpr int ROWCH = D / 8;                  // 16-byte chunks per item row
+  // XOR swizzle of a row's chunks: the 16 rows one 16-lane group reads land
+  // on distinct 16-byte bank slots of each 256-byte LDS line
+  static constexpr int RPL = D >= 128 ? 1 : 128 / D;   // rows per 256-byte line
+  __device__ static int swz(int n) { return (n / RPL) % ROWCH; }
   static constexpr int ST = kStageBytes / (2 * D);     // items per stage
   static constexpr int SORT = kSortKeys;
   static constexpr int SG = (kSortKeys - KL) / 2;      // staging slots per (list, lane half)
@@ -90,7 +97,7 @@ __global__ __launch_bounds__(64 * kWaves, 1) void k_topk_per_embd(
   if (total % 8 == 0) L = (blockIdx.x >> 3) + (total >> 3) * (blockIdx.x & 7);
   const int rg = L % G, unit = L / G;
   const int px = unit % Px, r = unit / Px;
-  const int vwave = rg * kVecPerWG + wave * kVecPerWave;   // first query vector of the wave
+  const int vwave = rg * S::VEC_WG + wave * S::VEC_WAVE;   // first query vector of the wave
   const int nr0 = r * range_len, nr1 = min(N, nr0 + range_len);
   const int nstages = nr1 > nr0 ? (nr1 - nr0 + S::ST - 1) / S::ST : 0;
 
@@ -102,7 +109,7 @@ __global__ __launch_bounds__(64 * kWaves, 1) void k_topk_per_embd(
     for (int blk = wave; blk < kStageBytes / 1024; blk += kWaves) {
       const int pos = blk * 64 + lane;
       const int n = pos / S::ROWCH, phys = pos % S::ROWCH;
-      const int cc = phys ^ (n % S::ROWCH);
+      const int cc = phys ^ S::swz(n);
       const int item = min(n0 + n, N - 1);
       const bf16_t* src = X + static_cast<long>(item) * D + 8 * cc;
       __builtin_amdgcn_global_load_lds((glb_void_t*)src, (lds_void_t*)(sX + buf * kStageBytes + blk * 1024),
@@ -112,9 +119,9 @@ __global__ __launch_bounds__(64 * kWaves, 1) void k_topk_per_embd(
   for (int t = 0; t < kRing - 1 && t < nstages; ++t) stage(t, t);
 
   // query vectors as B operands: column = lane % 32 within each block
-  uint4 qop[kNB][S::KD];
+  uint4 qop[S::NB][S::KD];
 #pragma unroll
-  for (int nb = 0; nb < kNB; ++nb) {
+  for (int nb = 0; nb < S::NB; ++nb) {
     const int v = vwave + 32 * nb + col;
 #pragma unroll
     for (int kk = 0; kk < S::KD; ++kk)
@@ -128,12 +135,12 @@ __global__ __launch_bounds__(64 * kWaves, 1) void k_topk_per_embd(
   // per-lane state.  Scan 1: running bucket maximum.  Scan 2: threshold
   // (float score every appended key reaches), staging count, and whether the
   // list has been merged into (it is empty otherwise).
-  bool vok[kNB];
-  float th[kNB], bm[kNB];
-  int cnt[kNB];
-  bool merged[kNB];
+  bool vok[S::NB];
+  float th[S::NB], bm[S::NB];
+  int cnt[S::NB];
+  bool merged[S::NB];
 #pragma unroll
-  for (int nb = 0; nb < kNB; ++nb) {
+  for (int nb = 0; nb < S::NB; ++nb) {
     vok[nb] = vwave + 32 * nb + col < nvec;
     bm[nb] = -__builtin_inff();
     cnt[nb] = 0;
@@ -190,10 +197,9 @@ __global__ __launch_bounds__(64 * kWaves, 1) void k_topk_per_embd(
   };
 
   // stage 0 complete; the copies of later stages may still be in flight
-  if (nstages >= kRing - 1) __builtin_amdgcn_s_waitcnt(waitcnt_vm((kRing - 2) * S::LOADS));
-  else if (nstages == 2) __builtin_amdgcn_s_waitcnt(waitcnt_vm(S::LOADS));
-  else __builtin_amdgcn_s_waitcnt(0);
-  __syncthreads();
+  if (nstages >= kRing - 1) ring_barrier<(kRing - 2) * S::LOADS>();
+  else if (nstages == 2) ring_barrier<S::LOADS>();
+  else ring_barrier<0>();
 
   int tile = 0;                                   // tile index within the range
   for (int t = 0; t < nstages; ++t) {
@@ -202,15 +208,15 @@ __global__ __launch_bounds__(64 * kWaves, 1) void k_topk_per_embd(
     for (int tt = 0; tt < S::ST / 32; ++tt, ++tile) {
       const int n = 32 * tt + col;                    // A-operand row = item
       const int n0 = nr0 + 32 * tile;                 // first item of the tile
-      f32x16_t acc[kNB];
+      f32x16_t acc[S::NB];
 #pragma unroll
-      for (int nb = 0; nb < kNB; ++nb) acc[nb] = f32x16_t{};
+      for (int nb = 0; nb < S::NB; ++nb) acc[nb] = f32x16_t{};
       const unsigned char* rowp = xs + n * (2 * D);
 #pragma unroll
       for (int kk = 0; kk < S::KD; ++kk) {
-        const uint4 xa = *reinterpret_cast<const uint4*>(rowp + 16 * ((2 * kk + half) ^ (n % S::ROWCH)));
+        const uint4 xa = *reinterpret_cast<const uint4*>(rowp + 16 * ((2 * kk + half) ^ S::swz(n)));
 #pragma unroll
-        for (int nb = 0; nb < kNB; ++nb) acc[nb] = mfma32_bf16(xa, qop[nb][kk], acc[nb]);
+        for (int nb = 0; nb < S::NB; ++nb) acc[nb] = mfma32_bf16(xa, qop[nb][kk], acc[nb]);
       }
       // lane (c, h) register v holds item n0 + (v/4)*8 + 4h + v%4 of list c;
       // items past the range end (last tile only) become -inf
@@ -223,12 +229,12 @@ __global__ __launch_bounds__(64 * kWaves, 1) void k_topk_per_embd(
           const bool ok = n0 + (v >> 2) * 8 + 4 * half + (v & 3) < nr1;
           vmask |= ok ? (1u << v) : 0u;
 #pragma unroll
-          for (int nb = 0; nb < kNB; ++nb) acc[nb][v] = ok ? acc[nb][v] : -__builtin_inff();
+          for (int nb = 0; nb < S::NB; ++nb) acc[nb][v] = ok ? acc[nb][v] : -__builtin_inff();
         }
       }
-      float m[kNB];
+      float m[S::NB];
 #pragma unroll
-      for (int nb = 0; nb < kNB; ++nb) {
+      for (int nb = 0; nb < S::NB; ++nb) {
         float a0 = fmaxf(fmaxf(acc[nb][0], acc[nb][1]), acc[nb][2]);
         float a1 = fmaxf(fmaxf(acc[nb][3], acc[nb][4]), acc[nb][5]);
         float a2 = fmaxf(fmaxf(acc[nb][6], acc[nb][7]), acc[nb][8]);
@@ -238,11 +244,11 @@ __global__ __launch_bounds__(64 * kWaves, 1) void k_topk_per_embd(
       }
       if (!SCAN2) {
 #pragma unroll
-        for (int nb = 0; nb < kNB; ++nb) bm[nb] = fmaxf(bm[nb], m[nb]);
+        for (int nb = 0; nb < S::NB; ++nb) bm[nb] = fmaxf(bm[nb], m[nb]);
         if ((tile + 1) % bucket_tiles == 0) {
           const int bk = tile / bucket_tiles;
 #pragma unroll
-          for (int nb = 0; nb < kNB; ++nb) {
+          for (int nb = 0; nb < S::NB; ++nb) {
             if (vok[nb]) bucket_ptr(nb)[bk] = bm[nb];
             bm[nb] = -__builtin_inff();
           }
@@ -251,11 +257,11 @@ __global__ __launch_bounds__(64 * kWaves, 1) void k_topk_per_embd(
       }
       bool hit = false;
 #pragma unroll
-      for (int nb = 0; nb < kNB; ++nb) hit = hit || m[nb] >= th[nb];
+      for (int nb = 0; nb < S::NB; ++nb) hit = hit || m[nb] >= th[nb];
       if (__ballot(hit) == 0ull) continue;
       // append survivors to the lane's own staging region
 #pragma unroll
-      for (int nb = 0; nb < kNB; ++nb) {
+      for (int nb = 0; nb < S::NB; ++nb) {
         if (m[nb] >= th[nb]) {
           uint64_t* sp = stg_ptr(nb, col, half);
 #pragma unroll
@@ -270,7 +276,7 @@ __global__ __launch_bounds__(64 * kWaves, 1) void k_topk_per_embd(
       }
       // merge lists whose staging could overflow on the next tile
 #pragma unroll
-      for (int nb = 0; nb < kNB; ++nb) {
+      for (int nb = 0; nb < S::NB; ++nb) {
         uint64_t need = __ballot(cnt[nb] > S::SG - 16);
         while (need) {
           const int c = __builtin_ctzll(need) & 31;
@@ -283,18 +289,19 @@ __global__ __launch_bounds__(64 * kWaves, 1) void k_topk_per_embd(
     // the barrier that ended iteration t-1), then wait for stage t+1
     if (t + kRing - 1 < nstages) {
       stage(t + kRing - 1, (t + kRing - 1) % kRing);
-      __builtin_amdgcn_s_waitcnt(waitcnt_vm((kRing - 2) * S::LOADS));
+      ring_barrier<(kRing - 2) * S::LOADS>();
+    } else if (t + kRing - 2 < nstages) {
+      ring_barrier<(kRing - 3) * S::LOADS>();   // stages t+2 .. end are in flight
     } else {
-      __builtin_amdgcn_s_waitcnt(0);
+      ring_barrier<0>();
     }
-    __syncthreads();
   }
   if (!SCAN2) {
     // the last partial bucket, then -inf for buckets past the range end
     const int ntiles = tile;
     const int done = ntiles / bucket_tiles;
 #pragma unroll
-    for (int nb = 0; nb < kNB; ++nb) {
+    for (int nb = 0; nb < S::NB; ++nb) {
       if (!vok[nb]) continue;
       float* bp = bucket_ptr(nb);
       int bk = done;
@@ -307,7 +314,7 @@ __global__ __launch_bounds__(64 * kWaves, 1) void k_topk_per_embd(
   // list when they fit; the others are merged
   __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "agent");
 #pragma unroll
-  for (int nb = 0; nb < kNB; ++nb) {
+  for (int nb = 0; nb < S::NB; ++nb) {
     const int other = __shfl_xor(cnt[nb], 32);
     const int c0 = half == 0 ? cnt[nb] : other;
     const int c1 = half == 0 ? other : cnt[nb];
@@ -319,7 +326,7 @@ __global__ __launch_bounds__(64 * kWaves, 1) void k_topk_per_embd(
     }
   }
 #pragma unroll
-  for (int nb = 0; nb < kNB; ++nb) {
+  for (int nb = 0; nb < S::NB; ++nb) {
     uint64_t need = __ballot(cnt[nb] > 0);
     while (need) {
       const int c = __builtin_ctzll(need) & 31;
@@ -370,7 +377,8 @@ int per_embd_stage_cap() { return 2 * kSGMax; }
 
 void per_embd_grid(const DevProb& pr, PerEmbdGrid& g) {
   const int nvec = pr.B * pr.Pq;
-  g.G = (nvec + kVecPerWG - 1) / kVecPerWG;
+  const int vec_wg = kWaves * 32 * nb_for(pr.d);
+  g.G = (nvec + vec_wg - 1) / vec_wg;
   const int units = g.G * pr.Px;
   int R = std::max(1, (256 + units - 1) / units);
   R = std::min(R, std::max(1, pr.N / 4096));

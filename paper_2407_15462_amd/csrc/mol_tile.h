@@ -86,11 +86,30 @@ __device__ __forceinline__ int lane_base(int g, int PX) { return (4 * (g & 1) + 
 // of later stages, vmcnt <= (their count) means every older load is done.
 constexpr int waitcnt_vm(int n) { return (n & 0xF) | ((n >> 4) << 14) | (0x7 << 4) | (0xF << 8); }
 
-// LDS fence for exchanges between lanes of one wave.
+// LDS exchange point between lanes of one wave.  LDS operations of a wave
+// execute in issue order, so waiting for the wave's own LDS accesses
+// (lgkmcnt(0)) and stopping the compiler from moving memory accesses across
+// is enough; a memory fence would also wait for every outstanding global
+// load (vmcnt(0)), draining the LDS ring's prefetches.
 __device__ __forceinline__ void wave_lds_sync() {
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(0xF | (0x7 << 4) | (0x3 << 14));   // lgkmcnt(0) only
   __builtin_amdgcn_wave_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+  asm volatile("" ::: "memory");
+}
+
+// Workgroup barrier of the LDS ring: waits until at most VM of this wave's
+// vector-memory operations are outstanding (its older direct-to-LDS copies
+// have landed) and its LDS accesses are done, then joins the barrier.
+// Unlike __syncthreads() it carries no memory fence, whose vmcnt(0) would
+// also wait for the copies of later stages.
+template <int VM>
+__device__ __forceinline__ void ring_barrier() {
+  static_assert(VM >= 0 && VM < 64, "vmcnt range");
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt((VM & 0xF) | ((VM >> 4) << 14) | (0x7 << 4));   // lgkmcnt(0)
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
 }
 
 typedef __attribute__((address_space(3))) uint64_t lds_u64_t;
