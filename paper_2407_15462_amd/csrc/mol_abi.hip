@@ -277,7 +277,7 @@ PerEmbdPlan plan_per_embd(const DevProb& pr, int kp) {
   StreamPlan& s = f.s;
   s.rows = pr.B * pr.P;
   s.k = kp;
-  const long L0 = static_cast<long>(f.g.R) * f.KL;
+  const long L0 = static_cast<long>(f.g.s2.R) * f.KL;
   const int S0 = segment_size_for(static_cast<int>(L0), kp);
   s.strideA = L0;
   s.strideB = std::max<long>((L0 + S0 - 1) / S0 * kp, kp);
@@ -285,8 +285,8 @@ PerEmbdPlan plan_per_embd(const DevProb& pr, int kp) {
   s.offA = off;     off = align_up(off + 8ul * s.rows * s.strideA);
   s.offB = off;     off = align_up(off + 8ul * s.rows * s.strideB);
   f.offFinal = off; off = align_up(off + 8ul * s.rows * kp);
-  f.offStg = off;   off = align_up(off + 8ul * s.rows * f.g.R * per_embd_stage_cap());
-  f.offBmax = off;  off = align_up(off + 4ul * s.rows * f.g.R * 2 * f.g.nbk);
+  f.offStg = off;   off = align_up(off + 8ul * s.rows * f.g.s2.R * per_embd_stage_cap());
+  f.offBmax = off;  off = align_up(off + 4ul * s.rows * f.g.s1.R * 2 * f.g.nbk);
   f.offThr = off;   off = align_up(off + 4ul * s.rows);
   f.bytes = off;
   return f;
@@ -430,7 +430,7 @@ int mol_topk_per_embd(const mol_problem* prob, int32_t kprime, float* out_dot, i
     float* thr = reinterpret_cast<float*>(w + f.offThr);
     MOL_TIMED_LAUNCH(MOL_OP_TOPK_PER_EMBD, st, launch_per_embd(pr, kprime, f.g, bmax, thr, lists, stg, st),
                      "per-component top-k'");
-    if ((rc = reduce_rows(f.s, w, static_cast<long>(f.g.R) * f.KL, fin, kprime, st))) return rc;
+    if ((rc = reduce_rows(f.s, w, static_cast<long>(f.g.s2.R) * f.KL, fin, kprime, st))) return rc;
     MOL_TRY_HIP(launch_decode(fin, kprime, rows, kprime, out_dot, out_idx, st), "decode");
     return MOL_OK;
   }

@@ -79,7 +79,8 @@ __global__ __launch_bounds__(64 * kWaves, 1) void k_mol_fused(
   uint32_t* sCb = reinterpret_cast<uint32_t*>(smem + S::LDS_X + S::LDS_AX);
   uint64_t* sTop = reinterpret_cast<uint64_t*>(smem + S::LDS_X + S::LDS_AX + S::LDS_CB);
 
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform
   const int c = lane & 15, g = lane >> 4;
   const int base = lane_base(g, PX);
   int r, qg;
@@ -114,7 +115,7 @@ __global__ __launch_bounds__(64 * kWaves, 1) void k_mol_fused(
       const int item = min(n0 + n, N - 1);
       const bf16_t* src = X + (static_cast<long>(px) * N + item) * D + 8 * cc;
       unsigned char* dst = sX + buf * S::XSTAGE + blk * 1024;
-      __builtin_amdgcn_global_load_lds((glb_void_t*)src, (lds_void_t*)dst, 16, 0, 0);
+      copy16_to_lds(src, lds_addr(dst));
     }
     for (int blk = wave; blk < S::ABLOCKS; blk += kWaves) {
       const int pos = blk * 64 + lane;
@@ -123,7 +124,7 @@ __global__ __launch_bounds__(64 * kWaves, 1) void k_mol_fused(
       const int item = min(n0 + n, N - 1);
       const float* src = pr.a_x + static_cast<long>(item) * P + 4 * cc;
       unsigned char* dst = sAx + buf * S::ASTAGE + blk * 1024;
-      __builtin_amdgcn_global_load_lds((glb_void_t*)src, (lds_void_t*)dst, 16, 0, 0);
+      copy16_to_lds(src, lds_addr(dst));
     }
   };
   for (int t = 0; t < kRing - 1 && t < ntiles; ++t) stage(t, t);

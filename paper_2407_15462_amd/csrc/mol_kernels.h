@@ -48,15 +48,18 @@ namespace mol {
 // starting threshold, and a threshold scan with staged merges
 // (bf16, d in {64, 128}, k' <= 256).
 struct PerEmbdGrid {
-  int R = 0, range_len = 0, G = 0;   // item ranges, items per range, vector groups
-  int bucket_tiles = 0, nbk = 0;     // 32-item tiles per bucket, buckets per (range, half)
+  struct Scan {
+    int R = 0, range_len = 0, G = 0;   // item ranges, items per range, vector groups
+  };
+  Scan s1, s2;                         // bucket scan, threshold scan
+  int bucket_tiles = 0, nbk = 0;       // 32-item tiles per bucket, buckets per (range, half)
 };
 bool per_embd_supported(const DevProb& pr, int kp);
 int per_embd_list_cap(int kp);
 int per_embd_stage_cap();
 void per_embd_grid(const DevProb& pr, PerEmbdGrid& g);
-// bmax: [B*Pq*Px][R][2][nbk] floats; thr: [B*Pq*Px] floats;
-// lists: [B*Pq*Px][R][KL] keys; stg: [B*Pq*Px][R][stage_cap] keys.
+// bmax: [B*Pq*Px][s1.R][2][nbk] floats; thr: [B*Pq*Px] floats;
+// lists: [B*Pq*Px][s2.R][KL] keys; stg: [B*Pq*Px][s2.R][stage_cap] keys.
 hipError_t launch_per_embd(const DevProb& pr, int kp, const PerEmbdGrid& g, float* bmax, float* thr,
                            uint64_t* lists, uint64_t* stg, hipStream_t st);
 

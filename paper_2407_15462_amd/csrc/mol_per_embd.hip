@@ -24,6 +24,8 @@
 // Both scans evaluate bit-identical dot products (same instructions, same
 // accumulation order), so the bound is exact.  Lists of several item ranges
 // are merged afterwards by segmented sorts.
+#include <type_traits>
+
 #include "mol_tile.h"
 
 namespace mol {
@@ -35,9 +37,10 @@ namespace {
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
 constexpr int kWaves = 8;
-// query-vector blocks of 32 per wave: 4 at d = 64, 2 at d = 128 (B operands
-// stay in registers)
-constexpr int nb_for(int d) { return d >= 128 ? 2 : 4; }
+// query-vector blocks of 32 per wave, chosen so that the B operands and two
+// tiles' accumulators stay in registers: 4 in the bucket scan at d = 64,
+// 2 otherwise (the threshold scan also keeps staging state)
+constexpr int nb_for(int d, bool scan2) { return (d >= 128 || scan2) ? 2 : 4; }
 constexpr int kStageBytes = 16384;           // bytes of one LDS item stage
 constexpr int kRing = 4;                     // item stages in flight
 constexpr int kSortKeys = 512;               // keys of one wave's merge sort
@@ -49,10 +52,10 @@ __device__ __forceinline__ f32x16_t mfma32_bf16(uint4 a, uint4 b, f32x16_t c) {
                                                  __builtin_bit_cast(bf16x8_t, b), c, 0, 0, 0);
 }
 
-template <int D, int KL>
+template <int D, int KL, bool SCAN2>
 struct EmbdShape {
   static constexpr int KD = D / 16;                    // K blocks (32x32x16)
-  static constexpr int NB = nb_for(D);
+  static constexpr int NB = nb_for(D, SCAN2);
   static constexpr int VEC_WAVE = 32 * NB;             // query vectors per wave
   static constexpr int VEC_WG = kWaves * VEC_WAVE;
   static constexpr int ROWCH = D / 8;                  // 16-byte chunks per item row
@@ -75,6 +78,7 @@ struct EmbdShape {
 
 // Grid: WG -> (vector group, px, range).  WGs sharing (px, range) are placed
 // on the same XCD (WG id mod 8) when the grid allows it.
+// R, range_len, G: this scan's item ranges and query-vector groups.
 // bmax: [nvec * Px][R][2][nbk] bucket maxima (scan 1 writes, scan 2 unused);
 // thr: [nvec * Px] starting thresholds (scan 2 reads);
 // lists: [nvec * Px][R][KL] keys; stg: [nvec * Px][R][2][SG] keys (scan 2).
@@ -83,12 +87,13 @@ __global__ __launch_bounds__(64 * kWaves, 1) void k_topk_per_embd(
     DevProb pr, int kp, int R, int range_len, int G, int bucket_tiles, int nbk,
     float* __restrict__ bmax, const float* __restrict__ thr, uint64_t* __restrict__ lists,
     uint64_t* __restrict__ stg) {
-  using S = EmbdShape<D, KL>;
+  using S = EmbdShape<D, KL, SCAN2>;
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   unsigned char* sX = smem;
   uint64_t* sSort = reinterpret_cast<uint64_t*>(smem + S::LDS_X);
 
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform
   const int col = lane & 31, half = lane >> 5;
   const int Px = pr.Px, N = pr.N;
   const int nvec = pr.B * pr.Pq;               // query vectors
@@ -112,8 +117,7 @@ __global__ __launch_bounds__(64 * kWaves, 1) void k_topk_per_embd(
       const int cc = phys ^ S::swz(n);
       const int item = min(n0 + n, N - 1);
       const bf16_t* src = X + static_cast<long>(item) * D + 8 * cc;
-      __builtin_amdgcn_global_load_lds((glb_void_t*)src, (lds_void_t*)(sX + buf * kStageBytes + blk * 1024),
-                                       16, 0, 0);
+      copy16_to_lds(src, lds_addr(sX + buf * kStageBytes + blk * 1024));
     }
   };
   for (int t = 0; t < kRing - 1 && t < nstages; ++t) stage(t, t);
@@ -169,20 +173,24 @@ __global__ __launch_bounds__(64 * kWaves, 1) void k_topk_per_embd(
     const uint64_t* s1 = stg_ptr(nb, c, 1);
     // every slot loads from a valid address (branch-free, so all loads are
     // in flight together); slots past the staged counts are cleared
-    uint64_t vals[S::SORT / 64];
+    constexpr int kBatch = 4;                     // loads in flight per lane
 #pragma unroll
-    for (int j = 0; j < S::SORT / 64; ++j) {
-      const int i = lane + 64 * j;
-      const int a = i - KL, b = i - KL - S::SG;
-      const uint64_t* src = i < KL ? lp + i : (a < S::SG ? s0 + max(a, 0) : s1 + min(max(b, 0), S::SG - 1));
-      vals[j] = *src;
-    }
+    for (int j0 = 0; j0 < S::SORT / 64; j0 += kBatch) {
+      uint64_t vals[kBatch];
 #pragma unroll
-    for (int j = 0; j < S::SORT / 64; ++j) {
-      const int i = lane + 64 * j;
-      const int a = i - KL, b = i - KL - S::SG;
-      const bool keep = i < KL || (a < S::SG ? a < c0 : (b < S::SG && b < c1));
-      mySort[i] = keep ? vals[j] : 0ull;
+      for (int j = 0; j < kBatch; ++j) {
+        const int i = lane + 64 * (j0 + j);
+        const int a = i - KL, b = i - KL - S::SG;
+        const uint64_t* src = i < KL ? lp + i : (a < S::SG ? s0 + max(a, 0) : s1 + min(max(b, 0), S::SG - 1));
+        vals[j] = *src;
+      }
+#pragma unroll
+      for (int j = 0; j < kBatch; ++j) {
+        const int i = lane + 64 * (j0 + j);
+        const int a = i - KL, b = i - KL - S::SG;
+        const bool keep = i < KL || (a < S::SG ? a < c0 : (b < S::SG && b < c1));
+        mySort[i] = keep ? vals[j] : 0ull;
+      }
     }
     wave_lds_sync();
     wave_sort<S::SORT>((lds_u64_t*)mySort, lane);
@@ -201,92 +209,104 @@ __global__ __launch_bounds__(64 * kWaves, 1) void k_topk_per_embd(
   else if (nstages == 2) ring_barrier<S::LOADS>();
   else ring_barrier<0>();
 
-  int tile = 0;                                   // tile index within the range
-  for (int t = 0; t < nstages; ++t) {
-    const int buf = t % kRing;
-    const unsigned char* xs = sX + buf * kStageBytes;
-    for (int tt = 0; tt < S::ST / 32; ++tt, ++tile) {
-      const int n = 32 * tt + col;                    // A-operand row = item
-      const int n0 = nr0 + 32 * tile;                 // first item of the tile
-      f32x16_t acc[S::NB];
+  // Tiles are software-pipelined in pairs: the MFMAs of one tile are issued
+  // before the threshold / bucket work of the previous one, so a wave keeps
+  // its matrix core busy while its VALU works.  Stages hold an even number
+  // of tiles, so a stage boundary always falls between pairs.
+  constexpr int TPS = S::ST / 32;                  // tiles per stage
+  static_assert(TPS % 2 == 0, "stages hold whole tile pairs");
+  const int ntiles = nstages * TPS;               // includes masked tail tiles
+  auto mma = [&](int j, f32x16_t(&acc)[S::NB]) {
+    const unsigned char* xs = sX + ((j / TPS) % kRing) * kStageBytes;
+    const int n = 32 * (j % TPS) + col;             // A-operand row = item
+    const unsigned char* rowp = xs + n * (2 * D);
 #pragma unroll
-      for (int nb = 0; nb < S::NB; ++nb) acc[nb] = f32x16_t{};
-      const unsigned char* rowp = xs + n * (2 * D);
+    for (int nb = 0; nb < S::NB; ++nb) acc[nb] = f32x16_t{};
 #pragma unroll
-      for (int kk = 0; kk < S::KD; ++kk) {
-        const uint4 xa = *reinterpret_cast<const uint4*>(rowp + 16 * ((2 * kk + half) ^ S::swz(n)));
+    for (int kk = 0; kk < S::KD; ++kk) {
+      const uint4 xa = *reinterpret_cast<const uint4*>(rowp + 16 * ((2 * kk + half) ^ S::swz(n)));
 #pragma unroll
-        for (int nb = 0; nb < S::NB; ++nb) acc[nb] = mfma32_bf16(xa, qop[nb][kk], acc[nb]);
+      for (int nb = 0; nb < S::NB; ++nb) acc[nb] = mfma32_bf16(xa, qop[nb][kk], acc[nb]);
+    }
+  };
+  // Threshold / bucket work of tile j.  RAGGED: the tile may reach past the
+  // range end (items there become -inf and are never staged).
+  int bcount = 0, bk = 0;                         // scan 1: tiles in the open bucket, its index
+  auto process = [&](auto ragged_tag, int j, f32x16_t(&acc)[S::NB]) {
+    constexpr bool RAGGED = decltype(ragged_tag)::value;
+    const int n0 = nr0 + 32 * j;                    // first item of the tile
+    // lane (c, h) register v holds item n0 + (v/4)*8 + 4h + v%4 of list c
+    uint32_t vmask = 0xFFFFu;
+    if constexpr (RAGGED) {
+      vmask = 0u;
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const bool ok = n0 + (v >> 2) * 8 + 4 * half + (v & 3) < nr1;
+        vmask |= ok ? (1u << v) : 0u;
+#pragma unroll
+        for (int nb = 0; nb < S::NB; ++nb) acc[nb][v] = ok ? acc[nb][v] : -__builtin_inff();
       }
-      // lane (c, h) register v holds item n0 + (v/4)*8 + 4h + v%4 of list c;
-      // items past the range end (last tile only) become -inf
-      const bool ragged = n0 + 32 > nr1;
-      uint32_t vmask = 0xFFFFu;
-      if (ragged) {
-        vmask = 0u;
+    }
+    float m[S::NB];
+#pragma unroll
+    for (int nb = 0; nb < S::NB; ++nb) {
+      float a0 = fmaxf(fmaxf(acc[nb][0], acc[nb][1]), acc[nb][2]);
+      float a1 = fmaxf(fmaxf(acc[nb][3], acc[nb][4]), acc[nb][5]);
+      float a2 = fmaxf(fmaxf(acc[nb][6], acc[nb][7]), acc[nb][8]);
+      float a3 = fmaxf(fmaxf(acc[nb][9], acc[nb][10]), acc[nb][11]);
+      float a4 = fmaxf(fmaxf(acc[nb][12], acc[nb][13]), acc[nb][14]);
+      m[nb] = fmaxf(fmaxf(fmaxf(a0, a1), a2), fmaxf(fmaxf(a3, a4), acc[nb][15]));
+    }
+    if constexpr (!SCAN2) {
+#pragma unroll
+      for (int nb = 0; nb < S::NB; ++nb) bm[nb] = fmaxf(bm[nb], m[nb]);
+      if (++bcount == bucket_tiles) {
+#pragma unroll
+        for (int nb = 0; nb < S::NB; ++nb) {
+          if (vok[nb]) bucket_ptr(nb)[bk] = bm[nb];
+          bm[nb] = -__builtin_inff();
+        }
+        bcount = 0;
+        ++bk;
+      }
+      return;
+    }
+    bool hit = false;
+#pragma unroll
+    for (int nb = 0; nb < S::NB; ++nb) hit = hit || m[nb] >= th[nb];
+    if (__ballot(hit) == 0ull) return;
+    // append survivors to the lane's own staging region
+#pragma unroll
+    for (int nb = 0; nb < S::NB; ++nb) {
+      if (m[nb] >= th[nb]) {
+        uint64_t* sp = stg_ptr(nb, col, half);
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
-          const bool ok = n0 + (v >> 2) * 8 + 4 * half + (v & 3) < nr1;
-          vmask |= ok ? (1u << v) : 0u;
-#pragma unroll
-          for (int nb = 0; nb < S::NB; ++nb) acc[nb][v] = ok ? acc[nb][v] : -__builtin_inff();
-        }
-      }
-      float m[S::NB];
-#pragma unroll
-      for (int nb = 0; nb < S::NB; ++nb) {
-        float a0 = fmaxf(fmaxf(acc[nb][0], acc[nb][1]), acc[nb][2]);
-        float a1 = fmaxf(fmaxf(acc[nb][3], acc[nb][4]), acc[nb][5]);
-        float a2 = fmaxf(fmaxf(acc[nb][6], acc[nb][7]), acc[nb][8]);
-        float a3 = fmaxf(fmaxf(acc[nb][9], acc[nb][10]), acc[nb][11]);
-        float a4 = fmaxf(fmaxf(acc[nb][12], acc[nb][13]), acc[nb][14]);
-        m[nb] = fmaxf(fmaxf(fmaxf(a0, a1), a2), fmaxf(fmaxf(a3, a4), acc[nb][15]));
-      }
-      if (!SCAN2) {
-#pragma unroll
-        for (int nb = 0; nb < S::NB; ++nb) bm[nb] = fmaxf(bm[nb], m[nb]);
-        if ((tile + 1) % bucket_tiles == 0) {
-          const int bk = tile / bucket_tiles;
-#pragma unroll
-          for (int nb = 0; nb < S::NB; ++nb) {
-            if (vok[nb]) bucket_ptr(nb)[bk] = bm[nb];
-            bm[nb] = -__builtin_inff();
+          if (acc[nb][v] >= th[nb] && ((vmask >> v) & 1u)) {
+            const int item = n0 + (v >> 2) * 8 + 4 * half + (v & 3);
+            sp[cnt[nb]] = make_key(acc[nb][v], item);
+            ++cnt[nb];
           }
-        }
-        continue;
-      }
-      bool hit = false;
-#pragma unroll
-      for (int nb = 0; nb < S::NB; ++nb) hit = hit || m[nb] >= th[nb];
-      if (__ballot(hit) == 0ull) continue;
-      // append survivors to the lane's own staging region
-#pragma unroll
-      for (int nb = 0; nb < S::NB; ++nb) {
-        if (m[nb] >= th[nb]) {
-          uint64_t* sp = stg_ptr(nb, col, half);
-#pragma unroll
-          for (int v = 0; v < 16; ++v) {
-            if (acc[nb][v] >= th[nb] && ((vmask >> v) & 1u)) {
-              const int item = n0 + (v >> 2) * 8 + 4 * half + (v & 3);
-              sp[cnt[nb]] = make_key(acc[nb][v], item);
-              ++cnt[nb];
-            }
-          }
-        }
-      }
-      // merge lists whose staging could overflow on the next tile
-#pragma unroll
-      for (int nb = 0; nb < S::NB; ++nb) {
-        uint64_t need = __ballot(cnt[nb] > S::SG - 16);
-        while (need) {
-          const int c = __builtin_ctzll(need) & 31;
-          need &= ~((1ull << c) | (1ull << (c + 32)));
-          merge(nb, c);
         }
       }
     }
-    // refill the buffer read in iteration t-1 (every wave finished it before
-    // the barrier that ended iteration t-1), then wait for stage t+1
+    // merge lists whose staging could overflow on the next tile
+#pragma unroll
+    for (int nb = 0; nb < S::NB; ++nb) {
+      uint64_t need = __ballot(cnt[nb] > S::SG - 16);
+      while (need) {
+        const int c = __builtin_ctzll(need) & 31;
+        need &= ~((1ull << c) | (1ull << (c + 32)));
+        merge(nb, c);
+      }
+    }
+  };
+  using Full = std::false_type;
+  using Ragged = std::true_type;
+  // end of stage t: refill the buffer of stage t-1 (every wave finished
+  // reading it before the barrier that ended stage t-1), then wait for
+  // stage t+1
+  auto stage_end = [&](int t) {
     if (t + kRing - 1 < nstages) {
       stage(t + kRing - 1, (t + kRing - 1) % kRing);
       ring_barrier<(kRing - 2) * S::LOADS>();
@@ -295,18 +315,40 @@ __global__ __launch_bounds__(64 * kWaves, 1) void k_topk_per_embd(
     } else {
       ring_barrier<0>();
     }
+  };
+
+  // Main loop over tile pairs whose tiles (and the next one) hold items
+  // only: the MFMAs of tile j+1 (j+2) are issued next to the threshold work
+  // of tile j (j+1) in one basic block.  The tail (last pair, ragged tiles,
+  // masked tiles of the last stage) runs unpipelined.
+  f32x16_t accA[S::NB], accB[S::NB];
+  const int nfull = (nr1 - nr0) / 32;             // tiles holding items only
+  int j = 0;
+  if (ntiles > 0) mma(0, accA);
+  for (; j + 2 < nfull; j += 2) {
+    mma(j + 1, accB);
+    process(Full{}, j, accA);
+    if ((j + 2) % TPS == 0) stage_end((j + 2) / TPS - 1);
+    mma(j + 2, accA);
+    process(Full{}, j + 1, accB);
+  }
+  if (ntiles > 0) {
+    process(Ragged{}, j, accA);                   // tile j, computed above
+    for (++j; j < ntiles; ++j) {
+      if (j % TPS == 0) stage_end(j / TPS - 1);
+      mma(j, accA);
+      process(Ragged{}, j, accA);
+    }
   }
   if (!SCAN2) {
     // the last partial bucket, then -inf for buckets past the range end
-    const int ntiles = tile;
-    const int done = ntiles / bucket_tiles;
 #pragma unroll
     for (int nb = 0; nb < S::NB; ++nb) {
       if (!vok[nb]) continue;
       float* bp = bucket_ptr(nb);
-      int bk = done;
-      if (ntiles % bucket_tiles != 0) bp[bk++] = bm[nb];
-      for (; bk < nbk; ++bk) bp[bk] = -__builtin_inff();
+      int b = bk;
+      if (bcount != 0) bp[b++] = bm[nb];
+      for (; b < nbk; ++b) bp[b] = -__builtin_inff();
     }
     return;
   }
@@ -375,21 +417,26 @@ bool per_embd_supported(const DevProb& pr, int kp) {
 int per_embd_list_cap(int kp) { return kp <= 128 ? 128 : 256; }
 int per_embd_stage_cap() { return 2 * kSGMax; }
 
-void per_embd_grid(const DevProb& pr, PerEmbdGrid& g) {
+static void scan_grid(const DevProb& pr, bool scan2, PerEmbdGrid::Scan& sc) {
   const int nvec = pr.B * pr.Pq;
-  const int vec_wg = kWaves * 32 * nb_for(pr.d);
-  g.G = (nvec + vec_wg - 1) / vec_wg;
-  const int units = g.G * pr.Px;
+  const int vec_wg = kWaves * 32 * nb_for(pr.d, scan2);
+  sc.G = (nvec + vec_wg - 1) / vec_wg;
+  const int units = sc.G * pr.Px;
   int R = std::max(1, (256 + units - 1) / units);
   R = std::min(R, std::max(1, pr.N / 4096));
-  g.range_len = (pr.N + R - 1) / R;
-  g.range_len = (g.range_len + 127) / 128 * 128;
-  g.R = (pr.N + g.range_len - 1) / g.range_len;
+  sc.range_len = (pr.N + R - 1) / R;
+  sc.range_len = (sc.range_len + 127) / 128 * 128;
+  sc.R = (pr.N + sc.range_len - 1) / sc.range_len;
+}
+
+void per_embd_grid(const DevProb& pr, PerEmbdGrid& g) {
+  scan_grid(pr, false, g.s1);
+  scan_grid(pr, true, g.s2);
   // buckets: as many as fit kMaxBuckets per list over all ranges and halves
-  const int ntiles = g.range_len / 32;
-  g.bucket_tiles = std::max(1, (2 * g.R * ntiles + kMaxBuckets - 1) / kMaxBuckets);
+  const int ntiles = g.s1.range_len / 32;
+  g.bucket_tiles = std::max(1, (2 * g.s1.R * ntiles + kMaxBuckets - 1) / kMaxBuckets);
   g.nbk = (ntiles + g.bucket_tiles - 1) / g.bucket_tiles;
-  while (2 * g.R * g.nbk > kMaxBuckets) {
+  while (2 * g.s1.R * g.nbk > kMaxBuckets) {
     ++g.bucket_tiles;
     g.nbk = (ntiles + g.bucket_tiles - 1) / g.bucket_tiles;
   }
@@ -398,13 +445,14 @@ void per_embd_grid(const DevProb& pr, PerEmbdGrid& g) {
 template <int D, int KL, bool SCAN2>
 static hipError_t launch_pe_t(const DevProb& pr, int kp, const PerEmbdGrid& g, float* bmax, const float* thr,
                               uint64_t* lists, uint64_t* stg, hipStream_t st) {
-  using S = EmbdShape<D, KL>;
+  using S = EmbdShape<D, KL, SCAN2>;
+  const PerEmbdGrid::Scan& sc = SCAN2 ? g.s2 : g.s1;
   auto kern = &k_topk_per_embd<D, KL, SCAN2>;
   hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                      hipFuncAttributeMaxDynamicSharedMemorySize, S::LDS_TOTAL);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(kern, dim3(g.G * pr.Px * g.R), dim3(64 * kWaves), S::LDS_TOTAL, st, pr, kp, g.R,
-                     g.range_len, g.G, g.bucket_tiles, g.nbk, bmax, thr, lists, stg);
+  hipLaunchKernelGGL(kern, dim3(sc.G * pr.Px * sc.R), dim3(64 * kWaves), S::LDS_TOTAL, st, pr, kp, sc.R,
+                     sc.range_len, sc.G, g.bucket_tiles, g.nbk, bmax, thr, lists, stg);
   return hipGetLastError();
 }
 
@@ -415,7 +463,7 @@ static hipError_t launch_pe_d(const DevProb& pr, int kp, const PerEmbdGrid& g, f
   if (e != hipSuccess) return e;
   const int nlists = pr.B * pr.Pq * pr.Px;
   hipLaunchKernelGGL(k_bucket_threshold, dim3((nlists + 3) / 4), dim3(256), 0, st, bmax, nlists,
-                     2 * g.R * g.nbk, kp, thr);
+                     2 * g.s1.R * g.nbk, kp, thr);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   return launch_pe_t<D, KL, true>(pr, kp, g, bmax, thr, lists, stg, st);

@@ -114,6 +114,31 @@ __device__ __forceinline__ void ring_barrier() {
 
 typedef __attribute__((address_space(3))) uint64_t lds_u64_t;
 
+// LDS offset of a pointer into shared memory.
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_void_t*)(p)));
+}
+
+// One lane's 16 bytes of a direct global -> LDS copy of a 1 KB block: lane i
+// writes LDS bytes [lds_block + 16 i, lds_block + 16 i + 16).  lds_block must
+// be wave-uniform.  Issued as inline asm so that the compiler does not see
+// an LDS store: it would otherwise make every later LDS read wait for all
+// outstanding copies (vmcnt(0)), including the prefetches of later stages.
+// The caller tracks completion with counted vmcnt waits (ring_barrier); M0
+// is saved and restored around the copy.
+__device__ __forceinline__ void copy16_to_lds(const void* src, uint32_t lds_block) {
+  uint32_t saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %2\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %1, off\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "v"(src), "s"(lds_block)
+      : "memory");
+}
+
 // Bitonic sort (descending) of SORT keys in LDS by one wave.
 template <int SORT>
 __device__ __noinline__ void wave_sort(lds_u64_t* r, int lane) {
