@@ -41,8 +41,8 @@ constexpr int kWaves = 8;
 // tiles' accumulators stay in registers: 4 in the bucket scan at d = 64,
 // 2 otherwise (the threshold scan also keeps staging state)
 constexpr int nb_for(int d, bool scan2) { return (d >= 128 || scan2) ? 2 : 4; }
-constexpr int kStageBytes = 16384;           // bytes of one LDS item stage
-constexpr int kRing = 4;                     // item stages in flight
+constexpr int kStageBytes = 32768;           // bytes of one LDS item stage
+constexpr int kRing = 3;                     // item stages in flight
 constexpr int kSortKeys = 512;               // keys of one wave's merge sort
 constexpr int kSGMax = (kSortKeys - 128) / 2;  // largest staging region per lane half
 constexpr int kMaxBuckets = 2048;            // bucket maxima per list (all ranges, both halves)
