@@ -41,7 +41,7 @@ struct FusedShape {
   static constexpr int ASTAGE = kTile * P * 4;        // bytes of one a_x stage
   static constexpr int LDS_X = kRing * XSTAGE;
   static constexpr int LDS_AX = kRing * ASTAGE;
-  static constexpr int LDS_CB = kQueriesPerWG * P * 4;
+  static constexpr int LDS_CB = kQueriesPerWG * 16 * 4 * 4;   // [query][row c][tile] (a_q + b2)
   static constexpr int LDS_TOPK = kQueriesPerWG * kTopkRegion * 8;
   static constexpr int LDS_TOTAL = LDS_X + LDS_AX + LDS_CB + LDS_TOPK;
   // 16-byte global->LDS copies per stage, in 1 KB blocks of one wave each
@@ -130,9 +130,13 @@ __global__ __launch_bounds__(64 * kWaves, 1) void k_mol_fused(
   for (int t = 0; t < kRing - 1 && t < ntiles; ++t) stage(t, t);
 
   // ---- per-workgroup constants ----
-  for (int i = tid; i < kQueriesPerWG * P; i += 64 * kWaves) {
-    const int qi = i / P, p = i % P, b = qwg + qi;
-    sCb[i] = split_f16(b < pr.B ? kLog2e * (pr.a_q[static_cast<long>(b) * P + p] + pr.b2[p]) : 0.f);
+  // log2(e) (a_q + b2) as f16 hi + lo, [query][row c][tile pt] so that a
+  // lane reads its four tiles' values with one 16-byte load
+  for (int i = tid; i < kQueriesPerWG * 64; i += 64 * kWaves) {
+    const int qi = i / 64, cc = (i / 4) % 16, pt = i % 4, b = qwg + qi;
+    const int p = Mlp::aug_p(cc, pt);
+    sCb[i] = (b < pr.B && pt < S::PT) ? split_f16(kLog2e * (pr.a_q[static_cast<long>(b) * P + p] + pr.b2[p]))
+                                      : 0u;
   }
   WaveTopk top[2];
   if (!DENSE) {
@@ -167,52 +171,74 @@ __global__ __launch_bounds__(64 * kWaves, 1) void k_mol_fused(
       const int item = nr0 + kTile * t + n;
       const bool item_ok = item < nr1;
 
+      // LDS operands of the step, all issued before the first MFMA so that
+      // one LDS round trip is exposed per step: the X tile (GEMM1 B
+      // operands), a_x and the a_q + b2 blocks
+      uint4 xb[PX][S::KD];
+#pragma unroll
+      for (int px = 0; px < PX; ++px) {
+        const unsigned char* row = xs + (px * kTile + n) * (D * 2);
+#pragma unroll
+        for (int kk = 0; kk < S::KD; ++kk) {
+          const int phys = (4 * kk + g) ^ (n % S::XROWCH);
+          xb[px][kk] = *reinterpret_cast<const uint4*>(row + 16 * phys);
+        }
+      }
+      float4 axv[S::PT];
+#pragma unroll
+      for (int q4 = 0; q4 < S::PT; ++q4) {
+        const int phys = (base / 4 + q4) ^ (n % S::AROWCH);
+        axv[q4] = *reinterpret_cast<const float4*>(as + n * (P * 4) + 16 * phys);
+      }
+      uint4 cbq[2];
+#pragma unroll
+      for (int qb = 0; qb < 2; ++qb)
+        cbq[qb] = *reinterpret_cast<const uint4*>(sCb + ((2 * wave + qb) * 16 + c) * 4);
+      __builtin_amdgcn_sched_barrier(0);
+
       // GEMM1: both queries x 16 items x all px
       f32x4_t acc1[PX];
 #pragma unroll
       for (int px = 0; px < PX; ++px) {
         acc1[px] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-        const unsigned char* row = xs + (px * kTile + n) * (D * 2);
 #pragma unroll
-        for (int kk = 0; kk < S::KD; ++kk) {
-          const int phys = (4 * kk + g) ^ (n % S::XROWCH);
-          acc1[px] = mfma_bf16(qop[kk], *reinterpret_cast<const uint4*>(row + 16 * phys), acc1[px]);
-        }
+        for (int kk = 0; kk < S::KD; ++kk) acc1[px] = mfma_bf16(qop[kk], xb[px][kk], acc1[px]);
       }
-      // separate the two queries: s0[mu], s1[mu] hold p = base(g) + mu
-      float s0[S::RUN], s1[S::RUN];
+      // separate the two queries: s[q][mu] holds p = base(g) + mu
+      float s2[2][S::RUN];
 #pragma unroll
       for (int mu = 0; mu < S::RUN; ++mu) {
         const float a = acc1[mu % PX][mu / PX];
         const float b = acc1[mu % PX][2 + mu / PX];
         auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(a), __float_as_uint(b), false, false);
-        s0[mu] = __uint_as_float(sw[0]);
-        s1[mu] = __uint_as_float(sw[1]);
+        s2[0][mu] = __uint_as_float(sw[0]);
+        s2[1][mu] = __uint_as_float(sw[1]);
       }
       // a_x (scaled by log2 e) in the GEMM3 accumulator layout
       f32x4_t axr[S::PT];
 #pragma unroll
-      for (int q4 = 0; q4 < S::PT; ++q4) {
-        const int phys = (base / 4 + q4) ^ (n % S::AROWCH);
-        const float4 a = *reinterpret_cast<const float4*>(as + n * (P * 4) + 16 * phys);
-        axr[q4] = f32x4_t{kLog2e * a.x, kLog2e * a.y, kLog2e * a.z, kLog2e * a.w};
-      }
-
+      for (int q4 = 0; q4 < S::PT; ++q4)
+        axr[q4] = f32x4_t{kLog2e * axv[q4].x, kLog2e * axv[q4].y, kLog2e * axv[q4].z, kLog2e * axv[q4].w};
+      // the two queries one after the other (keeps the register peak low)
+      float phi[2];
 #pragma unroll
       for (int qb = 0; qb < 2; ++qb) {
-        float s[S::RUN];
+        float sq[1][S::RUN];
 #pragma unroll
-        for (int mu = 0; mu < S::RUN; ++mu) s[mu] = qb == 0 ? s0[mu] : s1[mu];
-        uint32_t cb[S::PT];
+        for (int mu = 0; mu < S::RUN; ++mu) sq[0][mu] = s2[qb][mu];
+        const uint4 cq[1] = {cbq[qb]};
+        float pq[1];
+        mlp.template phi<1>(sq, axr, cq, pq);
+        phi[qb] = pq[0];
+        __builtin_amdgcn_sched_barrier(0);
+      }
 #pragma unroll
-        for (int pt = 0; pt < S::PT; ++pt)
-          cb[pt] = g == 0 ? sCb[(2 * wave + qb) * P + Mlp::aug_p(c, pt)] : 0u;
-        const float phi = mlp.phi(s, axr, cb);
+      for (int qb = 0; qb < 2; ++qb) {
         const int b = qwv + qb;
         if constexpr (DENSE) {
-          if (g == 0 && item_ok && b < pr.B) phi_out[b * phi_stride + (item - n_begin)] = phi;
+          if (g == 0 && item_ok && b < pr.B) phi_out[b * phi_stride + (item - n_begin)] = phi[qb];
         } else {
-          top[qb].offer((g == 0 && item_ok) ? make_key(phi, item) : 0ull, lane);
+          top[qb].offer((g == 0 && item_ok) ? make_key(phi[qb], item) : 0ull, lane);
         }
       }
     }

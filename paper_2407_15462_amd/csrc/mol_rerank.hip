@@ -46,12 +46,14 @@ __global__ __launch_bounds__(64 * kWaves, 2) void k_mol_rerank(
   top.init(sTop + wave * kTopkRegion, k, lane);
   Mlp mlp;
   mlp.load(pr, c, g);
-  uint32_t cb[PT];
+  // log2(e) (a_q + b2) of query b as f16 hi + lo, tile pt in dword pt
+  uint32_t cb[4] = {0u, 0u, 0u, 0u};
 #pragma unroll
   for (int pt = 0; pt < PT; ++pt) {
     const int p = Mlp::aug_p(c, pt);
-    cb[pt] = g == 0 ? split_f16(kLog2e * (pr.a_q[static_cast<long>(b) * P + p] + pr.b2[p])) : 0u;
+    cb[pt] = split_f16(kLog2e * (pr.a_q[static_cast<long>(b) * P + p] + pr.b2[p]));
   }
+  const uint4 cbq[1] = {make_uint4(cb[0], cb[1], cb[2], cb[3])};
   // query b's components as GEMM1 rows 0..7 (rows 8..15 zero)
   uint4 qop[KD];
 #pragma unroll
@@ -84,15 +86,16 @@ __global__ __launch_bounds__(64 * kWaves, 2) void k_mol_rerank(
 #pragma unroll
       for (int kk = 0; kk < KD; ++kk) acc1[px] = mfma_bf16(qop[kk], xop[px][kk], acc1[px]);
     }
-    float s[RUN];
+    float s[1][RUN];
 #pragma unroll
     for (int mu = 0; mu < RUN; ++mu) {
       auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(acc1[mu % PX][mu / PX]),
                                                  __float_as_uint(acc1[mu % PX][2 + mu / PX]), false, false);
-      s[mu] = __uint_as_float(sw[0]);
+      s[0][mu] = __uint_as_float(sw[0]);
     }
-    const float phi = mlp.phi(s, axr, cb);
-    top.offer((g == 0 && ok) ? make_key(phi, item) : 0ull, lane);
+    float phi[1];
+    mlp.template phi<1>(s, axr, cbq, phi);
+    top.offer((g == 0 && ok) ? make_key(phi[0], item) : 0ull, lane);
   }
   top.flush(lane);
   uint64_t* dst = partial + (static_cast<long>(b) * nchunks + j) * k;

@@ -45,9 +45,13 @@ __device__ __forceinline__ f32x4_t mfma_f16(uint4 a, uint4 b, f32x4_t c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8_t, a),
                                                 __builtin_bit_cast(f16x8_t, b), c, 0, 0, 0);
 }
+
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+typedef _Float16 f16x2_t __attribute__((ext_vector_type(2)));
+// (a, b) rounded to f16 (nearest-even) in the low / high half: one
+// v_cvt_pk_f16_f32 on gfx950
 __device__ __forceinline__ uint32_t pack_f16(float a, float b) {
-  return static_cast<uint32_t>(__builtin_bit_cast(uint16_t, static_cast<_Float16>(a))) |
-         (static_cast<uint32_t>(__builtin_bit_cast(uint16_t, static_cast<_Float16>(b))) << 16);
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{a, b}, f16x2_t));
 }
 // f16 bits of -scale * w (sign flipped on the integer side)
 __device__ __forceinline__ uint32_t neg_bf16_to_f16_bits(bf16_t w, float scale) {
@@ -210,10 +214,11 @@ struct MolMlp {
   static constexpr int JT = H / 16;   // output tiles of GEMM2
   static constexpr int KH = H / 32;   // K blocks of GEMM3
   static constexpr int PT = P / 16;   // output tiles of GEMM3
+  static_assert(PT <= 4, "a_q + b2 operand holds at most 4 tiles");
   uint4 w1op[JT][KP];
   uint4 w2op[PT][KH];
   f32x4_t b1acc[JT];
-  uint4 ones;
+  uint4 ones;                         // 1.0 at K slots 0, 1 (the a_q + b2 block)
 
   __device__ void load(const DevProb& pr, int c, int g) {
     const bf16_t* W1 = static_cast<const bf16_t*>(pr.W1);
@@ -256,13 +261,15 @@ struct MolMlp {
     ones = make_uint4(g == 0 ? 0x3C003C00u : 0u, 0u, 0u, 0u);
   }
 
-  // p of GEMM3 A-operand row 16 pt + c (the a_q + b2 block's rows)
+  // p of output row 16 pt + c of GEMM3 (the a_q + b2 operand's rows)
   __device__ static int aug_p(int c, int pt) { return lane_base(c >> 2, PX) + 4 * pt + (c & 3); }
 
-  // phi for the lane's item.  s: the lane's run of s values; axr: log2(e) a_x
-  // in the GEMM3 accumulator layout; cb[pt]: packed f16 hi/lo of
-  // log2(e) (a_q + b2) at p = aug_p(c, pt) for group-0 lanes, 0 elsewhere.
-  __device__ float phi(const float (&s)[RUN], const f32x4_t (&axr)[PT], const uint32_t (&cb)[PT]) const {
+  // Base-2 gating logits l' of one query for the lane's items (GEMM2 ->
+  // SiLU -> GEMM3).  s: the lane's run of s values; axr: log2(e) a_x in the
+  // GEMM3 accumulator layout; cbq: packed f16 hi/lo of log2(e) (a_q + b2)
+  // at p = aug_p(c, pt) in dword pt (finite in every lane).
+  __device__ void logits(const float (&s)[RUN], const f32x4_t (&axr)[PT], const uint4& cbq,
+                         f32x4_t (&lg)[PT]) const {
     uint4 sop[KP];
 #pragma unroll
     for (int m = 0; m < KP; ++m)
@@ -287,46 +294,73 @@ struct MolMlp {
       hop[m] = make_uint4(pack_f16(hv[0], hv[1]), pack_f16(hv[2], hv[3]), pack_f16(hv[4], hv[5]),
                           pack_f16(hv[6], hv[7]));
     }
-    f32x4_t lg[PT];
+    // the a_q + b2 block: only K slots 0, 1 (dword 0 of the g == 0 lanes)
+    // meet a nonzero B entry
+    const uint32_t cbs[4] = {cbq.x, cbq.y, cbq.z, cbq.w};
 #pragma unroll
     for (int pt = 0; pt < PT; ++pt) {
-      lg[pt] = mfma_f16(make_uint4(cb[pt], 0u, 0u, 0u), ones, axr[pt]);
+      lg[pt] = mfma_f16(make_uint4(cbs[pt], 0u, 0u, 0u), ones, axr[pt]);
 #pragma unroll
       for (int m = 0; m < KH; ++m) lg[pt] = mfma_f16(w2op[pt][m], hop[m], lg[pt]);
     }
-    float den = 0.f, num = 0.f;
+  }
+
+  // sum_p w_p and sum_p w_p s_p over the lane's p (w = 2^(l' - shift)),
+  // two partial sums each to shorten the dependency chains
+  __device__ static void weights(const f32x4_t (&lg)[PT], const float (&s)[RUN], float shift, float& den,
+                                 float& num) {
+    float d[2] = {0.f, 0.f}, n[2] = {0.f, 0.f};
 #pragma unroll
     for (int pt = 0; pt < PT; ++pt)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const float w = __builtin_amdgcn_exp2f(lg[pt][i]);
-        den += w;
-        num = fmaf(w, s[4 * pt + i], num);
+        const float w = __builtin_amdgcn_exp2f(lg[pt][i] - shift);
+        d[i & 1] += w;
+        n[i & 1] = fmaf(w, s[4 * pt + i], n[i & 1]);
       }
-    den = sum_groups(den);
-    num = sum_groups(num);
-    if (!__all(den >= 0x1p-60f && den <= 0x1p60f)) {
-      // logits far from zero: subtract the row maximum first
-      float mx = -__builtin_inff();
+    den = d[0] + d[1];
+    num = n[0] + n[1];
+  }
+
+  // phi for the lane's item under NQ queries.  The queries' chains are
+  // independent and branch-free, so they can be interleaved; a query whose
+  // max-free sum left [2^-60, 2^60] (logits far from zero) is redone with
+  // the row maximum subtracted.
+  template <int NQ>
+  __device__ void phi(const float (&s)[NQ][RUN], const f32x4_t (&axr)[PT], const uint4 (&cbq)[NQ],
+                      float (&out)[NQ]) const {
+    float den[NQ], num[NQ];
 #pragma unroll
-      for (int pt = 0; pt < PT; ++pt)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) mx = fmaxf(mx, lg[pt][i]);
-      mx = max_groups(mx);
-      den = 0.f;
-      num = 0.f;
-#pragma unroll
-      for (int pt = 0; pt < PT; ++pt)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const float w = __builtin_amdgcn_exp2f(lg[pt][i] - mx);
-          den += w;
-          num = fmaf(w, s[4 * pt + i], num);
-        }
-      den = sum_groups(den);
-      num = sum_groups(num);
+    for (int q = 0; q < NQ; ++q) {
+      f32x4_t lg[PT];
+      logits(s[q], axr, cbq[q], lg);
+      weights(lg, s[q], 0.f, den[q], num[q]);
     }
-    return num * __builtin_amdgcn_rcpf(den);
+    bool ok = true;
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) {
+      den[q] = sum_groups(den[q]);
+      num[q] = sum_groups(num[q]);
+      ok = ok && den[q] >= 0x1p-60f && den[q] <= 0x1p60f;
+    }
+    if (!__all(ok)) {
+#pragma unroll
+      for (int q = 0; q < NQ; ++q) {
+        if (__all(den[q] >= 0x1p-60f && den[q] <= 0x1p60f)) continue;
+        f32x4_t lg[PT];
+        logits(s[q], axr, cbq[q], lg);
+        float mx = -__builtin_inff();
+#pragma unroll
+        for (int pt = 0; pt < PT; ++pt)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) mx = fmaxf(mx, lg[pt][i]);
+        weights(lg, s[q], max_groups(mx), den[q], num[q]);
+        den[q] = sum_groups(den[q]);
+        num[q] = sum_groups(num[q]);
+      }
+    }
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) out[q] = num[q] * __builtin_amdgcn_rcpf(den[q]);
   }
 };
 
