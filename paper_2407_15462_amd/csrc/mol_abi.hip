@@ -272,7 +272,7 @@ struct PerEmbdPlan {
 
 PerEmbdPlan plan_per_embd(const DevProb& pr, int kp) {
   PerEmbdPlan f;
-  per_embd_grid(pr, f.g);
+  per_embd_grid(pr, kp, f.g);
   f.KL = per_embd_list_cap(kp);
   StreamPlan& s = f.s;
   s.rows = pr.B * pr.P;
@@ -285,7 +285,7 @@ PerEmbdPlan plan_per_embd(const DevProb& pr, int kp) {
   s.offA = off;     off = align_up(off + 8ul * s.rows * s.strideA);
   s.offB = off;     off = align_up(off + 8ul * s.rows * s.strideB);
   f.offFinal = off; off = align_up(off + 8ul * s.rows * kp);
-  f.offStg = off;   off = align_up(off + 8ul * s.rows * f.g.s2.R * per_embd_stage_cap());
+  f.offStg = off;   off = align_up(off + 8ul * s.rows * f.g.s2.R * per_embd_stage_cap(kp));
   f.offBmax = off;  off = align_up(off + 4ul * s.rows * f.g.s1.R * 2 * f.g.nbk);
   f.offThr = off;   off = align_up(off + 4ul * s.rows);
   f.bytes = off;

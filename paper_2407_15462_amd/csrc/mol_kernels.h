@@ -46,7 +46,7 @@ namespace mol {
 
 // Per-component top-k' with MFMA dots: a bucket-maximum scan, a per-list
 // starting threshold, and a threshold scan with staged merges
-// (bf16, d in {64, 128}, k' <= 256).
+// (bf16, d in {64, 128}, k' <= 1024).
 struct PerEmbdGrid {
   struct Scan {
     int R = 0, range_len = 0, G = 0;   // item ranges, items per range, vector groups
@@ -56,8 +56,8 @@ struct PerEmbdGrid {
 };
 bool per_embd_supported(const DevProb& pr, int kp);
 int per_embd_list_cap(int kp);
-int per_embd_stage_cap();
-void per_embd_grid(const DevProb& pr, PerEmbdGrid& g);
+int per_embd_stage_cap(int kp);
+void per_embd_grid(const DevProb& pr, int kp, PerEmbdGrid& g);
 // bmax: [B*Pq*Px][s1.R][2][nbk] floats; thr: [B*Pq*Px] floats;
 // lists: [B*Pq*Px][s2.R][KL] keys; stg: [B*Pq*Px][s2.R][stage_cap] keys.
 hipError_t launch_per_embd(const DevProb& pr, int kp, const PerEmbdGrid& g, float* bmax, float* thr,

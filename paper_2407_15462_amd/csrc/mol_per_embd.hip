@@ -36,15 +36,15 @@ namespace {
 
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
-constexpr int kWaves = 8;
 // query-vector blocks of 32 per wave, chosen so that the B operands and two
 // tiles' accumulators stay in registers: 4 in the bucket scan at d = 64,
 // 2 otherwise (the threshold scan also keeps staging state)
 constexpr int nb_for(int d, bool scan2) { return (d >= 128 || scan2) ? 2 : 4; }
-constexpr int kStageBytes = 32768;           // bytes of one LDS item stage
+// waves per workgroup: 8, or 4 for lists of 512 / 1024 keys, whose merge
+// sorts need 8 / 16 KB of LDS per wave
+constexpr int waves_for(int kl) { return kl >= 512 ? 4 : 8; }
 constexpr int kRing = 3;                     // item stages in flight
-constexpr int kSortKeys = 512;               // keys of one wave's merge sort
-constexpr int kSGMax = (kSortKeys - 128) / 2;  // largest staging region per lane half
+constexpr int kSGMax = 512;                  // largest staging region per lane half
 constexpr int kMaxBuckets = 2048;            // bucket maxima per list (all ranges, both halves)
 
 __device__ __forceinline__ f32x16_t mfma32_bf16(uint4 a, uint4 b, f32x16_t c) {
@@ -57,21 +57,24 @@ struct EmbdShape {
   static constexpr int KD = D / 16;                    // K blocks (32x32x16)
   static constexpr int NB = nb_for(D, SCAN2);
   static constexpr int VEC_WAVE = 32 * NB;             // query vectors per wave
-  static constexpr int VEC_WG = kWaves * VEC_WAVE;
+  static constexpr int WAVES = waves_for(KL);
+  static constexpr int VEC_WG = WAVES * VEC_WAVE;
+  static constexpr int STAGE_BYTES = WAVES == 8 ? 32768 : 16384;   // bytes of one LDS item stage
   static constexpr int ROWCH = D / 8;                  // 16-byte chunks per item row
   // XOR swizzle of a row's chunks: the 16 rows one 16-lane group reads land
   // on distinct 16-byte bank slots of each 256-byte LDS line
   static constexpr int RPL = D >= 128 ? 1 : 128 / D;   // rows per 256-byte line
   __device__ static int swz(int n) { return (n / RPL) % ROWCH; }
-  static constexpr int ST = kStageBytes / (2 * D);     // items per stage
-  static constexpr int SORT = kSortKeys;
-  static constexpr int SG = (kSortKeys - KL) / 2;      // staging slots per (list, lane half)
-  static constexpr int LOADS = kStageBytes / 1024 / kWaves;   // copies per lane per stage
-  static constexpr int LDS_X = kRing * kStageBytes;
-  static constexpr int LDS_SORT = kWaves * SORT * 8;
+  static constexpr int ST = STAGE_BYTES / (2 * D);     // items per stage
+  static constexpr int SORT = KL <= 256 ? 512 : 2 * KL;  // keys of one wave's merge sort
+  static constexpr int SG = (SORT - KL) / 2;           // staging slots per (list, lane half)
+  static constexpr int LOADS = STAGE_BYTES / 1024 / WAVES;   // copies per lane per stage
+  static constexpr int LDS_X = kRing * STAGE_BYTES;
+  static constexpr int LDS_SORT = WAVES * SORT * 8;
   static constexpr int LDS_TOTAL = LDS_X + LDS_SORT;
   static_assert(ST % 32 == 0, "stage holds whole 32-item tiles");
   static_assert(KL + 2 * SG <= SORT && SG <= kSGMax, "sort region holds list + both staging halves");
+  static_assert(LDS_TOTAL <= 160 * 1024, "LDS budget");
 };
 
 }  // namespace
@@ -83,7 +86,7 @@ struct EmbdShape {
 // thr: [nvec * Px] starting thresholds (scan 2 reads);
 // lists: [nvec * Px][R][KL] keys; stg: [nvec * Px][R][2][SG] keys (scan 2).
 template <int D, int KL, bool SCAN2>
-__global__ __launch_bounds__(64 * kWaves, 1) void k_topk_per_embd(
+__global__ __launch_bounds__(64 * waves_for(KL), 1) void k_topk_per_embd(
     DevProb pr, int kp, int R, int range_len, int G, int bucket_tiles, int nbk,
     float* __restrict__ bmax, const float* __restrict__ thr, uint64_t* __restrict__ lists,
     uint64_t* __restrict__ stg) {
@@ -111,13 +114,13 @@ __global__ __launch_bounds__(64 * kWaves, 1) void k_topk_per_embd(
 
   auto stage = [&](int t, int buf) {
     const int n0 = nr0 + S::ST * t;
-    for (int blk = wave; blk < kStageBytes / 1024; blk += kWaves) {
+    for (int blk = wave; blk < S::STAGE_BYTES / 1024; blk += S::WAVES) {
       const int pos = blk * 64 + lane;
       const int n = pos / S::ROWCH, phys = pos % S::ROWCH;
       const int cc = phys ^ S::swz(n);
       const int item = min(n0 + n, N - 1);
       const bf16_t* src = X + static_cast<long>(item) * D + 8 * cc;
-      copy16_to_lds(src, lds_addr(sX + buf * kStageBytes + blk * 1024));
+      copy16_to_lds(src, lds_addr(sX + buf * S::STAGE_BYTES + blk * 1024));
     }
   };
   for (int t = 0; t < kRing - 1 && t < nstages; ++t) stage(t, t);
@@ -217,7 +220,7 @@ __global__ __launch_bounds__(64 * kWaves, 1) void k_topk_per_embd(
   static_assert(TPS % 2 == 0, "stages hold whole tile pairs");
   const int ntiles = nstages * TPS;               // includes masked tail tiles
   auto mma = [&](int j, f32x16_t(&acc)[S::NB]) {
-    const unsigned char* xs = sX + ((j / TPS) % kRing) * kStageBytes;
+    const unsigned char* xs = sX + ((j / TPS) % kRing) * S::STAGE_BYTES;
     const int n = 32 * (j % TPS) + col;             // A-operand row = item
     const unsigned char* rowp = xs + n * (2 * D);
 #pragma unroll
@@ -411,15 +414,19 @@ __global__ __launch_bounds__(256) void k_bucket_threshold(const float* __restric
 bool per_embd_supported(const DevProb& pr, int kp) {
   if (pr.dtype != MOL_BF16) return false;
   if (pr.d != 64 && pr.d != 128) return false;
-  return kp <= 256;
+  return kp <= 1024;
 }
 
-int per_embd_list_cap(int kp) { return kp <= 128 ? 128 : 256; }
-int per_embd_stage_cap() { return 2 * kSGMax; }
+int per_embd_list_cap(int kp) { return kp <= 128 ? 128 : kp <= 256 ? 256 : kp <= 512 ? 512 : 1024; }
+int per_embd_stage_cap(int kp) {
+  // 2 SG of the list capacity's merge sort: SORT - KL
+  const int kl = per_embd_list_cap(kp);
+  return (kl <= 256 ? 512 : 2 * kl) - kl;
+}
 
-static void scan_grid(const DevProb& pr, bool scan2, PerEmbdGrid::Scan& sc) {
+static void scan_grid(const DevProb& pr, int kp, bool scan2, PerEmbdGrid::Scan& sc) {
   const int nvec = pr.B * pr.Pq;
-  const int vec_wg = kWaves * 32 * nb_for(pr.d, scan2);
+  const int vec_wg = waves_for(per_embd_list_cap(kp)) * 32 * nb_for(pr.d, scan2);
   sc.G = (nvec + vec_wg - 1) / vec_wg;
   const int units = sc.G * pr.Px;
   int R = std::max(1, (256 + units - 1) / units);
@@ -429,9 +436,9 @@ static void scan_grid(const DevProb& pr, bool scan2, PerEmbdGrid::Scan& sc) {
   sc.R = (pr.N + sc.range_len - 1) / sc.range_len;
 }
 
-void per_embd_grid(const DevProb& pr, PerEmbdGrid& g) {
-  scan_grid(pr, false, g.s1);
-  scan_grid(pr, true, g.s2);
+void per_embd_grid(const DevProb& pr, int kp, PerEmbdGrid& g) {
+  scan_grid(pr, kp, false, g.s1);
+  scan_grid(pr, kp, true, g.s2);
   // buckets: as many as fit kMaxBuckets per list over all ranges and halves
   const int ntiles = g.s1.range_len / 32;
   g.bucket_tiles = std::max(1, (2 * g.s1.R * ntiles + kMaxBuckets - 1) / kMaxBuckets);
@@ -451,7 +458,7 @@ static hipError_t launch_pe_t(const DevProb& pr, int kp, const PerEmbdGrid& g, f
   hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                      hipFuncAttributeMaxDynamicSharedMemorySize, S::LDS_TOTAL);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(kern, dim3(sc.G * pr.Px * sc.R), dim3(64 * kWaves), S::LDS_TOTAL, st, pr, kp, sc.R,
+  hipLaunchKernelGGL(kern, dim3(sc.G * pr.Px * sc.R), dim3(64 * S::WAVES), S::LDS_TOTAL, st, pr, kp, sc.R,
                      sc.range_len, sc.G, g.bucket_tiles, g.nbk, bmax, thr, lists, stg);
   return hipGetLastError();
 }
@@ -472,11 +479,20 @@ static hipError_t launch_pe_d(const DevProb& pr, int kp, const PerEmbdGrid& g, f
 hipError_t launch_per_embd(const DevProb& pr, int kp, const PerEmbdGrid& g, float* bmax, float* thr,
                            uint64_t* lists, uint64_t* stg, hipStream_t st) {
   const int KL = per_embd_list_cap(kp);
-  if (pr.d == 64)
-    return KL == 128 ? launch_pe_d<64, 128>(pr, kp, g, bmax, thr, lists, stg, st)
-                     : launch_pe_d<64, 256>(pr, kp, g, bmax, thr, lists, stg, st);
-  return KL == 128 ? launch_pe_d<128, 128>(pr, kp, g, bmax, thr, lists, stg, st)
-                   : launch_pe_d<128, 256>(pr, kp, g, bmax, thr, lists, stg, st);
+  if (pr.d == 64) {
+    switch (KL) {
+      case 128: return launch_pe_d<64, 128>(pr, kp, g, bmax, thr, lists, stg, st);
+      case 256: return launch_pe_d<64, 256>(pr, kp, g, bmax, thr, lists, stg, st);
+      case 512: return launch_pe_d<64, 512>(pr, kp, g, bmax, thr, lists, stg, st);
+      default: return launch_pe_d<64, 1024>(pr, kp, g, bmax, thr, lists, stg, st);
+    }
+  }
+  switch (KL) {
+    case 128: return launch_pe_d<128, 128>(pr, kp, g, bmax, thr, lists, stg, st);
+    case 256: return launch_pe_d<128, 256>(pr, kp, g, bmax, thr, lists, stg, st);
+    case 512: return launch_pe_d<128, 512>(pr, kp, g, bmax, thr, lists, stg, st);
+    default: return launch_pe_d<128, 1024>(pr, kp, g, bmax, thr, lists, stg, st);
+  }
 }
 
 }  // namespace mol

@@ -108,6 +108,8 @@ def test_duplicate_items_tie_to_lower_index():
     ("small_p32", W["exact_32k"].scaled(B=5, N=5003, clusters=32), 128),
     ("small_p64", W["exact_1m"].scaled(B=3, N=4099, clusters=32), 128),
     ("small_d128", W["hybrid_8m"].scaled(B=3, N=3001, clusters=32), 256),
+    ("small_p64_k600", W["exact_1m"].scaled(B=2, N=9001, clusters=32), 600),
+    ("small_d128_k1024", W["hybrid_8m"].scaled(B=2, N=12003, clusters=32), 1024),
     ("f32", W["tiny_exact_f32"].scaled(B=4, N=2000), 50),
 ])
 def test_topk_per_embd_matches_oracle(name, spec, kp):
@@ -165,12 +167,14 @@ def test_avg_embed_bit_exact_and_topk_avg():
     assert np.array_equal(q.view(torch.int16).cpu().numpy().view(np.uint16), qbar)
     assert np.array_equal(x.view(torch.int16).cpu().numpy().view(np.uint16), xbar)
     avg = mol.averaged_problem(prob, q, x)
-    dots, ids = mol.topk_per_embd(avg, 300)
-    torch.cuda.synchronize()
     oavg = mo.averaged_problem(op)
-    for b in range(spec.B):
-        s = mo.all_dots(oavg, b)[:, 0]
-        check_topk_row(s, ids.cpu().numpy()[b, 0], dots.cpu().numpy()[b, 0], 300, f"avg b={b}")
+    # TopKAvg list sizes up to the k_avg = 1024 of the 8M-item workload
+    for kp in (300, 1024):
+        dots, ids = mol.topk_per_embd(avg, kp)
+        torch.cuda.synchronize()
+        for b in range(spec.B):
+            s = mo.all_dots(oavg, b)[:, 0]
+            check_topk_row(s, ids.cpu().numpy()[b, 0], dots.cpu().numpy()[b, 0], kp, f"avg k'={kp} b={b}")
 
 
 @pytest.mark.parametrize("C,k", [(700, 100), (64, 100), (4096, 100)])
