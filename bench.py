@@ -150,7 +150,7 @@ def main():
             e0.record()
             mol.mol_topk_per_embd(pe_prob, kprime, pe_d, pe_i, ws_pe)
             e1.record()
-            mol.mol_rerank(prob, pe_i.view(B, C), C, k, rr_s, rr_i, rr_n, ws_rr)
+            mol.mol_rerank(prob, pe_i.view(B, C), C, None, 0, k, rr_s, rr_i, rr_n, ws_rr)
             e2.record()
             if record:
                 seg["per_embd"].append((e0, e1))

@@ -125,18 +125,21 @@ int mol_topk_per_embd(const mol_problem *prob, int32_t kprime, float *out_dot,
                       int32_t *out_idx, void *ws, size_t ws_bytes,
                       void *stream);
 
-/* Candidate union, deduplication and MoL rerank (Algorithm 2,
- * BruteForceTopKMoL over the deduplicated candidate set G).
- * cand int32 [B][C]: item ids, duplicates allowed; an id outside [0, N)
+/* Candidate union, deduplication and MoL rerank (Algorithm 2: the union G
+ * of the candidate sets, deduplicated, then BruteForceTopKMoL over G).
+ * cand int32 [B][C] and cand2 int32 [B][C2]: two candidate sets per query
+ * (e.g. TopKPerEmbedding's [B][P][k'] ids and TopKAvg's [B][k_avg]); cand2
+ * may be NULL when C2 == 0.  Duplicates are allowed; an id outside [0, N)
  * (e.g. -1) marks an empty slot and is skipped.  For each query the
- * distinct ids are scored with full MoL and the top-k kept.
+ * distinct ids of both sets are scored with full MoL and the top-k kept.
  * out_score float32 [B][k], out_idx int32 [B][k] (padded with -INFINITY /
  * -1 when a query has fewer than k distinct ids), out_n_unique int32 [B]
- * (may be NULL).  1 <= C <= 16384, 1 <= k <= 1024.  Needs every problem
- * pointer. */
+ * (may be NULL).  C >= 1, C2 >= 0, C + C2 <= 16384, 1 <= k <= 1024.
+ * Needs every problem pointer; mol_workspace_size takes C + C2 as C. */
 int mol_rerank(const mol_problem *prob, const int32_t *cand, int32_t C,
-               int32_t k, float *out_score, int32_t *out_idx,
-               int32_t *out_n_unique, void *ws, size_t ws_bytes, void *stream);
+               const int32_t *cand2, int32_t C2, int32_t k, float *out_score,
+               int32_t *out_idx, int32_t *out_n_unique, void *ws,
+               size_t ws_bytes, void *stream);
 
 /* TopKAvg materialisation (Section 3.2, Algorithm 2 TopKAvg):
  *   q_avg[b][t] = round( sum_pq Q[b][pq][t] ),  [B][d]

@@ -442,15 +442,19 @@ int mol_topk_per_embd(const mol_problem* prob, int32_t kprime, float* out_dot, i
   return stream_topk(s, prob->N, static_cast<char*>(ws), tile, out_dot, out_idx, st);
 }
 
-int mol_rerank(const mol_problem* prob, const int32_t* cand, int32_t C, int32_t k, float* out_score,
-               int32_t* out_idx, int32_t* out_n_unique, void* ws, size_t ws_bytes, void* stream) {
+int mol_rerank(const mol_problem* prob, const int32_t* cand, int32_t C, const int32_t* cand2, int32_t C2,
+               int32_t k, float* out_score, int32_t* out_idx, int32_t* out_n_unique, void* ws,
+               size_t ws_bytes, void* stream) {
   int rc;
   if ((rc = check_problem(prob, true))) return rc;
   if (k < 1 || k > MOL_MAX_K) return fail(MOL_EINVAL, "k = %d outside [1, %d]", k, MOL_MAX_K);
-  if (C < 1 || C > MOL_MAX_C) return fail(MOL_EINVAL, "C = %d outside [1, %d]", C, MOL_MAX_C);
+  if (C < 1 || C2 < 0 || static_cast<long>(C) + C2 > MOL_MAX_C)
+    return fail(MOL_EINVAL, "C = %d, C2 = %d: need C >= 1, C2 >= 0, C + C2 <= %d", C, C2, MOL_MAX_C);
   if (!cand || !out_score || !out_idx) return fail(MOL_EINVAL, "cand or output pointer is NULL");
+  if (C2 > 0 && !cand2) return fail(MOL_EINVAL, "cand2 is NULL with C2 = %d", C2);
   const DevProb pr = dev_prob(prob);
-  const RerankPlan r = plan_rerank(pr, C, k);
+  const int CT = C + C2;
+  const RerankPlan r = plan_rerank(pr, CT, k);
   if ((rc = check_ws(ws, ws_bytes, r.bytes))) return rc;
   hipStream_t st = static_cast<hipStream_t>(stream);
   char* w = static_cast<char*>(ws);
@@ -458,16 +462,16 @@ int mol_rerank(const mol_problem* prob, const int32_t* cand, int32_t C, int32_t 
   int32_t* nu = reinterpret_cast<int32_t*>(w + r.offNu);
   uint64_t* A = reinterpret_cast<uint64_t*>(w + r.s.offA);
   uint64_t* fin = reinterpret_cast<uint64_t*>(w + r.offFinal);
-  MOL_TRY_HIP(launch_dedup(cand, prob->B, C, prob->N, uniq, nu, st), "dedup");
+  MOL_TRY_HIP(launch_dedup(cand, C, cand2, C2, prob->B, prob->N, uniq, nu, st), "dedup");
   if (rerank_supported(pr, k)) {
-    const int chunk = rerank_chunk(C);
-    const long L0 = static_cast<long>((C + chunk - 1) / chunk) * k;
-    MOL_TIMED_LAUNCH(MOL_OP_RERANK, st, launch_rerank(pr, uniq, nu, C, k, A, st), "fused rerank");
+    const int chunk = rerank_chunk(CT);
+    const long L0 = static_cast<long>((CT + chunk - 1) / chunk) * k;
+    MOL_TIMED_LAUNCH(MOL_OP_RERANK, st, launch_rerank(pr, uniq, nu, CT, k, A, st), "fused rerank");
     if ((rc = reduce_rows(r.s, w, L0, fin, k, st))) return rc;
   } else {
-    MOL_TIMED_LAUNCH(MOL_OP_RERANK, st, launch_phi_generic(pr, 0, C, uniq, nu, C, nullptr, 0, A, r.s.strideA, st),
+    MOL_TIMED_LAUNCH(MOL_OP_RERANK, st, launch_phi_generic(pr, 0, CT, uniq, nu, CT, nullptr, 0, A, r.s.strideA, st),
                      "rerank score");
-    if ((rc = reduce_rows(r.s, w, C, fin, k, st))) return rc;
+    if ((rc = reduce_rows(r.s, w, CT, fin, k, st))) return rc;
   }
   MOL_TRY_HIP(launch_decode(fin, k, prob->B, k, out_score, out_idx, st), "decode");
   if (out_n_unique)

@@ -187,7 +187,8 @@ __global__ void k_copy_rows(const uint64_t* __restrict__ src, long src_stride, i
 // (linear probing, capacity a power of two >= 1.5 C) and appends each id the
 // first time it is seen.  Ids outside [0, N) are empty slots.
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(1024) void k_dedup(const int32_t* __restrict__ cand, int C, int N,
+__global__ __launch_bounds__(1024) void k_dedup(const int32_t* __restrict__ cand, int C,
+                                                const int32_t* __restrict__ cand2, int C2, int N,
                                                 int cap_log2, int32_t* __restrict__ uniq,
                                                 int32_t* __restrict__ n_unique) {
   extern __shared__ int32_t table[];
@@ -197,15 +198,16 @@ __global__ __launch_bounds__(1024) void k_dedup(const int32_t* __restrict__ cand
   for (int i = threadIdx.x; i < cap; i += blockDim.x) table[i] = -1;
   if (threadIdx.x == 0) count = 0;
   __syncthreads();
-  for (int i = threadIdx.x; i < C; i += blockDim.x) {
-    const int32_t id = cand[b * C + i];
+  const int CT = C + C2;                 // both sets; uniq rows hold CT slots
+  for (int i = threadIdx.x; i < CT; i += blockDim.x) {
+    const int32_t id = i < C ? cand[b * C + i] : cand2[b * C2 + (i - C)];
     if (id < 0 || id >= N) continue;
     uint32_t h = (static_cast<uint32_t>(id) * 0x9E3779B1u) >> (32 - cap_log2);
     for (int probe = 0; probe < cap; ++probe) {
       const int32_t prev = atomicCAS(&table[h], -1, id);
       if (prev == -1) {
         const int pos = atomicAdd(&count, 1);
-        uniq[b * C + pos] = id;
+        uniq[b * CT + pos] = id;
         break;
       }
       if (prev == id) break;
@@ -345,9 +347,9 @@ int dedup_cap_log2(int C) {
   return lg;
 }
 
-hipError_t launch_dedup(const int32_t* cand, int B, int C, int N, int32_t* uniq, int32_t* n_unique,
-                        hipStream_t st) {
-  const int lg = dedup_cap_log2(C);
+hipError_t launch_dedup(const int32_t* cand, int C, const int32_t* cand2, int C2, int B, int N,
+                        int32_t* uniq, int32_t* n_unique, hipStream_t st) {
+  const int lg = dedup_cap_log2(C + C2);
   const size_t smem = sizeof(int32_t) << lg;
   if (smem > 65536) {
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_dedup),
@@ -355,7 +357,7 @@ hipError_t launch_dedup(const int32_t* cand, int B, int C, int N, int32_t* uniq,
                                        static_cast<int>(smem));
     if (e != hipSuccess) return e;
   }
-  hipLaunchKernelGGL(k_dedup, dim3(B), dim3(1024), smem, st, cand, C, N, lg, uniq, n_unique);
+  hipLaunchKernelGGL(k_dedup, dim3(B), dim3(1024), smem, st, cand, C, cand2, C2, N, lg, uniq, n_unique);
   return hipGetLastError();
 }
 

@@ -62,7 +62,7 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "mol_score": [P, i32, i32, vp, vp],
         "mol_topk_exact": [P, i32, vp, vp, vp, sz, vp],
         "mol_topk_per_embd": [P, i32, vp, vp, vp, sz, vp],
-        "mol_rerank": [P, vp, i32, i32, vp, vp, vp, vp, sz, vp],
+        "mol_rerank": [P, vp, i32, vp, i32, i32, vp, vp, vp, vp, sz, vp],
         "mol_avg_embed": [P, vp, vp, vp],
         "mol_timing_enable": [ctypes.c_int],
         "mol_timing_read": [ctypes.c_int, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(i32)],
@@ -156,11 +156,11 @@ def mol_topk_per_embd(prob: Problem, kprime: int, out_dot, out_idx, ws, stream=N
                                     ws.numel() if ws is not None else 0, _stream(stream)))
 
 
-def mol_rerank(prob: Problem, cand, C: int, k: int, out_score, out_idx, out_n_unique, ws,
-               stream=None) -> None:
-    _check(load().mol_rerank(prob.ref, _ptr(cand), C, k, _ptr(out_score), _ptr(out_idx),
-                             _ptr(out_n_unique), _ptr(ws), ws.numel() if ws is not None else 0,
-                             _stream(stream)))
+def mol_rerank(prob: Problem, cand, C: int, cand2, C2: int, k: int, out_score, out_idx,
+               out_n_unique, ws, stream=None) -> None:
+    _check(load().mol_rerank(prob.ref, _ptr(cand), C, _ptr(cand2), C2, k, _ptr(out_score),
+                             _ptr(out_idx), _ptr(out_n_unique), _ptr(ws),
+                             ws.numel() if ws is not None else 0, _stream(stream)))
 
 
 def mol_avg_embed(prob: Problem, q_avg, x_avg, stream=None) -> None:
@@ -209,13 +209,17 @@ def topk_per_embd(prob: Problem, kprime: int, ws=None, stream=None):
     return s, i
 
 
-def rerank(prob: Problem, cand: torch.Tensor, k: int, ws=None, stream=None):
+def rerank(prob: Problem, cand: torch.Tensor, k: int, ws=None, stream=None,
+           cand2: Optional[torch.Tensor] = None):
+    """Union of the candidate rows of cand [B][C] (and cand2 [B][C2]),
+    deduplicated and reranked with full MoL: (scores, ids, n_unique)."""
     C = cand.shape[1]
-    ws = workspace(prob, MOL_OP_RERANK, k=k, C=C) if ws is None else ws
+    C2 = 0 if cand2 is None else cand2.shape[1]
+    ws = workspace(prob, MOL_OP_RERANK, k=k, C=C + C2) if ws is None else ws
     s = torch.empty((prob.B, k), dtype=torch.float32, device=prob.device)
     i = torch.empty((prob.B, k), dtype=torch.int32, device=prob.device)
     nu = torch.empty((prob.B,), dtype=torch.int32, device=prob.device)
-    mol_rerank(prob, cand, C, k, s, i, nu, ws, stream)
+    mol_rerank(prob, cand, C, cand2, C2, k, s, i, nu, ws, stream)
     return s, i, nu
 
 

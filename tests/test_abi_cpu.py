@@ -93,8 +93,16 @@ def test_entry_points_reject_before_launch():
     rc = lib.mol_score(ctypes.byref(c), 90, 20, 256, None)        # range past N
     assert rc == mol.MOL_EINVAL
     assert lib.mol_score(ctypes.byref(c), 0, 0, None, None) == mol.MOL_OK   # empty range
-    rc = lib.mol_rerank(ctypes.byref(c), None, 8, 5, 256, 256, None, ws, 1 << 40, None)
+    rc = lib.mol_rerank(ctypes.byref(c), None, 8, None, 0, 5, 256, 256, None, ws, 1 << 40, None)
     assert rc == mol.MOL_EINVAL
+    # second candidate set: NULL with C2 > 0, negative C2, total above the limit
+    cand = ctypes.c_void_p(256)
+    assert lib.mol_rerank(ctypes.byref(c), cand, 8, None, 4, 5, 256, 256, None, ws, 1 << 40,
+                          None) == mol.MOL_EINVAL
+    assert lib.mol_rerank(ctypes.byref(c), cand, 8, cand, -1, 5, 256, 256, None, ws, 1 << 40,
+                          None) == mol.MOL_EINVAL
+    assert lib.mol_rerank(ctypes.byref(c), cand, 16000, cand, 1000, 5, 256, 256, None, ws,
+                          1 << 40, None) == mol.MOL_EINVAL
     assert lib.mol_topk_exact(None, 10, 256, 256, ws, 1 << 40, None) == mol.MOL_EINVAL
 
 

@@ -177,6 +177,31 @@ def test_avg_embed_bit_exact_and_topk_avg():
             check_topk_row(s, ids.cpu().numpy()[b, 0], dots.cpu().numpy()[b, 0], kp, f"avg k'={kp} b={b}")
 
 
+def test_combined_candidates_rerank():
+    """CombTopK: the union of per-component top-k' and TopKAvg top-k_avg ids,
+    deduplicated across both sets and reranked with full MoL."""
+    spec = W["hybrid_8m"].scaled(B=4, N=6007, clusters=32)
+    kp, kavg, k = 32, 200, 100
+    inp = cuda_inputs(spec, seed=23)
+    prob = mol.Problem.from_inputs(inp)
+    _, pe_ids = mol.topk_per_embd(mol.Problem(inp.Q, inp.X), kp)
+    q, x = mol.avg_embed(prob)
+    _, avg_ids = mol.topk_per_embd(mol.averaged_problem(prob, q, x), kavg)
+    cand, cand2 = pe_ids.view(spec.B, -1), avg_ids.view(spec.B, -1)
+    rs, ri, nu = mol.rerank(prob, cand, k, cand2=cand2)
+    torch.cuda.synchronize()
+    op = oracle_problem(inp)
+    cand_np, cand2_np = cand.cpu().numpy(), cand2.cpu().numpy()
+    rs, ri, nu = rs.cpu().numpy(), ri.cpu().numpy(), nu.cpu().numpy()
+    for b in range(spec.B):
+        uniq = mo.union_dedup([cand_np[b], cand2_np[b]])
+        assert nu[b] == len(uniq), f"b={b}: {nu[b]} unique on the GPU, {len(uniq)} in the union"
+        _, _, phi = mo.mol_terms(op, b, uniq)
+        full = np.full(spec.N, -np.inf)
+        full[uniq] = phi
+        check_topk_row(full, ri[b], rs[b], k, f"comb b={b}")
+
+
 @pytest.mark.parametrize("C,k", [(700, 100), (64, 100), (4096, 100)])
 def test_rerank_matches_oracle(C, k):
     spec = W["exact_1m"].scaled(B=7, N=3000, clusters=32)
