@@ -1,10 +1,16 @@
 """Throughput benchmark of the MoL retrieval hot path on one MI355X.
 
-One step = one pass of the whole path over the 1M-item workload
-(B = 1024 queries, N = 1,048,576 items, P_q = P_x = 8, d = 64, H = 64, bf16):
+One step = one pass of the whole path over one batch of the workload.
+Default workload exact_1m (B = 1024 queries, N = 1,048,576 items,
+P_q = P_x = 8, d = 64, H = 64, bf16):
   exact:  mol_topk_exact (fused MoL scoring + top-100 selection)
   approx: mol_topk_per_embd (top-128 per component, all 64 components)
           + mol_rerank (union, dedup, MoL rerank to top-100)
+With --workload hybrid_8m (B = 256, N = 8,388,608, P = 8 x 4, d = 128,
+H = 128) the approximate path also runs TopKAvg (mol_avg_embed of the
+queries + mol_topk_per_embd top-1024 on the averaged embeddings, whose item
+side is precomputed outside the timed region) and reranks the union of both
+candidate sets.
 Inputs are synthetic, seeded, and resident in HBM before timing starts.
 Prints one JSON line.
 """
@@ -27,7 +33,7 @@ CSRC = os.path.join(ROOT, "paper_2407_15462_amd", "csrc")
 # sources of the fused exact scan kernel: a traffic figure measured on other
 # sources is stale and is not reported
 FUSED_SOURCES = ("mol_fused.hip", "mol_tile.h", "mol_device.h")
-TRAFFIC_FILE = "traffic_k_mol_fused_exact_1m.txt"
+TRAFFIC_FILE = "traffic_k_mol_fused_{workload}.txt"
 
 
 def parse():
@@ -37,7 +43,8 @@ def parse():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="exact_1m")
     ap.add_argument("--paths", default="exact,approx")
-    ap.add_argument("--cpu-baseline-queries", type=int, default=8)
+    ap.add_argument("--cpu-baseline-queries", type=int, default=None,
+                    help="oracle queries timed for cpu_baseline (default: about 10-20 s of work)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--copy-calibration", action="store_true",
@@ -61,11 +68,11 @@ def source_digest(names=FUSED_SOURCES) -> str:
     return h.hexdigest()
 
 
-def measured_traffic():
+def measured_traffic(workload: str):
     """HBM bytes per launch of the fused exact scan from the committed
-    counter summary, or None when it is missing or was taken on other
-    kernel sources."""
-    path = os.path.join(PROFILES, TRAFFIC_FILE)
+    counter summary of this workload, or None when it is missing or was
+    taken on other kernel sources."""
+    path = os.path.join(PROFILES, TRAFFIC_FILE.format(workload=workload))
     if not os.path.exists(path):
         return None
     kv = {}
@@ -125,17 +132,27 @@ def main():
     ex_i = torch.empty((B, k), dtype=torch.int32, device=dev)
     pe_prob = mol.Problem(inp.Q, inp.X)
     C = P * kprime
+    k_avg = spec.k_avg
     if "approx" in paths:
         ws_pe = mol.workspace(pe_prob, mol.MOL_OP_TOPK_PER_EMBD, kprime=kprime)
         pe_d = torch.empty((B, P, kprime), dtype=torch.float32, device=dev)
         pe_i = torch.empty((B, P, kprime), dtype=torch.int32, device=dev)
-        ws_rr = mol.workspace(prob, mol.MOL_OP_RERANK, k=k, C=C)
+        if k_avg:
+            # item side of TopKAvg: precomputed once (preprocessing, untimed)
+            x_avg = torch.empty((N, d), dtype=inp.Q.dtype, device=dev)
+            q_avg = torch.empty((B, d), dtype=inp.Q.dtype, device=dev)
+            mol.mol_avg_embed(pe_prob, None, x_avg)
+            avg_prob = mol.averaged_problem(pe_prob, q_avg, x_avg)
+            ws_av = mol.workspace(avg_prob, mol.MOL_OP_TOPK_PER_EMBD, kprime=k_avg)
+            av_d = torch.empty((B, 1, k_avg), dtype=torch.float32, device=dev)
+            av_i = torch.empty((B, 1, k_avg), dtype=torch.int32, device=dev)
+        ws_rr = mol.workspace(prob, mol.MOL_OP_RERANK, k=k, C=C + k_avg)
         rr_s = torch.empty((B, k), dtype=torch.float32, device=dev)
         rr_i = torch.empty((B, k), dtype=torch.int32, device=dev)
         rr_n = torch.empty((B,), dtype=torch.int32, device=dev)
 
     ev = lambda: torch.cuda.Event(enable_timing=True)
-    seg = {p: [] for p in ("exact", "per_embd", "rerank")}
+    seg = {p: [] for p in ("exact", "per_embd", "topk_avg", "rerank")}
 
     def step(record):
         if "exact" in paths:
@@ -146,15 +163,21 @@ def main():
             if record:
                 seg["exact"].append((e0, e1))
         if "approx" in paths:
-            e0, e1, e2 = ev(), ev(), ev()
+            e0, e1, e2, e3 = ev(), ev(), ev(), ev()
             e0.record()
             mol.mol_topk_per_embd(pe_prob, kprime, pe_d, pe_i, ws_pe)
             e1.record()
-            mol.mol_rerank(prob, pe_i.view(B, C), C, None, 0, k, rr_s, rr_i, rr_n, ws_rr)
+            if k_avg:
+                mol.mol_avg_embed(pe_prob, q_avg, None)
+                mol.mol_topk_per_embd(avg_prob, k_avg, av_d, av_i, ws_av)
             e2.record()
+            mol.mol_rerank(prob, pe_i.view(B, C), C, av_i.view(B, k_avg) if k_avg else None, k_avg, k,
+                           rr_s, rr_i, rr_n, ws_rr)
+            e3.record()
             if record:
                 seg["per_embd"].append((e0, e1))
-                seg["rerank"].append((e1, e2))
+                seg["topk_avg"].append((e1, e2))
+                seg["rerank"].append((e2, e3))
 
     for _ in range(args.warmup):
         step(False)
@@ -171,10 +194,12 @@ def main():
     mol.mol_timing_enable(False)
     ms_step = 1e3 * wall / args.steps
     ms = {p: (sum(a.elapsed_time(b) for a, b in v) / len(v) if v else None) for p, v in seg.items()}
-    kern = {}
+    kern = {}          # main-kernel milliseconds per launch
+    kern_step = {}     # main-kernel milliseconds per step (all launches of the op)
     for op in timed_ops:
         tot, n = mol.mol_timing_read(op)
         kern[op] = tot / n if n else None
+        kern_step[op] = tot / args.steps if n else None
 
     flops_pair = 2 * P * d + 4 * P * H
     out = {
@@ -197,28 +222,34 @@ def main():
         # algorithmic work of one launch: every (query, item) pair once,
         # 2 P d flops of component dots + 4 P H of the gating MLP
         ach = B * N * flops_pair / tk / 1e12
-        traffic = measured_traffic()
+        traffic = measured_traffic(spec.name)
         out["roofline"] = {"bound": "mfma", "achieved": ach, "peak": PEAK_BF16_TFLOPS,
                            "unit": "TFLOP/s", "frac": ach / PEAK_BF16_TFLOPS, "traffic": traffic,
                            "kernel": "k_mol_fused (MoL scoring + per-range top-k scan)",
                            "flops_per_launch": B * N * flops_pair}
     if ms["per_embd"]:
-        t = (ms["per_embd"] + ms["rerank"]) / 1e3
-        ex = ex_i.cpu()
-        got = rr_i.cpu()
-        hits = sum(len(set(a.tolist()) & set(b.tolist())) for a, b in zip(got, ex))
-        tpe = kern[mol.MOL_OP_TOPK_PER_EMBD] / 1e3
-        pe_flops = 2.0 * B * P * N * d
-        out["approx"] = {"ms_per_embd": ms["per_embd"], "ms_rerank": ms["rerank"],
-                         "kernel_ms_per_embd": tpe * 1e3,
+        t = (ms["per_embd"] + ms["topk_avg"] + ms["rerank"]) / 1e3
+        recall = None
+        if "exact" in paths:
+            ex = ex_i.cpu()
+            got = rr_i.cpu()
+            hits = sum(len(set(a.tolist()) & set(b.tolist())) for a, b in zip(got, ex))
+            recall = hits / ex.numel()
+        # both scans of every per-component (and TopKAvg) list, per step
+        tpe = kern_step[mol.MOL_OP_TOPK_PER_EMBD] / 1e3
+        pe_flops = 2.0 * B * P * N * d + (2.0 * B * N * d if k_avg else 0.0)
+        out["approx"] = {"ms_per_embd": ms["per_embd"], "ms_topk_avg": ms["topk_avg"] if k_avg else None,
+                         "k_avg": k_avg or None, "ms_rerank": ms["rerank"],
+                         "kernel_ms_per_embd_per_step": tpe * 1e3,
                          "kernel_ms_rerank": kern[mol.MOL_OP_RERANK],
                          "per_embd_mfma_frac": pe_flops / tpe / 1e12 / PEAK_BF16_TFLOPS,
                          "queries_per_s": B / t,
-                         "recall_at_100_vs_exact": hits / ex.numel(),
+                         "recall_at_100_vs_exact": recall,
                          "candidates_per_query_mean": float(rr_n.float().mean().item())}
 
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(inp, spec, args.cpu_baseline_queries)
+        nq = args.cpu_baseline_queries or max(1, (8 << 20) // spec.N)
+        out["cpu_baseline"] = cpu_baseline(inp, spec, nq)
     print(json.dumps(out), flush=True)
 
 
