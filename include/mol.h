@@ -150,6 +150,22 @@ int mol_rerank(const mol_problem *prob, const int32_t *cand, int32_t C,
 int mol_avg_embed(const mol_problem *prob, void *q_avg, void *x_avg,
                   void *stream);
 
+/* Gap certificate of TopKPerEmbedding (Theorem 2, Definition 2).
+ * dots float32 [B][P][m]: per-component lists sorted descending, as written
+ * by mol_topk_per_embd with kprime = m (m >= 2); scores float32 [B][k]: the
+ * MoL top-k (descending, as written by mol_rerank) over candidates that
+ * include at least the first m - 1 ids of every list.  Writes, per query b:
+ *   out_S[b]      = max_p dots[b][p][m - 1]   (the largest m-th dot product:
+ *                   no item outside the candidates has a larger MoL score)
+ *   out_SK[b]     = scores[b][k - 1]          (the k-th retrieved MoL score)
+ *   out_bound[b]  = out_S[b] - out_SK[b]      (>= the gap of Definition 2)
+ *   out_looser[b] = max_p dots[b][p][m - 2] - out_SK[b]
+ * (the looser bound of Theorem 2).  Any output pointer may be NULL.  Pure
+ * device reduction, no workspace.  1 <= k <= 1024, P <= 64. */
+int mol_gap_bound(int32_t B, int32_t P, int32_t m, const float *dots,
+                  int32_t k, const float *scores, float *out_S, float *out_SK,
+                  float *out_bound, float *out_looser, void *stream);
+
 /* Kernel timing, a diagnostic for throughput measurements.
  * mol_timing_enable(1) makes every later call record a pair of HIP events on
  * its stream around its main kernel: the fused scoring kernel of mol_score,

@@ -488,6 +488,17 @@ int mol_avg_embed(const mol_problem* prob, void* q_avg, void* x_avg, void* strea
   return MOL_OK;
 }
 
+int mol_gap_bound(int32_t B, int32_t P, int32_t m, const float* dots, int32_t k, const float* scores,
+                  float* out_S, float* out_SK, float* out_bound, float* out_looser, void* stream) {
+  if (B < 1 || P < 1 || P > MOL_MAX_P) return fail(MOL_EINVAL, "B = %d, P = %d: need B >= 1, 1 <= P <= %d", B, P, MOL_MAX_P);
+  if (m < 2) return fail(MOL_EINVAL, "m = %d: the lists need at least 2 entries", m);
+  if (k < 1 || k > MOL_MAX_K) return fail(MOL_EINVAL, "k = %d outside [1, %d]", k, MOL_MAX_K);
+  if (!dots || !scores) return fail(MOL_EINVAL, "dots or scores is NULL");
+  MOL_TRY_HIP(launch_gap_bound(B, P, m, dots, k, scores, out_S, out_SK, out_bound, out_looser,
+                               static_cast<hipStream_t>(stream)), "gap bound");
+  return MOL_OK;
+}
+
 int mol_timing_enable(int on) {
   TimingLog& t = timing_log();
   std::lock_guard<std::mutex> g(t.mu);

@@ -219,6 +219,35 @@ __global__ __launch_bounds__(1024) void k_dedup(const int32_t* __restrict__ cand
 }
 
 // ---------------------------------------------------------------------------
+// Theorem 2 certificate: one thread per query, a max over P list entries.
+// ---------------------------------------------------------------------------
+__global__ void k_gap_bound(int B, int P, int m, const float* __restrict__ dots, int k,
+                            const float* __restrict__ scores, float* out_S, float* out_SK,
+                            float* out_bound, float* out_looser) {
+  const int b = blockIdx.x * blockDim.x + threadIdx.x;
+  if (b >= B) return;
+  float S = -__builtin_inff(), Sk = -__builtin_inff();
+  for (int p = 0; p < P; ++p) {
+    const float* row = dots + (static_cast<long>(b) * P + p) * m;
+    S = fmaxf(S, row[m - 1]);
+    Sk = fmaxf(Sk, row[m - 2]);
+  }
+  const float SK = scores[static_cast<long>(b) * k + (k - 1)];
+  if (out_S) out_S[b] = S;
+  if (out_SK) out_SK[b] = SK;
+  if (out_bound) out_bound[b] = S - SK;
+  if (out_looser) out_looser[b] = Sk - SK;
+}
+
+hipError_t launch_gap_bound(int B, int P, int m, const float* dots, int k, const float* scores,
+                            float* out_S, float* out_SK, float* out_bound, float* out_looser,
+                            hipStream_t st) {
+  hipLaunchKernelGGL(k_gap_bound, dim3((B + 255) / 256), dim3(256), 0, st, B, P, m, dots, k, scores,
+                     out_S, out_SK, out_bound, out_looser);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
 // TopKAvg materialisation: out[m][t] = round(sum_c in[c*sc + m*sm + t]),
 // summed in float64, rounded once (nearest-even).
 // ---------------------------------------------------------------------------

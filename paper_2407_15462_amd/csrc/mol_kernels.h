@@ -26,6 +26,9 @@ hipError_t launch_copy_rows(const uint64_t* src, long src_stride, int rows, int 
 int dedup_cap_log2(int C);
 hipError_t launch_dedup(const int32_t* cand, int C, const int32_t* cand2, int C2, int B, int N,
                         int32_t* uniq, int32_t* n_unique, hipStream_t st);
+hipError_t launch_gap_bound(int B, int P, int m, const float* dots, int k, const float* scores,
+                            float* out_S, float* out_SK, float* out_bound, float* out_looser,
+                            hipStream_t st);
 hipError_t launch_avg_embed(const DevProb& pr, void* q_avg, void* x_avg, hipStream_t st);
 
 }  // namespace mol

@@ -21,7 +21,7 @@ MOL_F32, MOL_BF16 = 0, 1
 MOL_OP_SCORE, MOL_OP_TOPK_EXACT, MOL_OP_TOPK_PER_EMBD, MOL_OP_RERANK = range(4)
 
 EXPORTS = ("mol_workspace_size", "mol_score", "mol_topk_exact", "mol_topk_per_embd",
-           "mol_rerank", "mol_avg_embed", "mol_timing_enable", "mol_timing_read",
+           "mol_rerank", "mol_avg_embed", "mol_gap_bound", "mol_timing_enable", "mol_timing_read",
            "mol_status_str", "mol_last_error")
 
 
@@ -64,6 +64,7 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "mol_topk_per_embd": [P, i32, vp, vp, vp, sz, vp],
         "mol_rerank": [P, vp, i32, vp, i32, i32, vp, vp, vp, vp, sz, vp],
         "mol_avg_embed": [P, vp, vp, vp],
+        "mol_gap_bound": [i32, i32, i32, vp, i32, vp, vp, vp, vp, vp, vp],
         "mol_timing_enable": [ctypes.c_int],
         "mol_timing_read": [ctypes.c_int, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(i32)],
     }
@@ -167,6 +168,12 @@ def mol_avg_embed(prob: Problem, q_avg, x_avg, stream=None) -> None:
     _check(load().mol_avg_embed(prob.ref, _ptr(q_avg), _ptr(x_avg), _stream(stream)))
 
 
+def mol_gap_bound(B: int, P: int, m: int, dots, k: int, scores, out_S, out_SK, out_bound,
+                  out_looser, stream=None) -> None:
+    _check(load().mol_gap_bound(B, P, m, _ptr(dots), k, _ptr(scores), _ptr(out_S), _ptr(out_SK),
+                                _ptr(out_bound), _ptr(out_looser), _stream(stream)))
+
+
 def mol_timing_enable(on: bool) -> None:
     _check(load().mol_timing_enable(1 if on else 0))
 
@@ -221,6 +228,16 @@ def rerank(prob: Problem, cand: torch.Tensor, k: int, ws=None, stream=None,
     nu = torch.empty((prob.B,), dtype=torch.int32, device=prob.device)
     mol_rerank(prob, cand, C, cand2, C2, k, s, i, nu, ws, stream)
     return s, i, nu
+
+
+def gap_bound(dots: torch.Tensor, scores: torch.Tensor, stream=None):
+    """Theorem 2 certificate from per-component lists dots [B][P][m] and the
+    reranked scores [B][k]: (S, S_K, bound, looser), each float32 [B]."""
+    B, P, m = dots.shape
+    k = scores.shape[1]
+    outs = [torch.empty((B,), dtype=torch.float32, device=dots.device) for _ in range(4)]
+    mol_gap_bound(B, P, m, dots, k, scores, *outs, stream=stream)
+    return tuple(outs)
 
 
 def avg_embed(prob: Problem, stream=None) -> Tuple[torch.Tensor, torch.Tensor]:

@@ -123,3 +123,13 @@ def test_timing_records_are_empty_and_validated():
     assert lib.mol_timing_enable(0) == mol.MOL_OK
     assert lib.mol_timing_read(mol.MOL_OP_TOPK_EXACT, ctypes.byref(ms), ctypes.byref(n)) == mol.MOL_OK
     assert n.value == 0
+
+
+def test_gap_bound_validation():
+    lib = mol.load()
+    p = ctypes.c_void_p(256)
+    assert lib.mol_gap_bound(0, 8, 5, p, 10, p, None, None, None, None, None) == mol.MOL_EINVAL
+    assert lib.mol_gap_bound(4, 65, 5, p, 10, p, None, None, None, None, None) == mol.MOL_EINVAL
+    assert lib.mol_gap_bound(4, 8, 1, p, 10, p, None, None, None, None, None) == mol.MOL_EINVAL
+    assert lib.mol_gap_bound(4, 8, 5, p, 0, p, None, None, None, None, None) == mol.MOL_EINVAL
+    assert lib.mol_gap_bound(4, 8, 5, None, 10, p, None, None, None, None, None) == mol.MOL_EINVAL

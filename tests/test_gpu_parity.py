@@ -202,6 +202,38 @@ def test_combined_candidates_rerank():
         check_topk_row(full, ri[b], rs[b], k, f"comb b={b}")
 
 
+def test_gap_certificate_theorem2():
+    """Theorem 2: with per-component lists of k'+1 entries, S = the largest
+    (k'+1)-th dot product bounds every non-candidate's MoL score, so
+    S - S_K bounds the gap (Definition 2) of the reranked top-k."""
+    spec = W["exact_1m"].scaled(B=4, N=6007, clusters=16)
+    kp, k = 24, 20
+    inp = cuda_inputs(spec, seed=29)
+    prob = mol.Problem.from_inputs(inp)
+    dots, ids = mol.topk_per_embd(mol.Problem(inp.Q, inp.X), kp + 1)
+    cand = ids.view(spec.B, -1)
+    rs, ri, nu = mol.rerank(prob, cand, k)
+    S, SK, bound, looser = mol.gap_bound(dots, rs)
+    torch.cuda.synchronize()
+    op = oracle_problem(inp)
+    cand_np, ri = cand.cpu().numpy(), ri.cpu().numpy()
+    S, SK, bound, looser = (t.cpu().numpy() for t in (S, SK, bound, looser))
+    for b in range(spec.B):
+        s_all = mo.all_dots(op, b)
+        S_oracle = max(mo.kth_largest(s_all[:, p], kp + 1) for p in range(spec.P))
+        assert abs(S[b] - S_oracle) <= TAU
+        uniq = mo.union_dedup([cand_np[b]])
+        _, _, phi_c = mo.mol_terms(op, b, uniq)
+        assert abs(SK[b] - mo.kth_largest(phi_c, k)) <= TAU
+        assert abs(bound[b] - (S[b] - SK[b])) <= 1e-6 and looser[b] >= bound[b] - 1e-6
+        phi_all = mo.mol_scores(op, [b])[0]
+        outside = np.setdiff1d(np.arange(spec.N), uniq)
+        assert phi_all[outside].max() <= S_oracle + 1e-12      # the theorem's premise
+        g = mo.gap(phi_all, ri[b], k)
+        assert g <= bound[b] + TAU, f"b={b}: gap {g} above the bound {bound[b]}"
+        log(f"[gap] b={b} S={S[b]:.5f} S_K={SK[b]:.5f} bound={bound[b]:.5f} gap={g:.5f}")
+
+
 @pytest.mark.parametrize("C,k", [(700, 100), (64, 100), (4096, 100)])
 def test_rerank_matches_oracle(C, k):
     spec = W["exact_1m"].scaled(B=7, N=3000, clusters=32)
