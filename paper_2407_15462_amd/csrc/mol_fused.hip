@@ -41,7 +41,7 @@ struct FusedShape {
   static constexpr int ASTAGE = kTile * P * 4;        // bytes of one a_x stage
   static constexpr int LDS_X = kRing * XSTAGE;
   static constexpr int LDS_AX = kRing * ASTAGE;
-  static constexpr int LDS_CB = kQueriesPerWG * 16 * 4 * 4;   // [query][row c][tile] (a_q + b2)
+  static constexpr int LDS_CB = kQueriesPerWG * P * 4;   // [query][p] log2(e) (a_q + b2), f32
   static constexpr int LDS_TOPK = kQueriesPerWG * kTopkRegion * 8;
   static constexpr int LDS_TOTAL = LDS_X + LDS_AX + LDS_CB + LDS_TOPK;
   // 16-byte global->LDS copies per stage, in 1 KB blocks of one wave each
@@ -76,7 +76,7 @@ __global__ __launch_bounds__(64 * kWaves, 1) void k_mol_fused(
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   unsigned char* sX = smem;
   unsigned char* sAx = smem + S::LDS_X;
-  uint32_t* sCb = reinterpret_cast<uint32_t*>(smem + S::LDS_X + S::LDS_AX);
+  float* sCb = reinterpret_cast<float*>(smem + S::LDS_X + S::LDS_AX);
   uint64_t* sTop = reinterpret_cast<uint64_t*>(smem + S::LDS_X + S::LDS_AX + S::LDS_CB);
 
   const int tid = threadIdx.x, lane = tid & 63;
@@ -130,13 +130,10 @@ __global__ __launch_bounds__(64 * kWaves, 1) void k_mol_fused(
   for (int t = 0; t < kRing - 1 && t < ntiles; ++t) stage(t, t);
 
   // ---- per-workgroup constants ----
-  // log2(e) (a_q + b2) as f16 hi + lo, [query][row c][tile pt] so that a
-  // lane reads its four tiles' values with one 16-byte load
-  for (int i = tid; i < kQueriesPerWG * 64; i += 64 * kWaves) {
-    const int qi = i / 64, cc = (i / 4) % 16, pt = i % 4, b = qwg + qi;
-    const int p = Mlp::aug_p(cc, pt);
-    sCb[i] = (b < pr.B && pt < S::PT) ? split_f16(kLog2e * (pr.a_q[static_cast<long>(b) * P + p] + pr.b2[p]))
-                                      : 0u;
+  // log2(e) (a_q + b2) per query of the workgroup, [query][p]
+  for (int i = tid; i < kQueriesPerWG * P; i += 64 * kWaves) {
+    const int qi = i / P, p = i % P, b = qwg + qi;
+    sCb[i] = b < pr.B ? kLog2e * (pr.a_q[static_cast<long>(b) * P + p] + pr.b2[p]) : 0.f;
   }
   WaveTopk top[2];
   if (!DENSE) {
@@ -173,7 +170,7 @@ __global__ __launch_bounds__(64 * kWaves, 1) void k_mol_fused(
 
       // LDS operands of the step, all issued before the first MFMA so that
       // one LDS round trip is exposed per step: the X tile (GEMM1 B
-      // operands), a_x and the a_q + b2 blocks
+      // operands) and a_x
       uint4 xb[PX][S::KD];
 #pragma unroll
       for (int px = 0; px < PX; ++px) {
@@ -190,10 +187,6 @@ __global__ __launch_bounds__(64 * kWaves, 1) void k_mol_fused(
         const int phys = (base / 4 + q4) ^ (n % S::AROWCH);
         axv[q4] = *reinterpret_cast<const float4*>(as + n * (P * 4) + 16 * phys);
       }
-      uint4 cbq[2];
-#pragma unroll
-      for (int qb = 0; qb < 2; ++qb)
-        cbq[qb] = *reinterpret_cast<const uint4*>(sCb + ((2 * wave + qb) * 16 + c) * 4);
       __builtin_amdgcn_sched_barrier(0);
 
       // GEMM1: both queries x 16 items x all px
@@ -219,6 +212,7 @@ __global__ __launch_bounds__(64 * kWaves, 1) void k_mol_fused(
 #pragma unroll
       for (int q4 = 0; q4 < S::PT; ++q4)
         axr[q4] = f32x4_t{kLog2e * axv[q4].x, kLog2e * axv[q4].y, kLog2e * axv[q4].z, kLog2e * axv[q4].w};
+
       // the two queries one after the other (keeps the register peak low)
       float phi[2];
 #pragma unroll
@@ -226,9 +220,15 @@ __global__ __launch_bounds__(64 * kWaves, 1) void k_mol_fused(
         float sq[1][S::RUN];
 #pragma unroll
         for (int mu = 0; mu < S::RUN; ++mu) sq[0][mu] = s2[qb][mu];
-        const uint4 cq[1] = {cbq[qb]};
+        // + log2(e) (a_q + b2) of the query at the lane's p = base(g) + 4 pt + i
+        f32x4_t c0[1][S::PT];
+#pragma unroll
+        for (int pt = 0; pt < S::PT; ++pt) {
+          const float4 cb = *reinterpret_cast<const float4*>(sCb + (2 * wave + qb) * P + base + 4 * pt);
+          c0[0][pt] = axr[pt] + f32x4_t{cb.x, cb.y, cb.z, cb.w};
+        }
         float pq[1];
-        mlp.template phi<1>(sq, axr, cq, pq);
+        mlp.template phi<1>(sq, c0, pq);
         phi[qb] = pq[0];
         __builtin_amdgcn_sched_barrier(0);
       }
@@ -238,7 +238,7 @@ __global__ __launch_bounds__(64 * kWaves, 1) void k_mol_fused(
         if constexpr (DENSE) {
           if (g == 0 && item_ok && b < pr.B) phi_out[b * phi_stride + (item - n_begin)] = phi[qb];
         } else {
-          top[qb].offer((g == 0 && item_ok) ? make_key(phi[qb], item) : 0ull, lane);
+          top[qb].offer_score(phi[qb], item, g == 0 && item_ok, lane);
         }
       }
     }

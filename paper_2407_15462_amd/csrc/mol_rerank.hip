@@ -46,14 +46,15 @@ __global__ __launch_bounds__(64 * kWaves, 2) void k_mol_rerank(
   top.init(sTop + wave * kTopkRegion, k, lane);
   Mlp mlp;
   mlp.load(pr, c, g);
-  // log2(e) (a_q + b2) of query b as f16 hi + lo, tile pt in dword pt
-  uint32_t cb[4] = {0u, 0u, 0u, 0u};
+  // log2(e) (a_q + b2) of query b at the lane's p = base(g) + 4 pt + i
+  f32x4_t cbf[PT];
 #pragma unroll
-  for (int pt = 0; pt < PT; ++pt) {
-    const int p = Mlp::aug_p(c, pt);
-    cb[pt] = split_f16(kLog2e * (pr.a_q[static_cast<long>(b) * P + p] + pr.b2[p]));
-  }
-  const uint4 cbq[1] = {make_uint4(cb[0], cb[1], cb[2], cb[3])};
+  for (int pt = 0; pt < PT; ++pt)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int p = base + 4 * pt + i;
+      cbf[pt][i] = kLog2e * (pr.a_q[static_cast<long>(b) * P + p] + pr.b2[p]);
+    }
   // query b's components as GEMM1 rows 0..7 (rows 8..15 zero)
   uint4 qop[KD];
 #pragma unroll
@@ -73,11 +74,11 @@ __global__ __launch_bounds__(64 * kWaves, 2) void k_mol_rerank(
 #pragma unroll
       for (int kk = 0; kk < KD; ++kk)
         xop[px][kk] = *reinterpret_cast<const uint4*>(X + (static_cast<long>(px) * N + item) * D + 32 * kk + 8 * g);
-    f32x4_t axr[PT];
+    f32x4_t c0[1][PT];
 #pragma unroll
     for (int pt = 0; pt < PT; ++pt) {
       const float4 a = *reinterpret_cast<const float4*>(pr.a_x + static_cast<long>(item) * P + base + 4 * pt);
-      axr[pt] = f32x4_t{kLog2e * a.x, kLog2e * a.y, kLog2e * a.z, kLog2e * a.w};
+      c0[0][pt] = f32x4_t{kLog2e * a.x, kLog2e * a.y, kLog2e * a.z, kLog2e * a.w} + cbf[pt];
     }
     f32x4_t acc1[PX];
 #pragma unroll
@@ -94,8 +95,8 @@ __global__ __launch_bounds__(64 * kWaves, 2) void k_mol_rerank(
       s[0][mu] = __uint_as_float(sw[0]);
     }
     float phi[1];
-    mlp.template phi<1>(s, axr, cbq, phi);
-    top.offer((g == 0 && ok) ? make_key(phi[0], item) : 0ull, lane);
+    mlp.template phi<1>(s, c0, phi);
+    top.offer_score(phi[0], item, g == 0 && ok, lane);
   }
   top.flush(lane);
   uint64_t* dst = partial + (static_cast<long>(b) * nchunks + j) * k;

@@ -17,8 +17,8 @@
 //                 operand with K slot 8g + e of block m <-> j = 32 m +
 //                 16 (e/4) + 4 g + e%4; W2's rows are ordered so that output
 //                 row 16 pt + 4 g + i is p = base(g) + 4 pt + i, the lane's
-//                 own s value.  a_x enters as the accumulator input; a_q + b2
-//                 as one extra K block holding it split into f16 hi + lo.
+//                 own s value.  log2(e) (a_x + a_q + b2) enters as the
+//                 accumulator input (f32).
 //   softmax, phi  w_p = 2^{l'_p}, phi = sum w_p s_p / sum w_p (s in f32),
 //                 reduced over the 4 lanes of an item with permlane swaps.
 // (Eq. 1 / Eq. 2 with the two-layer SiLU gating MLP of Appendix A.3.)
@@ -172,11 +172,13 @@ struct WaveTopk {
   static constexpr int kStage = 128;
   uint64_t* reg;
   uint64_t theta;
+  float theta_score;   // score of theta (-inf while the list is not full)
   int stg;
   int k;
   __device__ void init(uint64_t* region, int k_, int lane) {
     reg = region;
     theta = 0ull;
+    theta_score = -__builtin_inff();
     stg = 0;
     k = k_;
     for (int i = lane; i < kList + kStage; i += 64) reg[i] = 0ull;
@@ -187,6 +189,7 @@ struct WaveTopk {
     for (int i = kList + lane; i < kList + kStage; i += 64) reg[i] = 0ull;
     wave_lds_sync();
     theta = reg[k - 1];
+    theta_score = key_score(theta);
     stg = 0;
   }
   // offer one key per lane (0 = none); at most 16 lanes offer per call
@@ -199,6 +202,14 @@ struct WaveTopk {
       stg += __popcll(mask);
       if (stg > kStage - 16) merge(lane);
     }
+  }
+  // offer (score, item) from lanes with valid set: a float compare rejects
+  // scores below the threshold's before any key is formed (a key beats
+  // theta only if its score is at least theta's score)
+  __device__ void offer_score(float score, int32_t item, bool valid, int lane) {
+    const bool maybe = valid && score >= theta_score;
+    if (__ballot(maybe) == 0ull) return;
+    offer(maybe ? make_key(score, item) : 0ull, lane);
   }
   __device__ void flush(int lane) {
     if (stg > 0) merge(lane);
@@ -218,7 +229,6 @@ struct MolMlp {
   uint4 w1op[JT][KP];
   uint4 w2op[PT][KH];
   f32x4_t b1acc[JT];
-  uint4 ones;                         // 1.0 at K slots 0, 1 (the a_q + b2 block)
 
   __device__ void load(const DevProb& pr, int c, int g) {
     const bf16_t* W1 = static_cast<const bf16_t*>(pr.W1);
@@ -258,18 +268,13 @@ struct MolMlp {
     for (int jt = 0; jt < JT; ++jt)
 #pragma unroll
       for (int i = 0; i < 4; ++i) b1acc[jt][i] = -kLog2e * pr.b1[16 * jt + 4 * g + i];
-    ones = make_uint4(g == 0 ? 0x3C003C00u : 0u, 0u, 0u, 0u);
   }
 
-  // p of output row 16 pt + c of GEMM3 (the a_q + b2 operand's rows)
-  __device__ static int aug_p(int c, int pt) { return lane_base(c >> 2, PX) + 4 * pt + (c & 3); }
-
   // Base-2 gating logits l' of one query for the lane's items (GEMM2 ->
-  // SiLU -> GEMM3).  s: the lane's run of s values; axr: log2(e) a_x in the
-  // GEMM3 accumulator layout; cbq: packed f16 hi/lo of log2(e) (a_q + b2)
-  // at p = aug_p(c, pt) in dword pt (finite in every lane).
-  __device__ void logits(const float (&s)[RUN], const f32x4_t (&axr)[PT], const uint4& cbq,
-                         f32x4_t (&lg)[PT]) const {
+  // SiLU -> GEMM3).  s: the lane's run of s values; c0: log2(e) (a_x + a_q
+  // + b2) in the GEMM3 accumulator layout (element i of tile pt <-> p =
+  // base(g) + 4 pt + i).
+  __device__ void logits(const float (&s)[RUN], const f32x4_t (&c0)[PT], f32x4_t (&lg)[PT]) const {
     uint4 sop[KP];
 #pragma unroll
     for (int m = 0; m < KP; ++m)
@@ -294,12 +299,9 @@ struct MolMlp {
       hop[m] = make_uint4(pack_f16(hv[0], hv[1]), pack_f16(hv[2], hv[3]), pack_f16(hv[4], hv[5]),
                           pack_f16(hv[6], hv[7]));
     }
-    // the a_q + b2 block: only K slots 0, 1 (dword 0 of the g == 0 lanes)
-    // meet a nonzero B entry
-    const uint32_t cbs[4] = {cbq.x, cbq.y, cbq.z, cbq.w};
 #pragma unroll
     for (int pt = 0; pt < PT; ++pt) {
-      lg[pt] = mfma_f16(make_uint4(cbs[pt], 0u, 0u, 0u), ones, axr[pt]);
+      lg[pt] = c0[pt];
 #pragma unroll
       for (int m = 0; m < KH; ++m) lg[pt] = mfma_f16(w2op[pt][m], hop[m], lg[pt]);
     }
@@ -326,14 +328,15 @@ struct MolMlp {
   // independent and branch-free, so they can be interleaved; a query whose
   // max-free sum left [2^-60, 2^60] (logits far from zero) is redone with
   // the row maximum subtracted.
+  // c0[q]: log2(e) (a_x + a_q + b2) of query q in the GEMM3 accumulator
+  // layout.
   template <int NQ>
-  __device__ void phi(const float (&s)[NQ][RUN], const f32x4_t (&axr)[PT], const uint4 (&cbq)[NQ],
-                      float (&out)[NQ]) const {
+  __device__ void phi(const float (&s)[NQ][RUN], const f32x4_t (&c0)[NQ][PT], float (&out)[NQ]) const {
     float den[NQ], num[NQ];
 #pragma unroll
     for (int q = 0; q < NQ; ++q) {
       f32x4_t lg[PT];
-      logits(s[q], axr, cbq[q], lg);
+      logits(s[q], c0[q], lg);
       weights(lg, s[q], 0.f, den[q], num[q]);
     }
     bool ok = true;
@@ -348,7 +351,7 @@ struct MolMlp {
       for (int q = 0; q < NQ; ++q) {
         if (__all(den[q] >= 0x1p-60f && den[q] <= 0x1p60f)) continue;
         f32x4_t lg[PT];
-        logits(s[q], axr, cbq[q], lg);
+        logits(s[q], c0[q], lg);
         float mx = -__builtin_inff();
 #pragma unroll
         for (int pt = 0; pt < PT; ++pt)
