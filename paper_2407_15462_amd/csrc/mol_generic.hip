@@ -333,6 +333,7 @@ int segment_size_for(int L, int k) {
   // One segment when it fits, else the largest segment (always >= 4k so
   // every pass shrinks the rows).
   if (L <= 256 && k <= 256) return 256;
+  if (L <= 512 && k <= 512) return 512;
   if (L <= 1024 && k <= 1024) return 1024;
   return 4096;
 }
@@ -343,6 +344,8 @@ hipError_t launch_segment_topk(const uint64_t* in, long in_stride, int rows, int
   dim3 grid((L + S - 1) / S, rows);
   if (S == 256)
     hipLaunchKernelGGL((k_segment_topk<256, 128>), grid, dim3(128), 0, st, in, in_stride, L, k, out, out_stride);
+  else if (S == 512)
+    hipLaunchKernelGGL((k_segment_topk<512, 256>), grid, dim3(256), 0, st, in, in_stride, L, k, out, out_stride);
   else if (S == 1024)
     hipLaunchKernelGGL((k_segment_topk<1024, 512>), grid, dim3(512), 0, st, in, in_stride, L, k, out, out_stride);
   else
