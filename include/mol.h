@@ -29,7 +29,8 @@
  *
  * Ordering: every top-k output row is sorted by score descending, ties
  * broken by item index ascending.  Where a row has fewer than k valid items
- * (mol_rerank only) it is padded with index -1 and score -INFINITY.
+ * (mol_rerank, mol_topk_exact_bounded) it is padded with index -1 and score
+ * -INFINITY.
  *
  * Errors: each entry point validates all arguments on the host before it
  * launches anything.  On error it returns a nonzero mol_status, launches
@@ -62,8 +63,17 @@ typedef enum {
   MOL_OP_SCORE = 0,
   MOL_OP_TOPK_EXACT = 1,
   MOL_OP_TOPK_PER_EMBD = 2,
-  MOL_OP_RERANK = 3
+  MOL_OP_RERANK = 3,
+  MOL_OP_TOPK_MAXDOT = 4,
+  MOL_OP_TOPK_BOUNDED = 5,
+  MOL_OP_TOPK_TWO_PASS = 6
 } mol_op;
+
+/* Threshold of the two-pass exact algorithm (mol_topk_two_pass). */
+typedef enum {
+  MOL_TWO_PASS_MIN = 0,  /* Algorithm 1: smallest MoL score over G           */
+  MOL_TWO_PASS_KTH = 1   /* k-th largest MoL score over G (tighter)          */
+} mol_two_pass_mode;
 
 /* Limits of the kernel set. */
 #define MOL_MAX_P 64      /* Pq * Px                                        */
@@ -113,6 +123,50 @@ int mol_score(const mol_problem *prob, int32_t n_begin, int32_t n_count,
  * bytes of workspace (any alignment of 256 bytes or more). */
 int mol_topk_exact(const mol_problem *prob, int32_t k, float *out_score,
                    int32_t *out_idx, void *ws, size_t ws_bytes, void *stream);
+
+/* Exact top-k with MoL among the items that can reach a per-query bound
+ * (Algorithm 1's RangeDotProduct followed by BruteForceTopKMoL, in one pass
+ * over the corpus).  phi is a convex combination of the s_p, so
+ * phi(q, x) <= m(q, x) = max_p s_p(q, x); for query b only items with
+ * m + margin >= bound[b] are scored and ranked, margin = 2^-12 (1 +
+ * max_p |s_p|) covering float32 rounding of phi.  Whenever bound[b] is at
+ * most the k-th largest phi over the corpus the result equals
+ * mol_topk_exact's, bit for bit; with a higher bound it is the top-k of the
+ * qualifying items (padded with -INFINITY / -1).  bound float32 [B], device.
+ * Groups of items that cannot qualify (nor beat the running k-th score)
+ * skip the gating MLP, which is where the time goes.  Same outputs, limits
+ * and workspace as mol_topk_exact (mol_workspace_size(MOL_OP_TOPK_BOUNDED)). */
+int mol_topk_exact_bounded(const mol_problem *prob, int32_t k,
+                           const float *bound, float *out_score,
+                           int32_t *out_idx, void *ws, size_t ws_bytes,
+                           void *stream);
+
+/* Two-pass exact top-k (Algorithm 1, Section 3.1):
+ *   1. G = union over p of TopKDotProduct(f_p(q), X_p) with K = k items each
+ *      (mol_topk_per_embd with kprime = k);
+ *   2. the bound: mode MOL_TWO_PASS_MIN, the smallest MoL score over G (the
+ *      algorithm as given); MOL_TWO_PASS_KTH, the k-th largest MoL score
+ *      over G (G holds k items scoring at least that much, so it is also at
+ *      most the corpus-wide k-th score: the same result, fewer items pass);
+ *   3. the exact top-k over the items with max_p s_p >= bound
+ *      (mol_topk_exact_bounded).
+ * out_score float32 [B][k], out_idx int32 [B][k]: equal to mol_topk_exact's
+ * output.  out_bound float32 [B] (may be NULL): the bound used per query.
+ * 1 <= k <= min(N, 1024) and P k <= 16384.  Needs every problem pointer and
+ * mol_workspace_size(MOL_OP_TOPK_TWO_PASS) bytes of workspace. */
+int mol_topk_two_pass(const mol_problem *prob, int32_t k, int32_t mode,
+                      float *out_score, int32_t *out_idx, float *out_bound,
+                      void *ws, size_t ws_bytes, void *stream);
+
+/* Max-component top-k (Section 3's "max approximation of MoL", a
+ * subsection the published text cuts): for every query, the k
+ * items with the largest m(q, x) = max_p s_p(q, x).  Since phi <= m, it is
+ * also the candidate generator whose k-th score bounds Algorithm 1's range.
+ * out_score float32 [B][k] (the m values), out_idx int32 [B][k].
+ * 1 <= k <= min(N, 1024).  Reads only Q and X (gating pointers may be NULL,
+ * H is ignored).  Workspace: mol_workspace_size(MOL_OP_TOPK_MAXDOT). */
+int mol_topk_maxdot(const mol_problem *prob, int32_t k, float *out_score,
+                    int32_t *out_idx, void *ws, size_t ws_bytes, void *stream);
 
 /* TopKPerEmbedding stage 1 (Algorithm 2, TopKDotProduct for every
  * component): for every query b and component p = pq * Px + px, the k'
@@ -169,7 +223,9 @@ int mol_gap_bound(int32_t B, int32_t P, int32_t m, const float *dots,
 /* Kernel timing, a diagnostic for throughput measurements.
  * mol_timing_enable(1) makes every later call record a pair of HIP events on
  * its stream around its main kernel: the fused scoring kernel of mol_score,
- * the scoring + per-range top-k scan of mol_topk_exact, the two
+ * the scoring + per-range top-k scan of mol_topk_exact (and of
+ * mol_topk_exact_bounded, mol_topk_maxdot), the whole sequence of
+ * mol_topk_two_pass, the two
  * per-component scans (with the threshold selection between them) of
  * mol_topk_per_embd and the candidate scoring of mol_rerank
  * (validation, merges of partial lists and decoding are outside the pair).

@@ -20,8 +20,11 @@ the stored bfloat16 / float32 arrays):
   component by dot product, union, dedup), TopKAvg (top-K by the dot product
   of the summed query and item components, Section 3.2), their combination,
   and the MoL rerank of the deduplicated candidates;
-* Algorithm 1 (exact two-pass top-K), Definition 2 (gap of an approximate
-  top-K) and the gap bounds of Theorems 2 and 3, used as cross-checks.
+* Algorithm 1 (exact two-pass top-K, with its second pass also available on
+  its own for a given threshold), the max approximation of MoL (top-K by
+  max_p s_p, a subsection of Section 3 cut from the published text),
+  Definition 2 (gap of an approximate top-K) and the gap bounds of
+  Theorems 2 and 3.
 
 Parity status: every function here is pinned by the CPU tests against the
 paper's worked example (Appendix B), closed forms or brute force, except the
@@ -326,17 +329,54 @@ def approx_topk(prob: Problem, b: int, k: int, kprime: int, k_avg: int = 0,
 # --------------------------------------------------------------------------
 # Cross-checks: Algorithm 1, Definition 2, Theorems 2 and 3
 # --------------------------------------------------------------------------
-def exact_two_pass(prob: Problem, b: int, k: int) -> Tuple[np.ndarray, np.ndarray]:
-    """Algorithm 1: top-k per component by dot product gives G; S_min is the
-    smallest MoL score over G; G' holds every item whose dot product reaches
-    S_min for some component; brute-force MoL top-k over G'."""
+def two_pass_threshold(prob: Problem, b: int, k: int, threshold: str = "min") -> float:
+    """Algorithm 1's first pass: G = union over p of the top-k items by s_p
+    (TopKDotProduct); the threshold is the smallest MoL score over G
+    ("min", the algorithm as given) or the k-th largest MoL score over G
+    ("kth": G holds k items scoring at least that much, so the corpus-wide
+    k-th score is no smaller and the second pass stays exact)."""
     s = all_dots(prob, b)
     G = union_dedup([topk_desc(s[:, p], k)[1] for p in range(prob.P)])
     _, _, phiG = mol_terms(prob, b, G)
-    s_min = phiG.min()
-    G2 = np.nonzero((s >= s_min).any(axis=1))[0]
-    _, _, phi2 = mol_terms(prob, b, G2)
-    return topk_desc(phi2, k, ids=G2)
+    if threshold == "min":
+        return float(phiG.min())
+    if threshold == "kth":
+        return kth_largest(phiG, k)
+    raise ValueError(threshold)
+
+
+def exact_topk_bounded(prob: Problem, b: int, k: int, bound: float
+                       ) -> Tuple[np.ndarray, np.ndarray]:
+    """Algorithm 1's second pass: G' holds every item whose dot product
+    reaches ``bound`` for some component (RangeDotProduct over all p); the
+    result is the brute-force MoL top-k over G', padded with (-inf, -1) when
+    G' has fewer than k items."""
+    s = all_dots(prob, b)
+    G2 = np.nonzero((s >= bound).any(axis=1))[0]
+    out_s = np.full(k, -np.inf)
+    out_i = np.full(k, -1, dtype=np.int64)
+    if G2.size:
+        _, _, phi2 = mol_terms(prob, b, G2)
+        v, i = topk_desc(phi2, k, ids=G2)
+        out_s[:len(v)], out_i[:len(i)] = v, i
+    return out_s, out_i
+
+
+def exact_two_pass(prob: Problem, b: int, k: int, threshold: str = "min"
+                   ) -> Tuple[np.ndarray, np.ndarray]:
+    """Algorithm 1: top-k per component by dot product gives G; S_min is the
+    smallest MoL score over G (or, with threshold="kth", the k-th largest);
+    G' holds every item whose dot product reaches it for some component;
+    brute-force MoL top-k over G'."""
+    return exact_topk_bounded(prob, b, k, two_pass_threshold(prob, b, k, threshold))
+
+
+def max_dot_topk(prob: Problem, b: int, k: int) -> Tuple[np.ndarray, np.ndarray]:
+    """Max approximation of MoL (a subsection of Section 3 that the published
+    text cuts): each item is scored by the largest of its component dot
+    products, m = max_p s_p, and the top-k items by m are returned as
+    (m values [k], ids [k])."""
+    return topk_desc(all_dots(prob, b).max(axis=1), k)
 
 
 def gap(phi_all: np.ndarray, approx_ids: np.ndarray, k: int) -> float:

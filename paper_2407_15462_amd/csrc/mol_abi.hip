@@ -40,7 +40,7 @@ int hip_fail(hipError_t e, const char* where) {
 // Kernel timing: while enabled, event pairs recorded on the caller's stream
 // around each entry point's main kernel; read (and recycled) by
 // mol_timing_read.
-constexpr int kTimedOps = 4;                  // mol_op codes 0..3
+constexpr int kTimedOps = 7;                  // mol_op codes 0..6
 
 struct EvPair {
   hipEvent_t a = nullptr, b = nullptr;
@@ -88,10 +88,11 @@ void timing_stop(int op, const EvPair& p, hipStream_t st, bool launched) {
   (ok ? t.rec[op] : t.spare).push_back(p);
 }
 
-// Launch `expr` (a hipError_t expression) between the events of `op`.
+// Launch `expr` (a hipError_t expression) between the events of `op`
+// (op < 0: not recorded).
 #define MOL_TIMED_LAUNCH(op, st, expr, where)              \
   do {                                                     \
-    const EvPair tp_ = timing_start(st);                   \
+    const EvPair tp_ = (op) >= 0 ? timing_start(st) : EvPair{}; \
     const hipError_t te_ = (expr);                         \
     timing_stop((op), tp_, (st), te_ == hipSuccess);       \
     MOL_TRY_HIP(te_, where);                               \
@@ -301,6 +302,33 @@ size_t exact_ws_bytes(const DevProb& pr, int k) {
   return fused_supported(pr, k) ? plan_fused_exact(pr, k).bytes : plan_stream(pr.B, pr.N, k).bytes;
 }
 
+size_t maxdot_ws_bytes(const DevProb& pr, int k) {
+  return fused_maxdot_supported(pr, k) ? plan_fused_exact(pr, k).bytes : plan_stream(pr.B, pr.N, k).bytes;
+}
+
+// Algorithm 1 workspace: per-component lists, the rerank output over G,
+// the bound, and one region shared by the three phases (they run in order
+// on one stream).
+struct TwoPassPlan {
+  size_t offDots = 0, offIdx = 0, offScore = 0, offRidx = 0, offBound = 0, offWork = 0, bytes = 0;
+};
+
+TwoPassPlan plan_two_pass(const DevProb& pr, int k) {
+  TwoPassPlan t;
+  const size_t lists = static_cast<size_t>(pr.B) * pr.P * k;
+  size_t off = 0;
+  t.offDots = off;  off = align_up(off + 4 * lists);
+  t.offIdx = off;   off = align_up(off + 4 * lists);
+  t.offScore = off; off = align_up(off + 4ul * pr.B * k);
+  t.offRidx = off;  off = align_up(off + 4ul * pr.B * k);
+  t.offBound = off; off = align_up(off + 4ul * pr.B);
+  t.offWork = off;
+  const size_t work = std::max({per_embd_ws_bytes(pr, k), plan_rerank(pr, pr.P * k, k).bytes,
+                                exact_ws_bytes(pr, k)});
+  t.bytes = off + align_up(work);
+  return t;
+}
+
 int check_ws(void* ws, size_t have, size_t need) {
   if (need == 0) return MOL_OK;
   if (!ws) return fail(MOL_EINVAL, "workspace is NULL (need %zu bytes)", need);
@@ -313,6 +341,148 @@ int check_ws(void* ws, size_t have, size_t need) {
 int check_k(int32_t k, int32_t N, const char* name) {
   if (k < 1 || k > MOL_MAX_K) return fail(MOL_EINVAL, "%s = %d outside [1, %d]", name, k, MOL_MAX_K);
   if (k > N) return fail(MOL_EINVAL, "%s = %d exceeds N = %d", name, k, N);
+  return MOL_OK;
+}
+
+// Algorithm 1 reranks the P k candidates of the first pass
+int check_two_pass_k(const mol_problem* prob, int32_t k) {
+  int rc;
+  if ((rc = check_k(k, prob->N, "k"))) return rc;
+  const long C = static_cast<long>(prob->Pq) * prob->Px * k;
+  if (C > MOL_MAX_C) return fail(MOL_EINVAL, "P * k = %ld candidates exceed %d", C, MOL_MAX_C);
+  return MOL_OK;
+}
+
+// ---------------------------------------------------------------------------
+// Entry-point bodies (arguments already validated, workspace checked).
+// timed_op: mol_op code under which the main kernel is timed, -1 for none.
+// ---------------------------------------------------------------------------
+
+// Exact MoL top-k over the corpus; with `bound` ([B] floats) only the items
+// whose max_p s_p can reach bound[b] are ranked.
+int run_exact(const DevProb& pr, int k, const float* bound, float* out_score, int32_t* out_idx,
+              char* w, int timed_op, hipStream_t st) {
+  int rc;
+  if (fused_supported(pr, k)) {
+    const FusedExactPlan f = plan_fused_exact(pr, k);
+    uint64_t* partial = reinterpret_cast<uint64_t*>(w + f.s.offA);
+    uint64_t* fin = reinterpret_cast<uint64_t*>(w + f.offFinal);
+    MOL_TIMED_LAUNCH(timed_op, st, launch_fused_topk(pr, k, f.R, f.range_len, f.G, bound, partial, st),
+                     "fused MoL top-k");
+    if ((rc = reduce_rows(f.s, w, static_cast<long>(f.R) * k, fin, k, st))) return rc;
+    MOL_TRY_HIP(launch_decode(fin, k, pr.B, k, out_score, out_idx, st), "decode");
+    return MOL_OK;
+  }
+  const StreamPlan s = plan_stream(pr.B, pr.N, k);
+  const int mode = bound ? kGenBounded : kGenPhi;
+  auto tile = [&](int n0, int nt, uint64_t* A, long strideA) {
+    return launch_phi_generic(pr, mode, bound, n0, nt, nullptr, nullptr, 0, nullptr, 0, A, strideA, st);
+  };
+  return stream_topk(s, pr.N, w, tile, out_score, out_idx, st);
+}
+
+// Top-k by the largest component dot product max_p s_p.
+int run_maxdot(const DevProb& pr, int k, float* out_score, int32_t* out_idx, char* w, int timed_op,
+               hipStream_t st) {
+  int rc;
+  if (fused_maxdot_supported(pr, k)) {
+    const FusedExactPlan f = plan_fused_exact(pr, k);
+    uint64_t* partial = reinterpret_cast<uint64_t*>(w + f.s.offA);
+    uint64_t* fin = reinterpret_cast<uint64_t*>(w + f.offFinal);
+    MOL_TIMED_LAUNCH(timed_op, st, launch_fused_maxdot(pr, k, f.R, f.range_len, f.G, partial, st),
+                     "fused max-dot top-k");
+    if ((rc = reduce_rows(f.s, w, static_cast<long>(f.R) * k, fin, k, st))) return rc;
+    MOL_TRY_HIP(launch_decode(fin, k, pr.B, k, out_score, out_idx, st), "decode");
+    return MOL_OK;
+  }
+  const StreamPlan s = plan_stream(pr.B, pr.N, k);
+  auto tile = [&](int n0, int nt, uint64_t* A, long strideA) {
+    return launch_phi_generic(pr, kGenMaxDot, nullptr, n0, nt, nullptr, nullptr, 0, nullptr, 0, A, strideA,
+                              st);
+  };
+  return stream_topk(s, pr.N, w, tile, out_score, out_idx, st);
+}
+
+int run_per_embd(const DevProb& pr, int kprime, float* out_dot, int32_t* out_idx, char* w, int timed_op,
+                 hipStream_t st) {
+  int rc;
+  const int rows = pr.B * pr.P;
+  if (per_embd_supported(pr, kprime)) {
+    const PerEmbdPlan f = plan_per_embd(pr, kprime);
+    uint64_t* lists = reinterpret_cast<uint64_t*>(w + f.s.offA);
+    uint64_t* fin = reinterpret_cast<uint64_t*>(w + f.offFinal);
+    uint64_t* stg = reinterpret_cast<uint64_t*>(w + f.offStg);
+    float* bmax = reinterpret_cast<float*>(w + f.offBmax);
+    float* thr = reinterpret_cast<float*>(w + f.offThr);
+    MOL_TIMED_LAUNCH(timed_op, st, launch_per_embd(pr, kprime, f.g, bmax, thr, lists, stg, st),
+                     "per-component top-k'");
+    if ((rc = reduce_rows(f.s, w, static_cast<long>(f.g.s2.R) * f.KL, fin, kprime, st))) return rc;
+    MOL_TRY_HIP(launch_decode(fin, kprime, rows, kprime, out_dot, out_idx, st), "decode");
+    return MOL_OK;
+  }
+  const StreamPlan s = plan_stream(rows, pr.N, kprime);
+  auto tile = [&](int n0, int nt, uint64_t* A, long strideA) {
+    return launch_dots_generic(pr, n0, nt, A, strideA, st);
+  };
+  return stream_topk(s, pr.N, w, tile, out_dot, out_idx, st);
+}
+
+// Union + dedup of two candidate sets, then MoL top-k over the distinct ids
+// (by -phi when `negate`: the smallest scores first).
+int run_rerank(const DevProb& pr, const int32_t* cand, int C, const int32_t* cand2, int C2, int k,
+               bool negate, float* out_score, int32_t* out_idx, int32_t* out_n_unique, char* w,
+               int timed_op, hipStream_t st) {
+  int rc;
+  const int CT = C + C2;
+  const RerankPlan r = plan_rerank(pr, CT, k);
+  int32_t* uniq = reinterpret_cast<int32_t*>(w + r.offUniq);
+  int32_t* nu = reinterpret_cast<int32_t*>(w + r.offNu);
+  uint64_t* A = reinterpret_cast<uint64_t*>(w + r.s.offA);
+  uint64_t* fin = reinterpret_cast<uint64_t*>(w + r.offFinal);
+  MOL_TRY_HIP(launch_dedup(cand, C, cand2, C2, pr.B, pr.N, uniq, nu, st), "dedup");
+  if (rerank_supported(pr, k)) {
+    const int chunk = rerank_chunk(CT);
+    const long L0 = static_cast<long>((CT + chunk - 1) / chunk) * k;
+    MOL_TIMED_LAUNCH(timed_op, st, launch_rerank(pr, uniq, nu, CT, k, negate, A, st), "fused rerank");
+    if ((rc = reduce_rows(r.s, w, L0, fin, k, st))) return rc;
+  } else {
+    MOL_TIMED_LAUNCH(timed_op, st,
+                     launch_phi_generic(pr, negate ? kGenNegPhi : kGenPhi, nullptr, 0, CT, uniq, nu, CT,
+                                        nullptr, 0, A, r.s.strideA, st),
+                     "rerank score");
+    if ((rc = reduce_rows(r.s, w, CT, fin, k, st))) return rc;
+  }
+  MOL_TRY_HIP(launch_decode(fin, k, pr.B, k, out_score, out_idx, st), "decode");
+  if (out_n_unique)
+    MOL_TRY_HIP(hipMemcpyAsync(out_n_unique, nu, sizeof(int32_t) * pr.B, hipMemcpyDeviceToDevice, st),
+                "copy n_unique");
+  return MOL_OK;
+}
+
+// Algorithm 1: G = union over p of TopKDotProduct(k); the bound from the
+// MoL scores over G; then the exact top-k over the items whose max_p s_p
+// reaches the bound (RangeDotProduct + BruteForceTopKMoL in one pass).
+int run_two_pass(const DevProb& pr, int k, int mode, float* out_score, int32_t* out_idx,
+                 float* out_bound, char* w, hipStream_t st) {
+  int rc;
+  const TwoPassPlan t = plan_two_pass(pr, k);
+  float* dots = reinterpret_cast<float*>(w + t.offDots);
+  int32_t* ids = reinterpret_cast<int32_t*>(w + t.offIdx);
+  float* rscore = reinterpret_cast<float*>(w + t.offScore);
+  int32_t* ridx = reinterpret_cast<int32_t*>(w + t.offRidx);
+  float* bound = reinterpret_cast<float*>(w + t.offBound);
+  char* work = w + t.offWork;
+  if ((rc = run_per_embd(pr, k, dots, ids, work, -1, st))) return rc;
+  const bool smallest = mode == MOL_TWO_PASS_MIN;
+  const int kk = smallest ? 1 : k;
+  if ((rc = run_rerank(pr, ids, pr.P * k, nullptr, 0, kk, smallest, rscore, ridx, nullptr, work, -1, st)))
+    return rc;
+  // MIN: bound = min over G of phi = -(top-1 of -phi); KTH: the k-th largest
+  MOL_TRY_HIP(launch_pick_bound(rscore, kk, kk - 1, smallest ? -1.f : 1.f, pr.B, bound, st), "bound");
+  if ((rc = run_exact(pr, k, bound, out_score, out_idx, work, -1, st))) return rc;
+  if (out_bound)
+    MOL_TRY_HIP(hipMemcpyAsync(out_bound, bound, sizeof(float) * pr.B, hipMemcpyDeviceToDevice, st),
+                "copy bound");
   return MOL_OK;
 }
 
@@ -358,6 +528,21 @@ int mol_workspace_size(const mol_problem* prob, int op, int32_t k, int32_t kprim
       if (C < 1 || C > MOL_MAX_C) return fail(MOL_EINVAL, "C = %d outside [1, %d]", C, MOL_MAX_C);
       *bytes = plan_rerank(dev_prob(prob), C, k).bytes;
       return MOL_OK;
+    case MOL_OP_TOPK_MAXDOT:
+      if ((rc = check_problem(prob, false))) return rc;
+      if ((rc = check_k(k, prob->N, "k"))) return rc;
+      *bytes = maxdot_ws_bytes(dev_prob(prob), k);
+      return MOL_OK;
+    case MOL_OP_TOPK_BOUNDED:
+      if ((rc = check_problem(prob, true))) return rc;
+      if ((rc = check_k(k, prob->N, "k"))) return rc;
+      *bytes = exact_ws_bytes(dev_prob(prob), k);
+      return MOL_OK;
+    case MOL_OP_TOPK_TWO_PASS:
+      if ((rc = check_problem(prob, true))) return rc;
+      if ((rc = check_two_pass_k(prob, k))) return rc;
+      *bytes = plan_two_pass(dev_prob(prob), k).bytes;
+      return MOL_OK;
     default:
       return fail(MOL_EINVAL, "unknown op %d", op);
   }
@@ -377,7 +562,8 @@ int mol_score(const mol_problem* prob, int32_t n_begin, int32_t n_count, float* 
     return MOL_OK;
   }
   MOL_TIMED_LAUNCH(MOL_OP_SCORE, st,
-                   launch_phi_generic(pr, n_begin, n_count, nullptr, nullptr, 0, phi, n_count, nullptr, 0, st),
+                   launch_phi_generic(pr, kGenPhi, nullptr, n_begin, n_count, nullptr, nullptr, 0, phi, n_count,
+                                      nullptr, 0, st),
                    "mol_score");
   return MOL_OK;
 }
@@ -388,26 +574,52 @@ int mol_topk_exact(const mol_problem* prob, int32_t k, float* out_score, int32_t
   if ((rc = check_problem(prob, true))) return rc;
   if ((rc = check_k(k, prob->N, "k"))) return rc;
   if (!out_score || !out_idx) return fail(MOL_EINVAL, "output pointer is NULL");
-  hipStream_t st = static_cast<hipStream_t>(stream);
   const DevProb pr = dev_prob(prob);
-  if (fused_supported(pr, k)) {
-    const FusedExactPlan f = plan_fused_exact(pr, k);
-    if ((rc = check_ws(ws, ws_bytes, f.bytes))) return rc;
-    char* w = static_cast<char*>(ws);
-    uint64_t* partial = reinterpret_cast<uint64_t*>(w + f.s.offA);
-    uint64_t* fin = reinterpret_cast<uint64_t*>(w + f.offFinal);
-    MOL_TIMED_LAUNCH(MOL_OP_TOPK_EXACT, st, launch_fused_topk(pr, k, f.R, f.range_len, f.G, partial, st),
-                     "fused MoL top-k");
-    if ((rc = reduce_rows(f.s, w, static_cast<long>(f.R) * k, fin, k, st))) return rc;
-    MOL_TRY_HIP(launch_decode(fin, k, prob->B, k, out_score, out_idx, st), "decode");
-    return MOL_OK;
-  }
-  const StreamPlan s = plan_stream(prob->B, prob->N, k);
-  if ((rc = check_ws(ws, ws_bytes, s.bytes))) return rc;
-  auto tile = [&](int n0, int nt, uint64_t* A, long strideA) {
-    return launch_phi_generic(pr, n0, nt, nullptr, nullptr, 0, nullptr, 0, A, strideA, st);
-  };
-  return stream_topk(s, prob->N, static_cast<char*>(ws), tile, out_score, out_idx, st);
+  if ((rc = check_ws(ws, ws_bytes, exact_ws_bytes(pr, k)))) return rc;
+  return run_exact(pr, k, nullptr, out_score, out_idx, static_cast<char*>(ws), MOL_OP_TOPK_EXACT,
+                   static_cast<hipStream_t>(stream));
+}
+
+int mol_topk_exact_bounded(const mol_problem* prob, int32_t k, const float* bound, float* out_score,
+                           int32_t* out_idx, void* ws, size_t ws_bytes, void* stream) {
+  int rc;
+  if ((rc = check_problem(prob, true))) return rc;
+  if ((rc = check_k(k, prob->N, "k"))) return rc;
+  if (!bound) return fail(MOL_EINVAL, "bound is NULL");
+  if (!out_score || !out_idx) return fail(MOL_EINVAL, "output pointer is NULL");
+  const DevProb pr = dev_prob(prob);
+  if ((rc = check_ws(ws, ws_bytes, exact_ws_bytes(pr, k)))) return rc;
+  return run_exact(pr, k, bound, out_score, out_idx, static_cast<char*>(ws), MOL_OP_TOPK_BOUNDED,
+                   static_cast<hipStream_t>(stream));
+}
+
+int mol_topk_maxdot(const mol_problem* prob, int32_t k, float* out_score, int32_t* out_idx, void* ws,
+                    size_t ws_bytes, void* stream) {
+  int rc;
+  if ((rc = check_problem(prob, false))) return rc;
+  if ((rc = check_k(k, prob->N, "k"))) return rc;
+  if (!out_score || !out_idx) return fail(MOL_EINVAL, "output pointer is NULL");
+  const DevProb pr = dev_prob(prob);
+  if ((rc = check_ws(ws, ws_bytes, maxdot_ws_bytes(pr, k)))) return rc;
+  return run_maxdot(pr, k, out_score, out_idx, static_cast<char*>(ws), MOL_OP_TOPK_MAXDOT,
+                    static_cast<hipStream_t>(stream));
+}
+
+int mol_topk_two_pass(const mol_problem* prob, int32_t k, int32_t mode, float* out_score, int32_t* out_idx,
+                      float* out_bound, void* ws, size_t ws_bytes, void* stream) {
+  int rc;
+  if ((rc = check_problem(prob, true))) return rc;
+  if ((rc = check_two_pass_k(prob, k))) return rc;
+  if (mode != MOL_TWO_PASS_MIN && mode != MOL_TWO_PASS_KTH)
+    return fail(MOL_EINVAL, "mode = %d is not MOL_TWO_PASS_MIN or MOL_TWO_PASS_KTH", mode);
+  if (!out_score || !out_idx) return fail(MOL_EINVAL, "output pointer is NULL");
+  const DevProb pr = dev_prob(prob);
+  if ((rc = check_ws(ws, ws_bytes, plan_two_pass(pr, k).bytes))) return rc;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const EvPair tp = timing_start(st);
+  rc = run_two_pass(pr, k, mode, out_score, out_idx, out_bound, static_cast<char*>(ws), st);
+  timing_stop(MOL_OP_TOPK_TWO_PASS, tp, st, rc == MOL_OK);
+  return rc;
 }
 
 int mol_topk_per_embd(const mol_problem* prob, int32_t kprime, float* out_dot, int32_t* out_idx,
@@ -416,30 +628,10 @@ int mol_topk_per_embd(const mol_problem* prob, int32_t kprime, float* out_dot, i
   if ((rc = check_problem(prob, false))) return rc;
   if ((rc = check_k(kprime, prob->N, "kprime"))) return rc;
   if (!out_dot || !out_idx) return fail(MOL_EINVAL, "output pointer is NULL");
-  const int rows = prob->B * prob->Pq * prob->Px;
-  hipStream_t st = static_cast<hipStream_t>(stream);
   const DevProb pr = dev_prob(prob);
-  if (per_embd_supported(pr, kprime)) {
-    const PerEmbdPlan f = plan_per_embd(pr, kprime);
-    if ((rc = check_ws(ws, ws_bytes, f.bytes))) return rc;
-    char* w = static_cast<char*>(ws);
-    uint64_t* lists = reinterpret_cast<uint64_t*>(w + f.s.offA);
-    uint64_t* fin = reinterpret_cast<uint64_t*>(w + f.offFinal);
-    uint64_t* stg = reinterpret_cast<uint64_t*>(w + f.offStg);
-    float* bmax = reinterpret_cast<float*>(w + f.offBmax);
-    float* thr = reinterpret_cast<float*>(w + f.offThr);
-    MOL_TIMED_LAUNCH(MOL_OP_TOPK_PER_EMBD, st, launch_per_embd(pr, kprime, f.g, bmax, thr, lists, stg, st),
-                     "per-component top-k'");
-    if ((rc = reduce_rows(f.s, w, static_cast<long>(f.g.s2.R) * f.KL, fin, kprime, st))) return rc;
-    MOL_TRY_HIP(launch_decode(fin, kprime, rows, kprime, out_dot, out_idx, st), "decode");
-    return MOL_OK;
-  }
-  const StreamPlan s = plan_stream(rows, prob->N, kprime);
-  if ((rc = check_ws(ws, ws_bytes, s.bytes))) return rc;
-  auto tile = [&](int n0, int nt, uint64_t* A, long strideA) {
-    return launch_dots_generic(pr, n0, nt, A, strideA, st);
-  };
-  return stream_topk(s, prob->N, static_cast<char*>(ws), tile, out_dot, out_idx, st);
+  if ((rc = check_ws(ws, ws_bytes, per_embd_ws_bytes(pr, kprime)))) return rc;
+  return run_per_embd(pr, kprime, out_dot, out_idx, static_cast<char*>(ws), MOL_OP_TOPK_PER_EMBD,
+                      static_cast<hipStream_t>(stream));
 }
 
 int mol_rerank(const mol_problem* prob, const int32_t* cand, int32_t C, const int32_t* cand2, int32_t C2,
@@ -453,31 +645,9 @@ int mol_rerank(const mol_problem* prob, const int32_t* cand, int32_t C, const in
   if (!cand || !out_score || !out_idx) return fail(MOL_EINVAL, "cand or output pointer is NULL");
   if (C2 > 0 && !cand2) return fail(MOL_EINVAL, "cand2 is NULL with C2 = %d", C2);
   const DevProb pr = dev_prob(prob);
-  const int CT = C + C2;
-  const RerankPlan r = plan_rerank(pr, CT, k);
-  if ((rc = check_ws(ws, ws_bytes, r.bytes))) return rc;
-  hipStream_t st = static_cast<hipStream_t>(stream);
-  char* w = static_cast<char*>(ws);
-  int32_t* uniq = reinterpret_cast<int32_t*>(w + r.offUniq);
-  int32_t* nu = reinterpret_cast<int32_t*>(w + r.offNu);
-  uint64_t* A = reinterpret_cast<uint64_t*>(w + r.s.offA);
-  uint64_t* fin = reinterpret_cast<uint64_t*>(w + r.offFinal);
-  MOL_TRY_HIP(launch_dedup(cand, C, cand2, C2, prob->B, prob->N, uniq, nu, st), "dedup");
-  if (rerank_supported(pr, k)) {
-    const int chunk = rerank_chunk(CT);
-    const long L0 = static_cast<long>((CT + chunk - 1) / chunk) * k;
-    MOL_TIMED_LAUNCH(MOL_OP_RERANK, st, launch_rerank(pr, uniq, nu, CT, k, A, st), "fused rerank");
-    if ((rc = reduce_rows(r.s, w, L0, fin, k, st))) return rc;
-  } else {
-    MOL_TIMED_LAUNCH(MOL_OP_RERANK, st, launch_phi_generic(pr, 0, CT, uniq, nu, CT, nullptr, 0, A, r.s.strideA, st),
-                     "rerank score");
-    if ((rc = reduce_rows(r.s, w, CT, fin, k, st))) return rc;
-  }
-  MOL_TRY_HIP(launch_decode(fin, k, prob->B, k, out_score, out_idx, st), "decode");
-  if (out_n_unique)
-    MOL_TRY_HIP(hipMemcpyAsync(out_n_unique, nu, sizeof(int32_t) * prob->B, hipMemcpyDeviceToDevice, st),
-                "copy n_unique");
-  return MOL_OK;
+  if ((rc = check_ws(ws, ws_bytes, plan_rerank(pr, C + C2, k).bytes))) return rc;
+  return run_rerank(pr, cand, C, cand2, C2, k, false, out_score, out_idx, out_n_unique, static_cast<char*>(ws),
+                    MOL_OP_RERANK, static_cast<hipStream_t>(stream));
 }
 
 int mol_avg_embed(const mol_problem* prob, void* q_avg, void* x_avg, void* stream) {

@@ -9,8 +9,19 @@
 // and phi (Eq. 1 / Eq. 2 with the SiLU gating MLP of Appendix A.3) without
 // any LDS re-layout.
 //
-// Epilogues: a running per-query top-k (Definition 1) kept in LDS with
-// threshold rejection, or a dense phi store.
+// Epilogues (EPI):
+//  - kEpiTopk: a running per-query top-k of phi (Definition 1) kept in LDS
+//    with threshold rejection;
+//  - kEpiDense: a dense phi store;
+//  - kEpiBounded: the same top-k over the items that can reach a per-query
+//    bound: phi is a convex combination of the s_p, so phi <= m = max_p s_p,
+//    and an item whose m (plus a rounding margin) stays below the bound, or
+//    below the running k-th score, cannot be in the result.  Groups of 16
+//    items where no item can are skipped before the gating MLP (Algorithm 1's
+//    RangeDotProduct + BruteForceTopKMoL in one pass);
+//  - kEpiMaxDot: a running top-k of m itself, without the gating MLP
+//    (Section 3's max approximation of MoL, a subsection cut from the
+//    published text).
 //
 // Workgroup: 8 waves (2 per SIMD) = 16 queries sharing an LDS-staged
 // stream of 32-item tiles (a three-deep ring) loaded with direct
@@ -23,13 +34,16 @@ using namespace tile;
 
 namespace {
 
+enum FusedEpi { kEpiTopk = 0, kEpiDense = 1, kEpiBounded = 2, kEpiMaxDot = 3 };
+
 constexpr int kWaves = 8;
 constexpr int kQueriesPerWG = 2 * kWaves;
 constexpr int kTile = 32;        // items per LDS stage (two 16-item steps)
 constexpr int kRing = 3;         // item stages in flight
 constexpr int kTopkRegion = WaveTopk::kList + WaveTopk::kStage;
 
-template <int PX, int D, int H>
+// PX, D, H: shape; AX: the gating inputs (a_x stream, a_q + b2) are needed
+template <int PX, int D, int H, bool AX>
 struct FusedShape {
   static constexpr int P = 8 * PX;
   static constexpr int RUN = 2 * PX;     // s values per lane per query
@@ -38,10 +52,10 @@ struct FusedShape {
   static constexpr int XROWCH = D / 8;   // 16-byte chunks per X row
   static constexpr int AROWCH = P / 4;   // 16-byte chunks per a_x row
   static constexpr int XSTAGE = PX * kTile * D * 2;   // bytes of one X stage
-  static constexpr int ASTAGE = kTile * P * 4;        // bytes of one a_x stage
+  static constexpr int ASTAGE = AX ? kTile * P * 4 : 0;   // bytes of one a_x stage
   static constexpr int LDS_X = kRing * XSTAGE;
   static constexpr int LDS_AX = kRing * ASTAGE;
-  static constexpr int LDS_CB = kQueriesPerWG * P * 4;   // [query][p] log2(e) (a_q + b2), f32
+  static constexpr int LDS_CB = AX ? kQueriesPerWG * P * 4 : 0;   // [query][p] log2(e) (a_q + b2), f32
   static constexpr int LDS_TOPK = kQueriesPerWG * kTopkRegion * 8;
   static constexpr int LDS_TOTAL = LDS_X + LDS_AX + LDS_CB + LDS_TOPK;
   // 16-byte global->LDS copies per stage, in 1 KB blocks of one wave each
@@ -67,11 +81,14 @@ __device__ __forceinline__ void wg_coords(int g, int R, int G, int& r, int& qg) 
 
 }  // namespace
 
-template <int PX, int D, int H, bool DENSE>
+template <int PX, int D, int H, int EPI>
 __global__ __launch_bounds__(64 * kWaves, 1) void k_mol_fused(
     DevProb pr, int k, int R, int range_len, int G, int n_begin, int n_end,
-    uint64_t* __restrict__ partial, float* __restrict__ phi_out, long phi_stride) {
-  using S = FusedShape<PX, D, H>;
+    const float* __restrict__ bound, uint64_t* __restrict__ partial, float* __restrict__ phi_out,
+    long phi_stride) {
+  constexpr bool DENSE = EPI == kEpiDense;
+  constexpr bool MLP = EPI != kEpiMaxDot;
+  using S = FusedShape<PX, D, H, MLP>;
   using Mlp = MolMlp<PX, H>;
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   unsigned char* sX = smem;
@@ -117,7 +134,7 @@ __global__ __launch_bounds__(64 * kWaves, 1) void k_mol_fused(
       unsigned char* dst = sX + buf * S::XSTAGE + blk * 1024;
       copy16_to_lds(src, lds_addr(dst));
     }
-    for (int blk = wave; blk < S::ABLOCKS; blk += kWaves) {
+    for (int blk = wave; MLP && blk < S::ABLOCKS; blk += kWaves) {
       const int pos = blk * 64 + lane;
       const int n = pos / S::AROWCH, phys = pos % S::AROWCH;
       const int cc = phys ^ (n % S::AROWCH);
@@ -131,17 +148,23 @@ __global__ __launch_bounds__(64 * kWaves, 1) void k_mol_fused(
 
   // ---- per-workgroup constants ----
   // log2(e) (a_q + b2) per query of the workgroup, [query][p]
-  for (int i = tid; i < kQueriesPerWG * P; i += 64 * kWaves) {
-    const int qi = i / P, p = i % P, b = qwg + qi;
-    sCb[i] = b < pr.B ? kLog2e * (pr.a_q[static_cast<long>(b) * P + p] + pr.b2[p]) : 0.f;
-  }
+  if (MLP)
+    for (int i = tid; i < kQueriesPerWG * P; i += 64 * kWaves) {
+      const int qi = i / P, p = i % P, b = qwg + qi;
+      sCb[i] = b < pr.B ? kLog2e * (pr.a_q[static_cast<long>(b) * P + p] + pr.b2[p]) : 0.f;
+    }
   WaveTopk top[2];
   if (!DENSE) {
     top[0].init(sTop + (2 * wave + 0) * kTopkRegion, k, lane);
     top[1].init(sTop + (2 * wave + 1) * kTopkRegion, k, lane);
   }
+  // per-query bound of the bounded epilogue (queries past B: +inf, skipped)
+  float qbound[2];
+#pragma unroll
+  for (int qb = 0; qb < 2; ++qb)
+    qbound[qb] = EPI == kEpiBounded && qwv + qb < pr.B ? bound[qwv + qb] : __builtin_inff();
   Mlp mlp;
-  mlp.load(pr, c, g);
+  if (MLP) mlp.load(pr, c, g);
   // Q as GEMM1 A operands: row c = 8 q + pq, K slot 8g+e <-> d = 32 kk + 8 g + e
   uint4 qop[S::KD];
   {
@@ -185,11 +208,13 @@ __global__ __launch_bounds__(64 * kWaves, 1) void k_mol_fused(
 #pragma unroll
       for (int q4 = 0; q4 < S::PT; ++q4) {
         const int phys = (base / 4 + q4) ^ (n % S::AROWCH);
-        axv[q4] = *reinterpret_cast<const float4*>(as + n * (P * 4) + 16 * phys);
+        axv[q4] = MLP ? *reinterpret_cast<const float4*>(as + n * (P * 4) + 16 * phys)
+                      : float4{0.f, 0.f, 0.f, 0.f};
       }
       __builtin_amdgcn_sched_barrier(0);
 
       // GEMM1: both queries x 16 items x all px
+      __builtin_amdgcn_s_setprio(1);
       f32x4_t acc1[PX];
 #pragma unroll
       for (int px = 0; px < PX; ++px) {
@@ -197,6 +222,7 @@ __global__ __launch_bounds__(64 * kWaves, 1) void k_mol_fused(
 #pragma unroll
         for (int kk = 0; kk < S::KD; ++kk) acc1[px] = mfma_bf16(qop[kk], xb[px][kk], acc1[px]);
       }
+      mfma_priority_end();
       // separate the two queries: s[q][mu] holds p = base(g) + mu
       float s2[2][S::RUN];
 #pragma unroll
@@ -207,30 +233,50 @@ __global__ __launch_bounds__(64 * kWaves, 1) void k_mol_fused(
         s2[0][mu] = __uint_as_float(sw[0]);
         s2[1][mu] = __uint_as_float(sw[1]);
       }
-      // a_x (scaled by log2 e) in the GEMM3 accumulator layout
-      f32x4_t axr[S::PT];
-#pragma unroll
-      for (int q4 = 0; q4 < S::PT; ++q4)
-        axr[q4] = f32x4_t{kLog2e * axv[q4].x, kLog2e * axv[q4].y, kLog2e * axv[q4].z, kLog2e * axv[q4].w};
-
       // the two queries one after the other (keeps the register peak low)
       float phi[2];
+      bool offer[2];
 #pragma unroll
       for (int qb = 0; qb < 2; ++qb) {
-        float sq[1][S::RUN];
+        offer[qb] = item_ok;
+        if constexpr (EPI == kEpiBounded || EPI == kEpiMaxDot) {
+          // m = max_p s_p of the lane's item (and max_p |s_p| for the margin)
+          float m = s2[qb][0], mabs = fabsf(s2[qb][0]);
 #pragma unroll
-        for (int mu = 0; mu < S::RUN; ++mu) sq[0][mu] = s2[qb][mu];
-        // + log2(e) (a_q + b2) of the query at the lane's p = base(g) + 4 pt + i
-        f32x4_t c0[1][S::PT];
-#pragma unroll
-        for (int pt = 0; pt < S::PT; ++pt) {
-          const float4 cb = *reinterpret_cast<const float4*>(sCb + (2 * wave + qb) * P + base + 4 * pt);
-          c0[0][pt] = axr[pt] + f32x4_t{cb.x, cb.y, cb.z, cb.w};
+          for (int mu = 1; mu < S::RUN; ++mu) {
+            m = fmaxf(m, s2[qb][mu]);
+            if (EPI == kEpiBounded) mabs = fmaxf(mabs, fabsf(s2[qb][mu]));
+          }
+          m = max_groups(m);
+          if constexpr (EPI == kEpiMaxDot) {
+            phi[qb] = m;
+            continue;
+          } else {
+            mabs = max_groups(mabs);
+            const float floor = fmaxf(qbound[qb], top[qb].theta_score);
+            offer[qb] = item_ok && m + bound_margin(mabs) >= floor;
+            phi[qb] = -__builtin_inff();
+            if (!__any(offer[qb])) continue;   // no item of the group can qualify
+          }
         }
-        float pq[1];
-        mlp.template phi<1>(sq, c0, pq);
-        phi[qb] = pq[0];
-        __builtin_amdgcn_sched_barrier(0);
+        if constexpr (MLP) {
+          float sq[1][S::RUN];
+#pragma unroll
+          for (int mu = 0; mu < S::RUN; ++mu) sq[0][mu] = s2[qb][mu];
+          // GEMM3 accumulator input: log2(e) a_x (the item's, from the stage)
+          // + log2(e) (a_q + b2) (the query's), at the lane's p = base(g) + 4 pt + i
+          f32x4_t c0[1][S::PT];
+#pragma unroll
+          for (int pt = 0; pt < S::PT; ++pt) {
+            const float4 cb = *reinterpret_cast<const float4*>(sCb + (2 * wave + qb) * P + base + 4 * pt);
+            c0[0][pt] = f32x4_t{fmaf(axv[pt].x, kLog2e, cb.x), fmaf(axv[pt].y, kLog2e, cb.y),
+                                fmaf(axv[pt].z, kLog2e, cb.z), fmaf(axv[pt].w, kLog2e, cb.w)};
+          }
+          float pq[1];
+          mlp.template phi<1>(sq, c0, pq);
+          phi[qb] = pq[0];
+          __builtin_amdgcn_sched_barrier(0);
+        }
       }
 #pragma unroll
       for (int qb = 0; qb < 2; ++qb) {
@@ -238,7 +284,7 @@ __global__ __launch_bounds__(64 * kWaves, 1) void k_mol_fused(
         if constexpr (DENSE) {
           if (g == 0 && item_ok && b < pr.B) phi_out[b * phi_stride + (item - n_begin)] = phi[qb];
         } else {
-          top[qb].offer_score(phi[qb], item, g == 0 && item_ok, lane);
+          top[qb].offer_score(phi[qb], item, g == 0 && offer[qb], lane);
         }
       }
     }
@@ -265,12 +311,17 @@ __global__ __launch_bounds__(64 * kWaves, 1) void k_mol_fused(
 }
 
 // ---------------------------------------------------------------------------
-bool fused_supported(const DevProb& pr, int k) {
+static bool fused_shape(const DevProb& pr, bool mlp) {
   if (pr.dtype != MOL_BF16 || pr.Pq != 8) return false;
-  if (!((pr.Px == 4 && pr.d == 128 && pr.H == 128) || (pr.Px == 4 && pr.d == 64 && pr.H == 64) ||
-        (pr.Px == 8 && pr.d == 64 && pr.H == 64)))
-    return false;
-  return k <= WaveTopk::kList;
+  if (pr.Px == 8 && pr.d == 64) return !mlp || pr.H == 64;
+  if (pr.Px == 4 && pr.d == 64) return !mlp || pr.H == 64;
+  if (pr.Px == 4 && pr.d == 128) return !mlp || pr.H == 128;
+  return false;
+}
+
+bool fused_supported(const DevProb& pr, int k) { return fused_shape(pr, true) && k <= WaveTopk::kList; }
+bool fused_maxdot_supported(const DevProb& pr, int k) {
+  return fused_shape(pr, false) && k <= WaveTopk::kList;
 }
 
 void fused_grid(const DevProb& pr, int n_count, int& R, int& range_len, int& G) {
@@ -283,42 +334,53 @@ void fused_grid(const DevProb& pr, int n_count, int& R, int& range_len, int& G) 
   R = (n_count + range_len - 1) / range_len;
 }
 
-template <int PX, int D, int H, bool DENSE>
+template <int PX, int D, int H, int EPI>
 static hipError_t launch_fused_t(const DevProb& pr, int k, int R, int range_len, int G, int n_begin,
-                                 int n_end, uint64_t* partial, float* phi, long phi_stride,
-                                 hipStream_t st) {
-  using S = FusedShape<PX, D, H>;
-  auto kern = &k_mol_fused<PX, D, H, DENSE>;
+                                 int n_end, const float* bound, uint64_t* partial, float* phi,
+                                 long phi_stride, hipStream_t st) {
+  using S = FusedShape<PX, D, H, EPI != kEpiMaxDot>;
+  auto kern = &k_mol_fused<PX, D, H, EPI>;
   hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                      hipFuncAttributeMaxDynamicSharedMemorySize, S::LDS_TOTAL);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(kern, dim3(R * G), dim3(64 * kWaves), S::LDS_TOTAL, st, pr, k, R, range_len,
-                     G, n_begin, n_end, partial, phi, phi_stride);
+                     G, n_begin, n_end, bound, partial, phi, phi_stride);
   return hipGetLastError();
 }
 
-template <bool DENSE>
+template <int EPI>
 static hipError_t launch_fused_d(const DevProb& pr, int k, int R, int range_len, int G, int n_begin,
-                                 int n_end, uint64_t* partial, float* phi, long phi_stride,
-                                 hipStream_t st) {
+                                 int n_end, const float* bound, uint64_t* partial, float* phi,
+                                 long phi_stride, hipStream_t st) {
+  // the max-dot epilogue has no gating MLP: one instantiation per (Px, d)
   if (pr.Px == 8)
-    return launch_fused_t<8, 64, 64, DENSE>(pr, k, R, range_len, G, n_begin, n_end, partial, phi, phi_stride, st);
+    return launch_fused_t<8, 64, 64, EPI>(pr, k, R, range_len, G, n_begin, n_end, bound, partial, phi,
+                                          phi_stride, st);
   if (pr.d == 128)
-    return launch_fused_t<4, 128, 128, DENSE>(pr, k, R, range_len, G, n_begin, n_end, partial, phi, phi_stride, st);
-  return launch_fused_t<4, 64, 64, DENSE>(pr, k, R, range_len, G, n_begin, n_end, partial, phi, phi_stride, st);
+    return launch_fused_t<4, 128, 128, EPI>(pr, k, R, range_len, G, n_begin, n_end, bound, partial, phi,
+                                            phi_stride, st);
+  return launch_fused_t<4, 64, 64, EPI>(pr, k, R, range_len, G, n_begin, n_end, bound, partial, phi,
+                                        phi_stride, st);
 }
 
 hipError_t launch_fused_topk(const DevProb& pr, int k, int R, int range_len, int G,
-                             uint64_t* partial, hipStream_t st) {
-  return launch_fused_d<false>(pr, k, R, range_len, G, 0, pr.N, partial, nullptr, 0, st);
+                             const float* bound, uint64_t* partial, hipStream_t st) {
+  if (bound)
+    return launch_fused_d<kEpiBounded>(pr, k, R, range_len, G, 0, pr.N, bound, partial, nullptr, 0, st);
+  return launch_fused_d<kEpiTopk>(pr, k, R, range_len, G, 0, pr.N, nullptr, partial, nullptr, 0, st);
+}
+
+hipError_t launch_fused_maxdot(const DevProb& pr, int k, int R, int range_len, int G,
+                               uint64_t* partial, hipStream_t st) {
+  return launch_fused_d<kEpiMaxDot>(pr, k, R, range_len, G, 0, pr.N, nullptr, partial, nullptr, 0, st);
 }
 
 hipError_t launch_fused_dense(const DevProb& pr, int n_begin, int n_count, float* phi,
                               hipStream_t st) {
   int R, range_len, G;
   fused_grid(pr, n_count, R, range_len, G);
-  return launch_fused_d<true>(pr, 1, R, range_len, G, n_begin, n_begin + n_count, nullptr, phi,
-                              n_count, st);
+  return launch_fused_d<kEpiDense>(pr, 1, R, range_len, G, n_begin, n_begin + n_count, nullptr, nullptr,
+                                   phi, n_count, st);
 }
 
 }  // namespace mol

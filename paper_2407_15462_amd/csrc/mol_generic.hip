@@ -68,13 +68,20 @@ __device__ __forceinline__ float pair_phi(const DevProb& pr, long n, const float
 
 // Grid: x over items (256 per block), y over queries.  Items are either the
 // contiguous range n_begin .. n_begin+n_count-1 or, when `items` is given,
-// items[b*item_stride + i] for i < item_count[b].  Writes phi (float32) and/or
-// sort keys; key slots past a query's item count are cleared to 0 (empty).
+// items[b*item_stride + i] for i < item_count[b].  Writes a score (float32)
+// and/or sort keys; key slots past a query's item count are cleared to 0
+// (empty).  The score is, by `mode`:
+//   kGenPhi      phi;
+//   kGenBounded  phi, for items whose m = max_p s_p plus the rounding
+//                margin reaches bound[b] (phi <= m: Algorithm 1's range
+//                condition); other items get an empty key;
+//   kGenMaxDot   m itself (no gating MLP);
+//   kGenNegPhi   -phi (the smallest phi as the top-1 of the negated keys).
 template <typename T, int PMAX>
 __global__ __launch_bounds__(256) void k_phi_generic(
-    DevProb pr, int n_begin, int n_count, const int32_t* __restrict__ items,
-    const int32_t* __restrict__ item_count, long item_stride, float* __restrict__ phi,
-    long phi_stride, uint64_t* __restrict__ keys, long key_stride) {
+    DevProb pr, int mode, const float* __restrict__ bound, int n_begin, int n_count,
+    const int32_t* __restrict__ items, const int32_t* __restrict__ item_count, long item_stride,
+    float* __restrict__ phi, long phi_stride, uint64_t* __restrict__ keys, long key_stride) {
   extern __shared__ float smem[];
   const int P = pr.P, H = pr.H;
   float* sW1 = smem;
@@ -82,12 +89,14 @@ __global__ __launch_bounds__(256) void k_phi_generic(
   float* sb1 = sW2 + P * H;
   float* sc = sb1 + H;
   const int b = blockIdx.y;
-  for (int i = threadIdx.x; i < H * P; i += blockDim.x) {
-    sW1[i] = to_f32(static_cast<const T*>(pr.W1)[i]);
-    sW2[i] = to_f32(static_cast<const T*>(pr.W2)[i]);
+  if (mode != kGenMaxDot) {
+    for (int i = threadIdx.x; i < H * P; i += blockDim.x) {
+      sW1[i] = to_f32(static_cast<const T*>(pr.W1)[i]);
+      sW2[i] = to_f32(static_cast<const T*>(pr.W2)[i]);
+    }
+    for (int i = threadIdx.x; i < H; i += blockDim.x) sb1[i] = pr.b1[i];
+    for (int i = threadIdx.x; i < P; i += blockDim.x) sc[i] = pr.a_q[static_cast<long>(b) * P + i] + pr.b2[i];
   }
-  for (int i = threadIdx.x; i < H; i += blockDim.x) sb1[i] = pr.b1[i];
-  for (int i = threadIdx.x; i < P; i += blockDim.x) sc[i] = pr.a_q[static_cast<long>(b) * P + i] + pr.b2[i];
   __syncthreads();
 
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
@@ -100,7 +109,28 @@ __global__ __launch_bounds__(256) void k_phi_generic(
   const long n = items ? static_cast<long>(items[b * item_stride + i]) : static_cast<long>(n_begin) + i;
   float s[PMAX];
   pair_dots<T, PMAX>(pr, b, n, s);
-  const float v = pair_phi<PMAX>(pr, n, s, sW1, sW2, sb1, sc);
+  float v;
+  if (mode == kGenBounded || mode == kGenMaxDot) {
+    float m = s[0], mabs = fabsf(s[0]);
+#pragma unroll
+    for (int p = 1; p < PMAX; ++p)
+      if (p < P) {
+        m = fmaxf(m, s[p]);
+        mabs = fmaxf(mabs, fabsf(s[p]));
+      }
+    if (mode == kGenMaxDot) {
+      v = m;
+    } else if (m + 0x1p-12f * (1.f + mabs) < bound[b]) {   // phi <= m: cannot reach the bound
+      if (phi) phi[b * phi_stride + i] = -__builtin_inff();
+      if (keys) keys[b * key_stride + i] = 0;
+      return;
+    } else {
+      v = pair_phi<PMAX>(pr, n, s, sW1, sW2, sb1, sc);
+    }
+  } else {
+    v = pair_phi<PMAX>(pr, n, s, sW1, sW2, sb1, sc);
+    if (mode == kGenNegPhi) v = -v;
+  }
   if (phi) phi[b * phi_stride + i] = v;
   if (keys) keys[b * key_stride + i] = make_key(v, static_cast<int32_t>(n));
 }
@@ -239,6 +269,21 @@ __global__ void k_gap_bound(int B, int P, int m, const float* __restrict__ dots,
   if (out_looser) out_looser[b] = Sk - SK;
 }
 
+// bound[b] = sign * scores[b][col] (Algorithm 1's threshold from the rerank
+// output over G).
+__global__ void k_pick_bound(const float* __restrict__ scores, int stride, int col, float sign, int B,
+                             float* __restrict__ bound) {
+  const int b = blockIdx.x * blockDim.x + threadIdx.x;
+  if (b < B) bound[b] = sign * scores[static_cast<long>(b) * stride + col];
+}
+
+hipError_t launch_pick_bound(const float* scores, int stride, int col, float sign, int B, float* bound,
+                             hipStream_t st) {
+  hipLaunchKernelGGL(k_pick_bound, dim3((B + 255) / 256), dim3(256), 0, st, scores, stride, col, sign, B,
+                     bound);
+  return hipGetLastError();
+}
+
 hipError_t launch_gap_bound(int B, int P, int m, const float* dots, int k, const float* scores,
                             float* out_S, float* out_SK, float* out_bound, float* out_looser,
                             hipStream_t st) {
@@ -273,10 +318,11 @@ static size_t phi_smem_bytes(const DevProb& pr) {
 }
 
 template <typename T, int PMAX>
-static hipError_t launch_phi_t(const DevProb& pr, int n_begin, int n_count, const int32_t* items,
-                               const int32_t* item_count, long item_stride, float* phi,
-                               long phi_stride, uint64_t* keys, long key_stride, hipStream_t st) {
-  const size_t smem = phi_smem_bytes(pr);
+static hipError_t launch_phi_t(const DevProb& pr, int mode, const float* bound, int n_begin, int n_count,
+                               const int32_t* items, const int32_t* item_count, long item_stride,
+                               float* phi, long phi_stride, uint64_t* keys, long key_stride,
+                               hipStream_t st) {
+  const size_t smem = mode == kGenMaxDot ? 0 : phi_smem_bytes(pr);
   if (smem > 65536) {
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_phi_generic<T, PMAX>),
                                        hipFuncAttributeMaxDynamicSharedMemorySize,
@@ -284,29 +330,36 @@ static hipError_t launch_phi_t(const DevProb& pr, int n_begin, int n_count, cons
     if (e != hipSuccess) return e;
   }
   dim3 grid((n_count + 255) / 256, pr.B);
-  hipLaunchKernelGGL((k_phi_generic<T, PMAX>), grid, dim3(256), smem, st, pr, n_begin, n_count,
-                     items, item_count, item_stride, phi, phi_stride, keys, key_stride);
+  hipLaunchKernelGGL((k_phi_generic<T, PMAX>), grid, dim3(256), smem, st, pr, mode, bound, n_begin,
+                     n_count, items, item_count, item_stride, phi, phi_stride, keys, key_stride);
   return hipGetLastError();
 }
 
 template <typename T>
-static hipError_t launch_phi_p(const DevProb& pr, int n_begin, int n_count, const int32_t* items,
-                               const int32_t* item_count, long item_stride, float* phi,
-                               long phi_stride, uint64_t* keys, long key_stride, hipStream_t st) {
+static hipError_t launch_phi_p(const DevProb& pr, int mode, const float* bound, int n_begin, int n_count,
+                               const int32_t* items, const int32_t* item_count, long item_stride,
+                               float* phi, long phi_stride, uint64_t* keys, long key_stride,
+                               hipStream_t st) {
   if (pr.P <= 4)
-    return launch_phi_t<T, 4>(pr, n_begin, n_count, items, item_count, item_stride, phi, phi_stride, keys, key_stride, st);
+    return launch_phi_t<T, 4>(pr, mode, bound, n_begin, n_count, items, item_count, item_stride, phi,
+                              phi_stride, keys, key_stride, st);
   if (pr.P <= 16)
-    return launch_phi_t<T, 16>(pr, n_begin, n_count, items, item_count, item_stride, phi, phi_stride, keys, key_stride, st);
-  return launch_phi_t<T, 64>(pr, n_begin, n_count, items, item_count, item_stride, phi, phi_stride, keys, key_stride, st);
+    return launch_phi_t<T, 16>(pr, mode, bound, n_begin, n_count, items, item_count, item_stride, phi,
+                               phi_stride, keys, key_stride, st);
+  return launch_phi_t<T, 64>(pr, mode, bound, n_begin, n_count, items, item_count, item_stride, phi,
+                             phi_stride, keys, key_stride, st);
 }
 
-hipError_t launch_phi_generic(const DevProb& pr, int n_begin, int n_count, const int32_t* items,
-                              const int32_t* item_count, long item_stride, float* phi,
-                              long phi_stride, uint64_t* keys, long key_stride, hipStream_t st) {
+hipError_t launch_phi_generic(const DevProb& pr, int mode, const float* bound, int n_begin, int n_count,
+                              const int32_t* items, const int32_t* item_count, long item_stride,
+                              float* phi, long phi_stride, uint64_t* keys, long key_stride,
+                              hipStream_t st) {
   if (n_count <= 0) return hipSuccess;
   if (pr.dtype == MOL_BF16)
-    return launch_phi_p<bf16_t>(pr, n_begin, n_count, items, item_count, item_stride, phi, phi_stride, keys, key_stride, st);
-  return launch_phi_p<float>(pr, n_begin, n_count, items, item_count, item_stride, phi, phi_stride, keys, key_stride, st);
+    return launch_phi_p<bf16_t>(pr, mode, bound, n_begin, n_count, items, item_count, item_stride, phi,
+                                phi_stride, keys, key_stride, st);
+  return launch_phi_p<float>(pr, mode, bound, n_begin, n_count, items, item_count, item_stride, phi,
+                             phi_stride, keys, key_stride, st);
 }
 
 template <typename T>

@@ -6,9 +6,13 @@
 namespace mol {
 
 // Generic (one thread per pair, float32 arithmetic) kernels.
-hipError_t launch_phi_generic(const DevProb& pr, int n_begin, int n_count, const int32_t* items,
-                              const int32_t* item_count, long item_stride, float* phi,
-                              long phi_stride, uint64_t* keys, long key_stride, hipStream_t st);
+// Score of the pair-wise kernel: phi; phi restricted to items whose
+// max_p s_p can reach bound[b]; max_p s_p; -phi.
+enum GenMode { kGenPhi = 0, kGenBounded = 1, kGenMaxDot = 2, kGenNegPhi = 3 };
+hipError_t launch_phi_generic(const DevProb& pr, int mode, const float* bound, int n_begin, int n_count,
+                              const int32_t* items, const int32_t* item_count, long item_stride,
+                              float* phi, long phi_stride, uint64_t* keys, long key_stride,
+                              hipStream_t st);
 hipError_t launch_dots_generic(const DevProb& pr, int n_begin, int n_count, uint64_t* keys,
                                long key_stride, hipStream_t st);
 
@@ -30,6 +34,8 @@ hipError_t launch_gap_bound(int B, int P, int m, const float* dots, int k, const
                             float* out_S, float* out_SK, float* out_bound, float* out_looser,
                             hipStream_t st);
 hipError_t launch_avg_embed(const DevProb& pr, void* q_avg, void* x_avg, hipStream_t st);
+hipError_t launch_pick_bound(const float* scores, int stride, int col, float sign, int B, float* bound,
+                             hipStream_t st);
 
 }  // namespace mol
 
@@ -37,9 +43,15 @@ namespace mol {
 
 // Fused MFMA scoring (bf16, Pq = 8; (Px, d, H) in {(8,64,64), (4,64,64), (4,128,128)}).
 bool fused_supported(const DevProb& pr, int k);
+// max-component-dot epilogue: the same shapes with H ignored
+bool fused_maxdot_supported(const DevProb& pr, int k);
 void fused_grid(const DevProb& pr, int n_count, int& R, int& range_len, int& G);
+// bound: NULL, or [B] floats: only items with max_p s_p (plus the rounding
+// margin) at or above bound[b] are ranked for query b
 hipError_t launch_fused_topk(const DevProb& pr, int k, int R, int range_len, int G,
-                             uint64_t* partial, hipStream_t st);
+                             const float* bound, uint64_t* partial, hipStream_t st);
+hipError_t launch_fused_maxdot(const DevProb& pr, int k, int R, int range_len, int G,
+                               uint64_t* partial, hipStream_t st);
 hipError_t launch_fused_dense(const DevProb& pr, int n_begin, int n_count, float* phi,
                               hipStream_t st);
 
@@ -73,7 +85,8 @@ namespace mol {
 // Fused MFMA rerank of deduplicated candidates (same shapes as the fused scorer).
 bool rerank_supported(const DevProb& pr, int k);
 int rerank_chunk(int C);
+// negate: rank by -phi (the smallest scores first)
 hipError_t launch_rerank(const DevProb& pr, const int32_t* uniq, const int32_t* n_unique, int C, int k,
-                         uint64_t* partial, hipStream_t st);
+                         bool negate, uint64_t* partial, hipStream_t st);
 
 }  // namespace mol

@@ -21,7 +21,7 @@ constexpr int kWaves = 4;
 constexpr int kTopkRegion = WaveTopk::kList + WaveTopk::kStage;
 }  // namespace
 
-template <int PX, int D, int H>
+template <int PX, int D, int H, bool NEG>
 __global__ __launch_bounds__(64 * kWaves, 2) void k_mol_rerank(
     DevProb pr, const int32_t* __restrict__ uniq, const int32_t* __restrict__ n_unique, int C,
     int k, int chunk, int nchunks, uint64_t* __restrict__ partial) {
@@ -96,7 +96,7 @@ __global__ __launch_bounds__(64 * kWaves, 2) void k_mol_rerank(
     }
     float phi[1];
     mlp.template phi<1>(s, c0, phi);
-    top.offer_score(phi[0], item, g == 0 && ok, lane);
+    top.offer_score(NEG ? -phi[0] : phi[0], item, g == 0 && ok, lane);
   }
   top.flush(lane);
   uint64_t* dst = partial + (static_cast<long>(b) * nchunks + j) * k;
@@ -108,21 +108,30 @@ bool rerank_supported(const DevProb& pr, int k) { return fused_supported(pr, k);
 
 int rerank_chunk(int C) { return C <= 1024 ? 256 : 1024; }
 
+template <bool NEG>
+static void launch_rerank_t(const DevProb& pr, dim3 grid, const int32_t* uniq, const int32_t* n_unique,
+                            int C, int k, int chunk, int nchunks, uint64_t* partial, hipStream_t st) {
+  if (pr.Px == 8)
+    hipLaunchKernelGGL((k_mol_rerank<8, 64, 64, NEG>), grid, dim3(64 * kWaves), 0, st, pr, uniq, n_unique, C,
+                       k, chunk, nchunks, partial);
+  else if (pr.d == 128)
+    hipLaunchKernelGGL((k_mol_rerank<4, 128, 128, NEG>), grid, dim3(64 * kWaves), 0, st, pr, uniq, n_unique,
+                       C, k, chunk, nchunks, partial);
+  else
+    hipLaunchKernelGGL((k_mol_rerank<4, 64, 64, NEG>), grid, dim3(64 * kWaves), 0, st, pr, uniq, n_unique, C,
+                       k, chunk, nchunks, partial);
+}
+
 hipError_t launch_rerank(const DevProb& pr, const int32_t* uniq, const int32_t* n_unique, int C, int k,
-                         uint64_t* partial, hipStream_t st) {
+                         bool negate, uint64_t* partial, hipStream_t st) {
   const int chunk = rerank_chunk(C);
   const int nchunks = (C + chunk - 1) / chunk;
   const long waves = static_cast<long>(pr.B) * nchunks;
   const dim3 grid(static_cast<unsigned>((waves + kWaves - 1) / kWaves));
-  if (pr.Px == 8)
-    hipLaunchKernelGGL((k_mol_rerank<8, 64, 64>), grid, dim3(64 * kWaves), 0, st, pr, uniq, n_unique, C, k,
-                       chunk, nchunks, partial);
-  else if (pr.d == 128)
-    hipLaunchKernelGGL((k_mol_rerank<4, 128, 128>), grid, dim3(64 * kWaves), 0, st, pr, uniq, n_unique, C,
-                       k, chunk, nchunks, partial);
+  if (negate)
+    launch_rerank_t<true>(pr, grid, uniq, n_unique, C, k, chunk, nchunks, partial, st);
   else
-    hipLaunchKernelGGL((k_mol_rerank<4, 64, 64>), grid, dim3(64 * kWaves), 0, st, pr, uniq, n_unique, C, k,
-                       chunk, nchunks, partial);
+    launch_rerank_t<false>(pr, grid, uniq, n_unique, C, k, chunk, nchunks, partial, st);
   return hipGetLastError();
 }
 

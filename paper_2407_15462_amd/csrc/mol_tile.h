@@ -82,6 +82,15 @@ __device__ __forceinline__ float max_groups(float x) {
   return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
 }
 
+// Margin of the bound phi <= max_p s_p under float32 rounding.  phi is
+// formed as sum_p w_p s_p / sum_p w_p with w_p >= 0: each of the two sums of
+// at most 64 terms is off by under 64 units of 2^-24 relative to
+// sum_p w_p |s_p| (resp. sum_p w_p), and the reciprocal and product add a
+// few more, so the computed phi exceeds max_p s_p by less than
+// 140 * 2^-24 * max_p |s_p|.  The margin is 2^-12 (1 + max_p |s_p|), more
+// than 100 times that.
+__device__ __forceinline__ float bound_margin(float mabs) { return 0x1p-12f * (1.f + mabs); }
+
 __device__ __forceinline__ int lane_base(int g, int PX) { return (4 * (g & 1) + 2 * (g >> 1)) * PX; }
 
 // s_waitcnt immediate that waits until at most n vector-memory operations
@@ -114,6 +123,21 @@ __device__ __forceinline__ void ring_barrier() {
   __builtin_amdgcn_s_waitcnt((VM & 0xF) | ((VM >> 4) << 14) | (0x7 << 4));   // lgkmcnt(0)
   __builtin_amdgcn_s_barrier();
   asm volatile("" ::: "memory");
+}
+
+// Wave priority around a chain of matrix instructions: while a wave issues
+// its MFMAs it wins the SIMD's issue arbitration over the other wave's
+// vector ALU stream, so the matrix pipe starts early and runs under that
+// stream instead of after it.  Only the issue order changes.
+__device__ __forceinline__ void mfma_priority_begin() {
+  __builtin_amdgcn_sched_barrier(0);
+  __builtin_amdgcn_s_setprio(1);
+  __builtin_amdgcn_sched_barrier(0);
+}
+__device__ __forceinline__ void mfma_priority_end() {
+  __builtin_amdgcn_sched_barrier(0);
+  __builtin_amdgcn_s_setprio(0);
+  __builtin_amdgcn_sched_barrier(0);
 }
 
 typedef __attribute__((address_space(3))) uint64_t lds_u64_t;
@@ -281,12 +305,14 @@ struct MolMlp {
       sop[m] = make_uint4(pack_f16(s[8 * m + 0], s[8 * m + 1]), pack_f16(s[8 * m + 2], s[8 * m + 3]),
                           pack_f16(s[8 * m + 4], s[8 * m + 5]), pack_f16(s[8 * m + 6], s[8 * m + 7]));
     f32x4_t u[JT];
+    mfma_priority_begin();
 #pragma unroll
     for (int jt = 0; jt < JT; ++jt) {
       u[jt] = b1acc[jt];
 #pragma unroll
       for (int m = 0; m < KP; ++m) u[jt] = mfma_f16(w1op[jt][m], sop[m], u[jt]);
     }
+    mfma_priority_end();
     uint4 hop[KH];
 #pragma unroll
     for (int m = 0; m < KH; ++m) {
@@ -299,26 +325,33 @@ struct MolMlp {
       hop[m] = make_uint4(pack_f16(hv[0], hv[1]), pack_f16(hv[2], hv[3]), pack_f16(hv[4], hv[5]),
                           pack_f16(hv[6], hv[7]));
     }
+    mfma_priority_begin();
 #pragma unroll
     for (int pt = 0; pt < PT; ++pt) {
       lg[pt] = c0[pt];
 #pragma unroll
       for (int m = 0; m < KH; ++m) lg[pt] = mfma_f16(w2op[pt][m], hop[m], lg[pt]);
     }
+    mfma_priority_end();
   }
 
   // sum_p w_p and sum_p w_p s_p over the lane's p (w = 2^(l' - shift)),
   // two partial sums each to shorten the dependency chains
   __device__ static void weights(const f32x4_t (&lg)[PT], const float (&s)[RUN], float shift, float& den,
                                  float& num) {
-    float d[2] = {0.f, 0.f}, n[2] = {0.f, 0.f};
+    float d[2], n[2];
 #pragma unroll
     for (int pt = 0; pt < PT; ++pt)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const float w = __builtin_amdgcn_exp2f(lg[pt][i] - shift);
-        d[i & 1] += w;
-        n[i & 1] = fmaf(w, s[4 * pt + i], n[i & 1]);
+        if (pt == 0 && i < 2) {   // first term of each partial sum
+          d[i] = w;
+          n[i] = w * s[i];
+        } else {
+          d[i & 1] += w;
+          n[i & 1] = fmaf(w, s[4 * pt + i], n[i & 1]);
+        }
       }
     den = d[0] + d[1];
     num = n[0] + n[1];

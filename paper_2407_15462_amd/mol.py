@@ -18,9 +18,12 @@ LIB_PATH = os.path.join(_HERE, "libmol.so")
 
 MOL_OK, MOL_EINVAL, MOL_EUNSUPPORTED, MOL_EWORKSPACE, MOL_EHIP = range(5)
 MOL_F32, MOL_BF16 = 0, 1
-MOL_OP_SCORE, MOL_OP_TOPK_EXACT, MOL_OP_TOPK_PER_EMBD, MOL_OP_RERANK = range(4)
+(MOL_OP_SCORE, MOL_OP_TOPK_EXACT, MOL_OP_TOPK_PER_EMBD, MOL_OP_RERANK, MOL_OP_TOPK_MAXDOT,
+ MOL_OP_TOPK_BOUNDED, MOL_OP_TOPK_TWO_PASS) = range(7)
+MOL_TWO_PASS_MIN, MOL_TWO_PASS_KTH = 0, 1
 
-EXPORTS = ("mol_workspace_size", "mol_score", "mol_topk_exact", "mol_topk_per_embd",
+EXPORTS = ("mol_workspace_size", "mol_score", "mol_topk_exact", "mol_topk_exact_bounded",
+           "mol_topk_two_pass", "mol_topk_maxdot", "mol_topk_per_embd",
            "mol_rerank", "mol_avg_embed", "mol_gap_bound", "mol_timing_enable", "mol_timing_read",
            "mol_status_str", "mol_last_error")
 
@@ -61,6 +64,9 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "mol_workspace_size": [P, ctypes.c_int, i32, i32, i32, ctypes.POINTER(sz)],
         "mol_score": [P, i32, i32, vp, vp],
         "mol_topk_exact": [P, i32, vp, vp, vp, sz, vp],
+        "mol_topk_exact_bounded": [P, i32, vp, vp, vp, vp, sz, vp],
+        "mol_topk_two_pass": [P, i32, i32, vp, vp, vp, vp, sz, vp],
+        "mol_topk_maxdot": [P, i32, vp, vp, vp, sz, vp],
         "mol_topk_per_embd": [P, i32, vp, vp, vp, sz, vp],
         "mol_rerank": [P, vp, i32, vp, i32, i32, vp, vp, vp, vp, sz, vp],
         "mol_avg_embed": [P, vp, vp, vp],
@@ -152,6 +158,24 @@ def mol_topk_exact(prob: Problem, k: int, out_score, out_idx, ws, stream=None) -
                                  ws.numel() if ws is not None else 0, _stream(stream)))
 
 
+def mol_topk_exact_bounded(prob: Problem, k: int, bound, out_score, out_idx, ws, stream=None) -> None:
+    _check(load().mol_topk_exact_bounded(prob.ref, k, _ptr(bound), _ptr(out_score), _ptr(out_idx),
+                                         _ptr(ws), ws.numel() if ws is not None else 0,
+                                         _stream(stream)))
+
+
+def mol_topk_two_pass(prob: Problem, k: int, mode: int, out_score, out_idx, out_bound, ws,
+                      stream=None) -> None:
+    _check(load().mol_topk_two_pass(prob.ref, k, mode, _ptr(out_score), _ptr(out_idx),
+                                    _ptr(out_bound), _ptr(ws), ws.numel() if ws is not None else 0,
+                                    _stream(stream)))
+
+
+def mol_topk_maxdot(prob: Problem, k: int, out_score, out_idx, ws, stream=None) -> None:
+    _check(load().mol_topk_maxdot(prob.ref, k, _ptr(out_score), _ptr(out_idx), _ptr(ws),
+                                  ws.numel() if ws is not None else 0, _stream(stream)))
+
+
 def mol_topk_per_embd(prob: Problem, kprime: int, out_dot, out_idx, ws, stream=None) -> None:
     _check(load().mol_topk_per_embd(prob.ref, kprime, _ptr(out_dot), _ptr(out_idx), _ptr(ws),
                                     ws.numel() if ws is not None else 0, _stream(stream)))
@@ -205,6 +229,36 @@ def topk_exact(prob: Problem, k: int, ws=None, stream=None) -> Tuple[torch.Tenso
     s = torch.empty((prob.B, k), dtype=torch.float32, device=prob.device)
     i = torch.empty((prob.B, k), dtype=torch.int32, device=prob.device)
     mol_topk_exact(prob, k, s, i, ws, stream)
+    return s, i
+
+
+def _topk_out(prob: Problem, k: int):
+    return (torch.empty((prob.B, k), dtype=torch.float32, device=prob.device),
+            torch.empty((prob.B, k), dtype=torch.int32, device=prob.device))
+
+
+def topk_exact_bounded(prob: Problem, k: int, bound: torch.Tensor, ws=None, stream=None):
+    """Exact top-k among items whose max component dot can reach bound[b]."""
+    ws = workspace(prob, MOL_OP_TOPK_BOUNDED, k=k) if ws is None else ws
+    s, i = _topk_out(prob, k)
+    mol_topk_exact_bounded(prob, k, bound, s, i, ws, stream)
+    return s, i
+
+
+def topk_two_pass(prob: Problem, k: int, mode: int = MOL_TWO_PASS_MIN, ws=None, stream=None):
+    """Algorithm 1: (scores, ids, bound used per query)."""
+    ws = workspace(prob, MOL_OP_TOPK_TWO_PASS, k=k) if ws is None else ws
+    s, i = _topk_out(prob, k)
+    bound = torch.empty((prob.B,), dtype=torch.float32, device=prob.device)
+    mol_topk_two_pass(prob, k, mode, s, i, bound, ws, stream)
+    return s, i, bound
+
+
+def topk_maxdot(prob: Problem, k: int, ws=None, stream=None):
+    """Top-k by max_p s_p: (max dots, ids)."""
+    ws = workspace(prob, MOL_OP_TOPK_MAXDOT, k=k) if ws is None else ws
+    s, i = _topk_out(prob, k)
+    mol_topk_maxdot(prob, k, s, i, ws, stream)
     return s, i
 
 

@@ -59,6 +59,7 @@ class Workload:
     q_noise: float = 0.0
     kprime: int = 0       # per-component top-k' (approximate path)
     k_avg: int = 0        # averaged-embedding top-k (approximate path)
+    gating_std: float = 0.1   # standard deviation of a_q, a_x, W1, b1, W2, b2
     note: str = ""
 
     @property
@@ -91,6 +92,11 @@ WORKLOADS: Dict[str, Workload] = {
                  dtype="bf16", k=100, items="mixture", clusters=4096,
                  q_noise=0.2, kprime=128,
                  note="TopKPerEmbd(128) over all 64 components, then rerank"),
+        Workload("exact_1m_skewed", B=1024, N=1 << 20, Pq=8, Px=8, d=64, H=64,
+                 dtype="bf16", k=100, items="mixture", clusters=4096,
+                 q_noise=0.2, kprime=128, gating_std=1.0,
+                 note="the 1M-item data with gating parameters of standard "
+                      "deviation 1: the largest gating weight is about 0.2"),
         Workload("hybrid_8m", B=256, N=1 << 23, Pq=8, Px=4, d=128, H=128,
                  dtype="bf16", k=100, items="mixture", clusters=16384,
                  q_noise=0.2, kprime=256, k_avg=1024,
@@ -99,7 +105,7 @@ WORKLOADS: Dict[str, Workload] = {
 }
 
 # The 1M-item approximate workload reuses the exact one's data.
-_DATA_ALIAS = {"approx_1m": "exact_1m"}
+_DATA_ALIAS = {"approx_1m": "exact_1m", "exact_1m_skewed": "exact_1m"}
 
 
 @dataclasses.dataclass
@@ -155,7 +161,7 @@ def generate(spec: Workload, seed: int = 0, device: str = "cpu") -> MolInputs:
                                 generator=_generator(device, *key, "cluster", c0))
             z = centres[cid] + 0.3 * z
         X[:, c0:c0 + n, :] = _unit(z).to(store).permute(1, 0, 2)
-        a_x[c0:c0 + n] = 0.1 * randn((n, P), "a_x", c0)
+        a_x[c0:c0 + n] = spec.gating_std * randn((n, P), "a_x", c0)
 
     if spec.items == "mixture":
         src = torch.randint(0, N, (B,), device=device,
@@ -165,14 +171,15 @@ def generate(spec: Workload, seed: int = 0, device: str = "cpu") -> MolInputs:
     else:
         Q = _unit(randn((B, Pq, d), "queries")).to(store)
 
+    sd = spec.gating_std
     return MolInputs(
         spec=spec, Q=Q.contiguous(), X=X,
-        a_q=(0.1 * randn((B, P), "a_q")).contiguous(),
+        a_q=(sd * randn((B, P), "a_q")).contiguous(),
         a_x=a_x,
-        W1=(0.1 * randn((H, P), "W1")).to(store).contiguous(),
-        b1=(0.1 * randn((H,), "b1")).contiguous(),
-        W2=(0.1 * randn((P, H), "W2")).to(store).contiguous(),
-        b2=(0.1 * randn((P,), "b2")).contiguous(),
+        W1=(sd * randn((H, P), "W1")).to(store).contiguous(),
+        b1=(sd * randn((H,), "b1")).contiguous(),
+        W2=(sd * randn((P, H), "W2")).to(store).contiguous(),
+        b2=(sd * randn((P,), "b2")).contiguous(),
     )
 
 

@@ -112,7 +112,7 @@ def test_timing_records_are_empty_and_validated():
     assert lib.mol_timing_enable(0) == mol.MOL_OK
     assert lib.mol_timing_read(mol.MOL_OP_TOPK_EXACT, ctypes.byref(ms), ctypes.byref(n)) == mol.MOL_OK
     assert (ms.value, n.value) == (0.0, 0)
-    assert lib.mol_timing_read(4, ctypes.byref(ms), ctypes.byref(n)) == mol.MOL_EINVAL
+    assert lib.mol_timing_read(7, ctypes.byref(ms), ctypes.byref(n)) == mol.MOL_EINVAL
     assert lib.mol_timing_read(-1, ctypes.byref(ms), ctypes.byref(n)) == mol.MOL_EINVAL
     assert lib.mol_timing_read(0, None, ctypes.byref(n)) == mol.MOL_EINVAL
     # a call rejected before launch records nothing
@@ -133,3 +133,45 @@ def test_gap_bound_validation():
     assert lib.mol_gap_bound(4, 8, 1, p, 10, p, None, None, None, None, None) == mol.MOL_EINVAL
     assert lib.mol_gap_bound(4, 8, 5, p, 0, p, None, None, None, None, None) == mol.MOL_EINVAL
     assert lib.mol_gap_bound(4, 8, 5, None, 10, p, None, None, None, None, None) == mol.MOL_EINVAL
+
+
+def test_two_pass_bounded_and_maxdot_validation():
+    """Algorithm 1 / bounded / max-dot entry points reject bad arguments
+    before launching anything."""
+    lib = mol.load()
+    c = _problem(N=100000)
+    ws = ctypes.c_void_p(256)
+    big = 1 << 40
+    # workspace sizes exist for the new operations
+    for op, k in ((mol.MOL_OP_TOPK_MAXDOT, 10), (mol.MOL_OP_TOPK_BOUNDED, 10),
+                  (mol.MOL_OP_TOPK_TWO_PASS, 10)):
+        rc, n = _ws(c, op, k=k)
+        assert rc == mol.MOL_OK and n > 0, op
+    # the two-pass algorithm reranks P k candidates: at most 16384
+    wide = _problem(N=100000, Pq=8, Px=8)
+    assert _ws(wide, mol.MOL_OP_TOPK_TWO_PASS, k=256)[0] == mol.MOL_OK
+    assert _ws(wide, mol.MOL_OP_TOPK_TWO_PASS, k=257)[0] == mol.MOL_EINVAL
+    assert lib.mol_topk_two_pass(ctypes.byref(wide), 257, 0, 256, 256, None, ws, big, None) \
+        == mol.MOL_EINVAL
+    assert lib.mol_topk_two_pass(ctypes.byref(c), 10, 2, 256, 256, None, ws, big, None) \
+        == mol.MOL_EINVAL
+    assert lib.mol_topk_two_pass(ctypes.byref(c), 10, mol.MOL_TWO_PASS_KTH, None, 256, None, ws,
+                                 big, None) == mol.MOL_EINVAL
+    assert lib.mol_topk_two_pass(ctypes.byref(c), 10, mol.MOL_TWO_PASS_MIN, 256, 256, None, ws, 16,
+                                 None) == mol.MOL_EWORKSPACE
+    assert lib.mol_topk_two_pass(ctypes.byref(_problem(a_q=None)), 10, 0, 256, 256, None, ws, big,
+                                 None) == mol.MOL_EINVAL
+    # bounded: the bound array is required; k within [1, min(N, 1024)]
+    assert lib.mol_topk_exact_bounded(ctypes.byref(c), 10, None, 256, 256, ws, big, None) \
+        == mol.MOL_EINVAL
+    assert lib.mol_topk_exact_bounded(ctypes.byref(c), 0, 256, 256, 256, ws, big, None) \
+        == mol.MOL_EINVAL
+    assert lib.mol_topk_exact_bounded(ctypes.byref(c), 10, 256, 256, 256, ws, 16, None) \
+        == mol.MOL_EWORKSPACE
+    # max-dot reads only Q and X: gating pointers may be NULL, H is ignored
+    bare = _problem(N=100000, a_q=None, a_x=None, W1=None, b1=None, W2=None, b2=None, H=0)
+    rc, n = _ws(bare, mol.MOL_OP_TOPK_MAXDOT, k=10)
+    assert rc == mol.MOL_OK and n > 0
+    assert lib.mol_topk_maxdot(ctypes.byref(bare), 10, 256, 256, ws, 16, None) == mol.MOL_EWORKSPACE
+    assert lib.mol_topk_maxdot(ctypes.byref(bare), 100001, 256, 256, ws, big, None) == mol.MOL_EINVAL
+    assert lib.mol_topk_maxdot(ctypes.byref(bare), 10, None, 256, ws, big, None) == mol.MOL_EINVAL

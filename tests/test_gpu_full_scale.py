@@ -43,6 +43,24 @@ def test_exact_top100_full_scale(full):
         check_topk_row(phi, i[b], s[b], spec.k, f"exact_1m query {b}")
 
 
+def test_two_pass_and_maxdot_full_scale(full):
+    """Algorithm 1 (k-th-score threshold) returns the brute-force rows bit for
+    bit for every query; the max-component top-k of sampled queries against
+    the oracle."""
+    spec, inp, prob, op = full
+    es, ei = mol.topk_exact(prob, spec.k)
+    s, i, bound = mol.topk_two_pass(prob, spec.k, mol.MOL_TWO_PASS_KTH)
+    ms, mi = mol.topk_maxdot(mol.Problem(inp.Q, inp.X), spec.k)
+    torch.cuda.synchronize()
+    assert torch.equal(i, ei) and torch.equal(s, es)
+    log(f"[full] two-pass bound {bound.min().item():.4f} .. {bound.max().item():.4f}")
+    ms, mi = ms.cpu().numpy(), mi.cpu().numpy()
+    for r, b in enumerate(SAMPLE):
+        log(f"[full] max-dot query {b}")
+        m = mo.all_dots(op, r).max(axis=1)
+        check_topk_row(m, mi[b], ms[b], spec.k, f"maxdot_1m query {b}")
+
+
 def test_per_embd_and_rerank_full_scale(full):
     spec, inp, prob, op = full
     kp = spec.kprime

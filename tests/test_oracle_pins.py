@@ -289,6 +289,71 @@ def test_two_pass_equals_brute_force_on_random_instances():
             assert np.array_equal(got_v, want_v[0])
 
 
+def test_two_pass_kth_threshold_is_exact_and_tighter():
+    """Algorithm 1 with the k-th largest MoL score over G as threshold: the
+    result is still the brute-force top-k, the threshold is at least S_min and
+    at most the corpus-wide k-th score, and its second-pass set is a subset
+    of the S_min one."""
+    rng = np.random.default_rng(21)
+    for seed in range(3):
+        prob = make_problem(rng, B=2, N=500, Pq=2, Px=3, d=8, H=8, scale=2.0)
+        for b in range(2):
+            phi = mo.mol_scores(prob, [b])[0]
+            want_v, want_i = mo.topk_desc(phi, 10)
+            t_min = mo.two_pass_threshold(prob, b, 10, "min")
+            t_kth = mo.two_pass_threshold(prob, b, 10, "kth")
+            assert t_min <= t_kth <= mo.kth_largest(phi, 10)
+            got_v, got_i = mo.exact_two_pass(prob, b, 10, "kth")
+            assert got_i.tolist() == want_i.tolist() and np.array_equal(got_v, want_v)
+            s = mo.all_dots(prob, b)
+            assert np.all((s >= t_kth).any(axis=1) <= (s >= t_min).any(axis=1))
+
+
+def test_bounded_topk_filters_by_max_component_dot():
+    """The second pass on its own, against a filter written out item by item
+    from exact rational dot products: only items with some s_p >= bound are
+    ranked; a bound at or below the k-th score gives the exact top-k, a bound
+    above every s_p gives an all-padding row."""
+    rng = np.random.default_rng(22)
+    prob = make_problem(rng, B=1, N=90, Pq=2, Px=2, d=4, H=4, scale=2.0)
+    phi = mo.mol_scores(prob, [0])[0]
+    m = [max(frac_dot(prob.Q[0, pq], prob.X[px, n]) for pq in range(2) for px in range(2))
+         for n in range(prob.N)]
+    kth = mo.kth_largest(phi, 6)
+    mid = float(sorted(m)[prob.N // 2])           # half the items qualify
+    for bound in (-math.inf, kth, mid, float(max(m)) + 1.0):
+        keep = [n for n in range(prob.N) if float(m[n]) >= bound]
+        order = sorted(keep, key=lambda n: (-phi[n], n))[:6]
+        v, i = mo.exact_topk_bounded(prob, 0, 6, bound)
+        assert i[:len(order)].tolist() == order
+        assert np.all(i[len(order):] == -1) and np.all(np.isneginf(v[len(order):]))
+        assert np.array_equal(v[:len(order)], phi[order])
+    # phi never exceeds the largest component dot (Eq. 1 is a convex combination)
+    assert np.all(phi <= np.array([float(x) for x in m]) + 1e-15)
+
+
+def test_max_dot_topk_against_rational_dots_and_per_component_lists():
+    """Max approximation: ranking by m = max_p s_p written out from exact
+    rational dot products; the top-k by m lies in the union of the
+    per-component top-k lists (an item outside list p is beaten in s_p by k
+    items, which then also beat it in m)."""
+    rng = np.random.default_rng(23)
+    prob = make_problem(rng, B=2, N=120, Pq=2, Px=3, d=4, H=4)
+    for b in range(2):
+        m = [max(frac_dot(prob.Q[b, pq], prob.X[px, n]) for pq in range(2) for px in range(3))
+             for n in range(prob.N)]
+        order = sorted(range(prob.N), key=lambda n: (-m[n], n))[:9]
+        v, i = mo.max_dot_topk(prob, b, 9)
+        assert i.tolist() == order
+        assert np.allclose(v, [float(m[n]) for n in order], rtol=0, atol=1e-15)
+        _, ids, _, _ = mo.topk_per_embedding(prob, b, 9)
+        assert set(i.tolist()) <= set(mo.union_dedup([ids]).tolist())
+    # with one component it is the dot-product top-k (Lemma 1's setting)
+    one = make_problem(rng, B=1, N=200, Pq=1, Px=1, d=8, H=4)
+    _, ids, _, _ = mo.topk_per_embedding(one, 0, 20)
+    assert mo.max_dot_topk(one, 0, 20)[1].tolist() == ids[0].tolist()
+
+
 def test_theorem2_non_candidates_score_at_most_S():
     rng = np.random.default_rng(11)
     prob = make_problem(rng, B=2, N=800, Pq=2, Px=4, d=8, H=8, scale=2.0)
