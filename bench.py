@@ -11,6 +11,13 @@ H = 128) the approximate path also runs TopKAvg (mol_avg_embed of the
 queries + mol_topk_per_embd top-1024 on the averaged embeddings, whose item
 side is precomputed outside the timed region) and reranks the union of both
 candidate sets.
+With --workload paper_ml20m / paper_books / paper_nq320k (the item counts,
+component counts and widths of the paper's top-K benchmark, 32 queries per
+call) it times each method row of the paper's table instead -- brute force,
+TopKPerEmbd(N), TopKAvg(N), CombTopK(N1, N2) -- plus the two-pass exact
+algorithm and the max-component heuristic: mean and standard deviation of the
+call latency over --steps warm runs (HIP events on the stream), and
+recall@100 against the brute-force result.
 Inputs are synthetic, seeded, and resident in HBM before timing starts.
 Prints one JSON line.
 """
@@ -116,6 +123,9 @@ def main():
     from paper_2407_15462_amd import mol
 
     spec = synth.WORKLOADS[args.workload]
+    if spec.name in synth.PAPER_METHODS:
+        paper_table(spec, args)
+        return
     paths = [p for p in args.paths.split(",") if p]
     dev = "cuda"
     t0 = time.time()
@@ -251,6 +261,128 @@ def main():
         nq = args.cpu_baseline_queries or max(1, (8 << 20) // spec.N)
         out["cpu_baseline"] = cpu_baseline(inp, spec, nq)
     print(json.dumps(out), flush=True)
+
+
+def paper_table(spec, args):
+    """Latency of every method row of the paper's top-K table on a synthetic
+    instance of one of its workload shapes (32 queries per call)."""
+    import statistics
+
+    import torch
+
+    import synth
+    from paper_2407_15462_amd import mol
+
+    dev = "cuda"
+    inp = synth.generate(spec, seed=args.seed, device=dev)
+    prob = mol.Problem.from_inputs(inp)
+    pe_prob = mol.Problem(inp.Q, inp.X)
+    B, N, P, d, k = spec.B, spec.N, spec.P, spec.d, spec.k
+    # item side of TopKAvg: materialised once, untimed (preprocessing)
+    x_avg = torch.empty((N, d), dtype=inp.Q.dtype, device=dev)
+    q_avg = torch.empty((B, d), dtype=inp.Q.dtype, device=dev)
+    mol.mol_avg_embed(pe_prob, None, x_avg)
+    avg_prob = mol.averaged_problem(pe_prob, q_avg, x_avg)
+
+    def out2(n):
+        return (torch.empty((B, n), dtype=torch.float32, device=dev),
+                torch.empty((B, n), dtype=torch.int32, device=dev))
+
+    ex_s, ex_i = out2(k)
+    ws_ex = mol.workspace(prob, mol.MOL_OP_TOPK_EXACT, k=k)
+    rr_s, rr_i = out2(k)
+    rr_n = torch.empty((B,), dtype=torch.int32, device=dev)
+
+    def method(row):
+        """(label, callable running the whole method) or (label, reason)"""
+        kind = row[0]
+        n1 = row[1] if kind in ("per_embd", "comb") else 0
+        n2 = row[1] if kind == "avg" else (row[2] if kind == "comb" else 0)
+        label = {"per_embd": f"TopKPerEmbd({n1})", "avg": f"TopKAvg({n2})",
+                 "comb": f"CombTopK{n1}_{n2}"}[kind]
+        try:
+            C = P * n1
+            if n1:
+                ws_pe = mol.workspace(pe_prob, mol.MOL_OP_TOPK_PER_EMBD, kprime=n1)
+                pe_d = torch.empty((B, P, n1), dtype=torch.float32, device=dev)
+                pe_i = torch.empty((B, P, n1), dtype=torch.int32, device=dev)
+            if n2:
+                ws_av = mol.workspace(avg_prob, mol.MOL_OP_TOPK_PER_EMBD, kprime=n2)
+                av_d = torch.empty((B, 1, n2), dtype=torch.float32, device=dev)
+                av_i = torch.empty((B, 1, n2), dtype=torch.int32, device=dev)
+            ws_rr = mol.workspace(prob, mol.MOL_OP_RERANK, k=k, C=C + n2)
+        except mol.MolError as e:
+            return label, str(e)
+
+        def run():
+            if n1:
+                mol.mol_topk_per_embd(pe_prob, n1, pe_d, pe_i, ws_pe)
+            if n2:
+                mol.mol_avg_embed(pe_prob, q_avg, None)
+                mol.mol_topk_per_embd(avg_prob, n2, av_d, av_i, ws_av)
+            first = pe_i.view(B, C) if n1 else av_i.view(B, n2)
+            second = av_i.view(B, n2) if (n1 and n2) else None
+            mol.mol_rerank(prob, first, C if n1 else n2, second, n2 if (n1 and n2) else 0, k,
+                           rr_s, rr_i, rr_n, ws_rr)
+        return label, run
+
+    rows = [("BruteForce", lambda: mol.mol_topk_exact(prob, k, ex_s, ex_i, ws_ex))]
+    for r in synth.PAPER_METHODS[spec.name]:
+        rows.append(method(r))
+    ws_tp = mol.workspace(prob, mol.MOL_OP_TOPK_TWO_PASS, k=k)
+    tp_s, tp_i = out2(k)
+    rows.append(("TwoPassExact(k-th bound)",
+                 lambda: mol.mol_topk_two_pass(prob, k, mol.MOL_TWO_PASS_KTH, tp_s, tp_i, None, ws_tp)))
+    mx_n = min(1024, 10 * k)
+    ws_mx = mol.workspace(pe_prob, mol.MOL_OP_TOPK_MAXDOT, k=mx_n)
+    ws_mr = mol.workspace(prob, mol.MOL_OP_RERANK, k=k, C=mx_n)
+    mx_s, mx_i = out2(mx_n)
+
+    def maxdot_rerank():
+        mol.mol_topk_maxdot(pe_prob, mx_n, mx_s, mx_i, ws_mx)
+        mol.mol_rerank(prob, mx_i, mx_n, None, 0, k, rr_s, rr_i, rr_n, ws_mr)
+    rows.append((f"MaxTopK({mx_n})", maxdot_rerank))
+
+    # brute force first: its result is the recall reference of every row
+    results = []
+    exact_ids = None
+    for label, fn in rows:
+        if not callable(fn):
+            results.append({"method": label, "supported": False, "reason": fn})
+            continue
+        for _ in range(args.warmup):
+            fn()
+        torch.cuda.synchronize()
+        times = []
+        for _ in range(args.steps):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            fn()
+            e1.record()
+            times.append((e0, e1))
+        torch.cuda.synchronize()
+        ms = [a.elapsed_time(b) for a, b in times]
+        got = (ex_i if label == "BruteForce" else tp_i if label.startswith("TwoPass") else rr_i).cpu()
+        if exact_ids is None:
+            exact_ids = got.clone()
+        hits = sum(len(set(a.tolist()) & set(b.tolist())) for a, b in zip(got, exact_ids))
+        mean = statistics.fmean(ms)
+        results.append({"method": label, "latency_ms": mean,
+                        "latency_std_ms": statistics.stdev(ms) if len(ms) > 1 else 0.0,
+                        "queries_per_s": B / (mean / 1e3),
+                        "recall_at_100_vs_exact": hits / exact_ids.numel(),
+                        "candidates_per_query_mean": None if label in ("BruteForce",) or
+                        label.startswith("TwoPass") else float(rr_n.float().mean().item())})
+        print(f"# {label}: {mean:.3f} ms", file=sys.stderr, flush=True)
+    bf = results[0]["latency_ms"]
+    print(json.dumps({
+        "metric": "MoL top-100 latency per batch of 32 queries, paper top-K table shapes",
+        "value": bf, "unit": "ms (brute force)", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "higher_is_better": False, "vs_baseline": None,
+        "dtype": spec.dtype, "data": "synthetic",
+        "config": {"workload": spec.name, "B": B, "N": N, "Pq": spec.Pq, "Px": spec.Px, "d": d,
+                   "H": spec.H, "k": k},
+        "methods": results}), flush=True)
 
 
 def cpu_baseline(inp, spec, nq):

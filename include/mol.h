@@ -79,7 +79,7 @@ typedef enum {
 #define MOL_MAX_P 64      /* Pq * Px                                        */
 #define MOL_MAX_H 256     /* gating MLP hidden width                         */
 #define MOL_MAX_D 1024    /* component embedding width                       */
-#define MOL_MAX_K 1024    /* k of every top-k output                         */
+#define MOL_MAX_K 8192    /* k of every top-k output                         */
 #define MOL_MAX_C 16384   /* candidates per query handed to mol_rerank       */
 
 /* One retrieval problem: shapes, storage type and device pointers (the
@@ -118,7 +118,7 @@ int mol_score(const mol_problem *prob, int32_t n_begin, int32_t n_count,
 
 /* Exact top-k with MoL (Definition 1; the paper's brute-force baseline):
  * for every query, the k items of the whole corpus with the largest phi.
- * out_score float32 [B][k], out_idx int32 [B][k].  1 <= k <= min(N, 1024).
+ * out_score float32 [B][k], out_idx int32 [B][k].  1 <= k <= min(N, 8192).
  * Needs every problem pointer and mol_workspace_size(MOL_OP_TOPK_EXACT)
  * bytes of workspace (any alignment of 256 bytes or more). */
 int mol_topk_exact(const mol_problem *prob, int32_t k, float *out_score,
@@ -152,7 +152,7 @@ int mol_topk_exact_bounded(const mol_problem *prob, int32_t k,
  *      (mol_topk_exact_bounded).
  * out_score float32 [B][k], out_idx int32 [B][k]: equal to mol_topk_exact's
  * output.  out_bound float32 [B] (may be NULL): the bound used per query.
- * 1 <= k <= min(N, 1024) and P k <= 16384.  Needs every problem pointer and
+ * 1 <= k <= min(N, 8192) and P k <= 16384.  Needs every problem pointer and
  * mol_workspace_size(MOL_OP_TOPK_TWO_PASS) bytes of workspace. */
 int mol_topk_two_pass(const mol_problem *prob, int32_t k, int32_t mode,
                       float *out_score, int32_t *out_idx, float *out_bound,
@@ -163,7 +163,7 @@ int mol_topk_two_pass(const mol_problem *prob, int32_t k, int32_t mode,
  * items with the largest m(q, x) = max_p s_p(q, x).  Since phi <= m, it is
  * also the candidate generator whose k-th score bounds Algorithm 1's range.
  * out_score float32 [B][k] (the m values), out_idx int32 [B][k].
- * 1 <= k <= min(N, 1024).  Reads only Q and X (gating pointers may be NULL,
+ * 1 <= k <= min(N, 8192).  Reads only Q and X (gating pointers may be NULL,
  * H is ignored).  Workspace: mol_workspace_size(MOL_OP_TOPK_MAXDOT). */
 int mol_topk_maxdot(const mol_problem *prob, int32_t k, float *out_score,
                     int32_t *out_idx, void *ws, size_t ws_bytes, void *stream);
@@ -172,7 +172,7 @@ int mol_topk_maxdot(const mol_problem *prob, int32_t k, float *out_score,
  * component): for every query b and component p = pq * Px + px, the k'
  * items with the largest s_p = <f_pq(q_b), g_px(x)>.
  * out_dot float32 [B][P][k'], out_idx int32 [B][P][k'].
- * 1 <= kprime <= min(N, 1024).  Reads only Q and X (a_q, a_x, W1, b1, W2,
+ * 1 <= kprime <= min(N, 8192).  Reads only Q and X (a_q, a_x, W1, b1, W2,
  * b2 may be NULL; H is ignored).  TopKAvg (Section 3.2) is this call on the
  * averaged problem: Pq = Px = 1, Q = q', X = x' from mol_avg_embed. */
 int mol_topk_per_embd(const mol_problem *prob, int32_t kprime, float *out_dot,
@@ -188,7 +188,7 @@ int mol_topk_per_embd(const mol_problem *prob, int32_t kprime, float *out_dot,
  * distinct ids of both sets are scored with full MoL and the top-k kept.
  * out_score float32 [B][k], out_idx int32 [B][k] (padded with -INFINITY /
  * -1 when a query has fewer than k distinct ids), out_n_unique int32 [B]
- * (may be NULL).  C >= 1, C2 >= 0, C + C2 <= 16384, 1 <= k <= 1024.
+ * (may be NULL).  C >= 1, C2 >= 0, C + C2 <= 16384, 1 <= k <= 8192.
  * Needs every problem pointer; mol_workspace_size takes C + C2 as C. */
 int mol_rerank(const mol_problem *prob, const int32_t *cand, int32_t C,
                const int32_t *cand2, int32_t C2, int32_t k, float *out_score,
@@ -215,7 +215,7 @@ int mol_avg_embed(const mol_problem *prob, void *q_avg, void *x_avg,
  *   out_bound[b]  = out_S[b] - out_SK[b]      (>= the gap of Definition 2)
  *   out_looser[b] = max_p dots[b][p][m - 2] - out_SK[b]
  * (the looser bound of Theorem 2).  Any output pointer may be NULL.  Pure
- * device reduction, no workspace.  1 <= k <= 1024, P <= 64. */
+ * device reduction, no workspace.  1 <= k <= 8192, P <= 64. */
 int mol_gap_bound(int32_t B, int32_t P, int32_t m, const float *dots,
                   int32_t k, const float *scores, float *out_S, float *out_SK,
                   float *out_bound, float *out_looser, void *stream);

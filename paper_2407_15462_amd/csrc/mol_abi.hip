@@ -134,18 +134,28 @@ DevProb dev_prob(const mol_problem* p) {
 // keys of one tile plus the running top-k are reduced by repeated segmented
 // sorts until k remain.
 // ---------------------------------------------------------------------------
+// rows longer than this are reduced by radix selection, shorter ones by
+// segmented sorts
+constexpr long kRadixRowMin = 1l << 15;
+
 struct StreamPlan {
   int rows = 0, k = 0, T = 0;
   long strideA = 0, strideB = 0;
-  size_t offRun = 0, offA = 0, offB = 0, bytes = 0;
+  long sRow = 0;                   // dot buffer: floats per (p, b) row (0: no buffer)
+  size_t offRun = 0, offA = 0, offB = 0, offS = 0, bytes = 0;
 };
 
-StreamPlan plan_stream(int rows, int N, int k) {
+// dots_P, dots_B: when nonzero, a buffer of the tile's component dot
+// products [dots_P][dots_B][T] is planned too (the MFMA dots kernel feeds
+// the pair-wise kernel through it), and the tile is sized to keep it under
+// 512 MB.
+StreamPlan plan_stream(int rows, int N, int k, int dots_P = 0, int dots_B = 0) {
   StreamPlan s;
   s.rows = rows;
   s.k = k;
-  const long budget = 256l << 20;  // bytes of tile keys
+  const long budget = 512l << 20;  // bytes of tile keys
   long T = budget / (8l * rows);
+  if (dots_P > 0) T = std::min(T, (512l << 20) / (4l * dots_P * dots_B));
   T = std::max(1024l, std::min(T, static_cast<long>(N)));
   T = (T + 255) / 256 * 256;
   s.T = static_cast<int>(T);
@@ -157,8 +167,32 @@ StreamPlan plan_stream(int rows, int N, int k) {
   s.offRun = off; off = align_up(off + 8ul * rows * k);
   s.offA = off;   off = align_up(off + 8ul * rows * s.strideA);
   s.offB = off;   off = align_up(off + 8ul * rows * s.strideB);
+  if (dots_P > 0) {
+    s.sRow = dots_buffer_row(s.T);
+    s.offS = off;  off = align_up(off + 4ul * dots_P * dots_B * s.sRow);
+  }
   s.bytes = off;
   return s;
+}
+
+// Plan of the tile-streamed pair-wise path of a MoL-scored selection: with
+// the MFMA dots kernel where the shape allows.
+StreamPlan plan_pairwise(const DevProb& pr, int k) {
+  return dots_mfma_supported(pr) ? plan_stream(pr.B, pr.N, k, pr.P, pr.B) : plan_stream(pr.B, pr.N, k);
+}
+
+// Score one tile of the pair-wise path into keys A (mode: GenMode).
+hipError_t pairwise_tile(const DevProb& pr, const StreamPlan& s, char* w, int mode, const float* bound,
+                         int n0, int nt, uint64_t* A, long strideA, hipStream_t st) {
+  if (s.sRow == 0)
+    return launch_phi_generic(pr, mode, bound, n0, nt, nullptr, nullptr, 0, nullptr, 0, 0, nullptr, 0, A,
+                              strideA, st);
+  float* sbuf = reinterpret_cast<float*>(w + s.offS);
+  const long pstride = s.sRow * pr.B;
+  hipError_t e = launch_dots_mfma(pr, n0, nt, kDotsToBuffer, sbuf, pstride, s.sRow, nullptr, 0, st);
+  if (e != hipSuccess) return e;
+  return launch_phi_generic(pr, mode, bound, n0, nt, nullptr, nullptr, 0, sbuf, pstride, s.sRow, nullptr, 0, A,
+                            strideA, st);
 }
 
 // Reduce rows of `len` keys held in buffer A (stride strideA) to the top k,
@@ -167,6 +201,11 @@ int reduce_rows(const StreamPlan& s, char* ws, long len, uint64_t* out, long out
                 hipStream_t st) {
   uint64_t* bufs[2] = {reinterpret_cast<uint64_t*>(ws + s.offA), reinterpret_cast<uint64_t*>(ws + s.offB)};
   long strides[2] = {s.strideA, s.strideB};
+  // long rows or large k: one radix selection per row
+  if (s.k > 1024 || len > kRadixRowMin) {
+    MOL_TRY_HIP(launch_radix_topk(bufs[0], strides[0], s.rows, len, s.k, out, out_stride, st), "radix top-k");
+    return MOL_OK;
+  }
   int cur = 0;
   for (;;) {
     const int S = segment_size_for(static_cast<int>(len), s.k);
@@ -204,10 +243,12 @@ int stream_topk(const StreamPlan& s, int N, char* ws, F score_tile, float* out_s
   return MOL_OK;
 }
 
-// Rerank workspace: uniq [B][C], n_unique [B], key rows A/B, final keys.
+// Rerank workspace: uniq [B][C], n_unique [B], key rows A/B, final keys,
+// and on the generic path with MFMA dots the candidates' dot products.
 struct RerankPlan {
   StreamPlan s;
-  size_t offUniq = 0, offNu = 0, offFinal = 0, bytes = 0;
+  long sRow = 0;
+  size_t offUniq = 0, offNu = 0, offFinal = 0, offS = 0, bytes = 0;
 };
 
 RerankPlan plan_rerank(const DevProb& pr, int C, int k) {
@@ -232,6 +273,10 @@ RerankPlan plan_rerank(const DevProb& pr, int C, int k) {
   r.offFinal = off; off = align_up(off + 8ul * B * k);
   r.offUniq = off;  off = align_up(off + 4ul * B * C);
   r.offNu = off;    off = align_up(off + 4ul * B);
+  if (!rerank_supported(pr, k) && dots_mfma_supported(pr)) {
+    r.sRow = dots_buffer_row(C);
+    r.offS = off;   off = align_up(off + 4ul * pr.P * B * r.sRow);
+  }
   r.bytes = off;
   return r;
 }
@@ -299,11 +344,11 @@ size_t per_embd_ws_bytes(const DevProb& pr, int kp) {
 }
 
 size_t exact_ws_bytes(const DevProb& pr, int k) {
-  return fused_supported(pr, k) ? plan_fused_exact(pr, k).bytes : plan_stream(pr.B, pr.N, k).bytes;
+  return fused_supported(pr, k) ? plan_fused_exact(pr, k).bytes : plan_pairwise(pr, k).bytes;
 }
 
 size_t maxdot_ws_bytes(const DevProb& pr, int k) {
-  return fused_maxdot_supported(pr, k) ? plan_fused_exact(pr, k).bytes : plan_stream(pr.B, pr.N, k).bytes;
+  return fused_maxdot_supported(pr, k) ? plan_fused_exact(pr, k).bytes : plan_pairwise(pr, k).bytes;
 }
 
 // Algorithm 1 workspace: per-component lists, the rerank output over G,
@@ -373,10 +418,10 @@ int run_exact(const DevProb& pr, int k, const float* bound, float* out_score, in
     MOL_TRY_HIP(launch_decode(fin, k, pr.B, k, out_score, out_idx, st), "decode");
     return MOL_OK;
   }
-  const StreamPlan s = plan_stream(pr.B, pr.N, k);
+  const StreamPlan s = plan_pairwise(pr, k);
   const int mode = bound ? kGenBounded : kGenPhi;
   auto tile = [&](int n0, int nt, uint64_t* A, long strideA) {
-    return launch_phi_generic(pr, mode, bound, n0, nt, nullptr, nullptr, 0, nullptr, 0, A, strideA, st);
+    return pairwise_tile(pr, s, w, mode, bound, n0, nt, A, strideA, st);
   };
   return stream_topk(s, pr.N, w, tile, out_score, out_idx, st);
 }
@@ -395,10 +440,9 @@ int run_maxdot(const DevProb& pr, int k, float* out_score, int32_t* out_idx, cha
     MOL_TRY_HIP(launch_decode(fin, k, pr.B, k, out_score, out_idx, st), "decode");
     return MOL_OK;
   }
-  const StreamPlan s = plan_stream(pr.B, pr.N, k);
+  const StreamPlan s = plan_pairwise(pr, k);
   auto tile = [&](int n0, int nt, uint64_t* A, long strideA) {
-    return launch_phi_generic(pr, kGenMaxDot, nullptr, n0, nt, nullptr, nullptr, 0, nullptr, 0, A, strideA,
-                              st);
+    return pairwise_tile(pr, s, w, kGenMaxDot, nullptr, n0, nt, A, strideA, st);
   };
   return stream_topk(s, pr.N, w, tile, out_score, out_idx, st);
 }
@@ -421,8 +465,10 @@ int run_per_embd(const DevProb& pr, int kprime, float* out_dot, int32_t* out_idx
     return MOL_OK;
   }
   const StreamPlan s = plan_stream(rows, pr.N, kprime);
+  const bool gemm = dots_mfma_supported(pr);
   auto tile = [&](int n0, int nt, uint64_t* A, long strideA) {
-    return launch_dots_generic(pr, n0, nt, A, strideA, st);
+    return gemm ? launch_dots_mfma(pr, n0, nt, kDotsToKeys, nullptr, 0, 0, A, strideA, st)
+                : launch_dots_generic(pr, n0, nt, A, strideA, st);
   };
   return stream_topk(s, pr.N, w, tile, out_dot, out_idx, st);
 }
@@ -446,9 +492,15 @@ int run_rerank(const DevProb& pr, const int32_t* cand, int C, const int32_t* can
     MOL_TIMED_LAUNCH(timed_op, st, launch_rerank(pr, uniq, nu, CT, k, negate, A, st), "fused rerank");
     if ((rc = reduce_rows(r.s, w, L0, fin, k, st))) return rc;
   } else {
+    // candidates' dot products on MFMA where the shape allows, then the
+    // pair-wise gating kernel
+    float* sbuf = r.sRow ? reinterpret_cast<float*>(w + r.offS) : nullptr;
+    const long pstride = r.sRow * pr.B;
+    if (sbuf)
+      MOL_TRY_HIP(launch_dots_mfma_gather(pr, uniq, nu, CT, CT, sbuf, pstride, r.sRow, st), "rerank dots");
     MOL_TIMED_LAUNCH(timed_op, st,
                      launch_phi_generic(pr, negate ? kGenNegPhi : kGenPhi, nullptr, 0, CT, uniq, nu, CT,
-                                        nullptr, 0, A, r.s.strideA, st),
+                                        sbuf, pstride, r.sRow, nullptr, 0, A, r.s.strideA, st),
                      "rerank score");
     if ((rc = reduce_rows(r.s, w, CT, fin, k, st))) return rc;
   }
@@ -562,8 +614,8 @@ int mol_score(const mol_problem* prob, int32_t n_begin, int32_t n_count, float* 
     return MOL_OK;
   }
   MOL_TIMED_LAUNCH(MOL_OP_SCORE, st,
-                   launch_phi_generic(pr, kGenPhi, nullptr, n_begin, n_count, nullptr, nullptr, 0, phi, n_count,
-                                      nullptr, 0, st),
+                   launch_phi_generic(pr, kGenPhi, nullptr, n_begin, n_count, nullptr, nullptr, 0, nullptr, 0,
+                                      0, phi, n_count, nullptr, 0, st),
                    "mol_score");
   return MOL_OK;
 }

@@ -313,7 +313,7 @@ __global__ __launch_bounds__(64 * kWaves, 1) void k_mol_fused(
 // ---------------------------------------------------------------------------
 static bool fused_shape(const DevProb& pr, bool mlp) {
   if (pr.dtype != MOL_BF16 || pr.Pq != 8) return false;
-  if (pr.Px == 8 && pr.d == 64) return !mlp || pr.H == 64;
+  if (pr.Px == 8 && (pr.d == 64 || pr.d == 32)) return !mlp || pr.H == 64;
   if (pr.Px == 4 && pr.d == 64) return !mlp || pr.H == 64;
   if (pr.Px == 4 && pr.d == 128) return !mlp || pr.H == 128;
   return false;
@@ -353,6 +353,9 @@ static hipError_t launch_fused_d(const DevProb& pr, int k, int R, int range_len,
                                  int n_end, const float* bound, uint64_t* partial, float* phi,
                                  long phi_stride, hipStream_t st) {
   // the max-dot epilogue has no gating MLP: one instantiation per (Px, d)
+  if (pr.Px == 8 && pr.d == 32)
+    return launch_fused_t<8, 32, 64, EPI>(pr, k, R, range_len, G, n_begin, n_end, bound, partial, phi,
+                                          phi_stride, st);
   if (pr.Px == 8)
     return launch_fused_t<8, 64, 64, EPI>(pr, k, R, range_len, G, n_begin, n_end, bound, partial, phi,
                                           phi_stride, st);

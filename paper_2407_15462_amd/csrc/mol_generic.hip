@@ -81,6 +81,7 @@ template <typename T, int PMAX>
 __global__ __launch_bounds__(256) void k_phi_generic(
     DevProb pr, int mode, const float* __restrict__ bound, int n_begin, int n_count,
     const int32_t* __restrict__ items, const int32_t* __restrict__ item_count, long item_stride,
+    const float* __restrict__ sbuf, long s_pstride, long s_bstride,
     float* __restrict__ phi, long phi_stride, uint64_t* __restrict__ keys, long key_stride) {
   extern __shared__ float smem[];
   const int P = pr.P, H = pr.H;
@@ -108,7 +109,12 @@ __global__ __launch_bounds__(256) void k_phi_generic(
   }
   const long n = items ? static_cast<long>(items[b * item_stride + i]) : static_cast<long>(n_begin) + i;
   float s[PMAX];
-  pair_dots<T, PMAX>(pr, b, n, s);
+  if (sbuf) {   // dot products formed by the MFMA kernel
+#pragma unroll
+    for (int p = 0; p < PMAX; ++p) s[p] = p < P ? sbuf[p * s_pstride + b * s_bstride + i] : 0.f;
+  } else {
+    pair_dots<T, PMAX>(pr, b, n, s);
+  }
   float v;
   if (mode == kGenBounded || mode == kGenMaxDot) {
     float m = s[0], mabs = fabsf(s[0]);
@@ -320,6 +326,7 @@ static size_t phi_smem_bytes(const DevProb& pr) {
 template <typename T, int PMAX>
 static hipError_t launch_phi_t(const DevProb& pr, int mode, const float* bound, int n_begin, int n_count,
                                const int32_t* items, const int32_t* item_count, long item_stride,
+                               const float* sbuf, long s_pstride, long s_bstride,
                                float* phi, long phi_stride, uint64_t* keys, long key_stride,
                                hipStream_t st) {
   const size_t smem = mode == kGenMaxDot ? 0 : phi_smem_bytes(pr);
@@ -331,35 +338,38 @@ static hipError_t launch_phi_t(const DevProb& pr, int mode, const float* bound, 
   }
   dim3 grid((n_count + 255) / 256, pr.B);
   hipLaunchKernelGGL((k_phi_generic<T, PMAX>), grid, dim3(256), smem, st, pr, mode, bound, n_begin,
-                     n_count, items, item_count, item_stride, phi, phi_stride, keys, key_stride);
+                     n_count, items, item_count, item_stride, sbuf, s_pstride, s_bstride, phi, phi_stride,
+                     keys, key_stride);
   return hipGetLastError();
 }
 
 template <typename T>
 static hipError_t launch_phi_p(const DevProb& pr, int mode, const float* bound, int n_begin, int n_count,
                                const int32_t* items, const int32_t* item_count, long item_stride,
+                               const float* sbuf, long s_pstride, long s_bstride,
                                float* phi, long phi_stride, uint64_t* keys, long key_stride,
                                hipStream_t st) {
   if (pr.P <= 4)
-    return launch_phi_t<T, 4>(pr, mode, bound, n_begin, n_count, items, item_count, item_stride, phi,
-                              phi_stride, keys, key_stride, st);
+    return launch_phi_t<T, 4>(pr, mode, bound, n_begin, n_count, items, item_count, item_stride, sbuf,
+                              s_pstride, s_bstride, phi, phi_stride, keys, key_stride, st);
   if (pr.P <= 16)
-    return launch_phi_t<T, 16>(pr, mode, bound, n_begin, n_count, items, item_count, item_stride, phi,
-                               phi_stride, keys, key_stride, st);
-  return launch_phi_t<T, 64>(pr, mode, bound, n_begin, n_count, items, item_count, item_stride, phi,
-                             phi_stride, keys, key_stride, st);
+    return launch_phi_t<T, 16>(pr, mode, bound, n_begin, n_count, items, item_count, item_stride, sbuf,
+                               s_pstride, s_bstride, phi, phi_stride, keys, key_stride, st);
+  return launch_phi_t<T, 64>(pr, mode, bound, n_begin, n_count, items, item_count, item_stride, sbuf,
+                             s_pstride, s_bstride, phi, phi_stride, keys, key_stride, st);
 }
 
 hipError_t launch_phi_generic(const DevProb& pr, int mode, const float* bound, int n_begin, int n_count,
                               const int32_t* items, const int32_t* item_count, long item_stride,
+                              const float* sbuf, long s_pstride, long s_bstride,
                               float* phi, long phi_stride, uint64_t* keys, long key_stride,
                               hipStream_t st) {
   if (n_count <= 0) return hipSuccess;
   if (pr.dtype == MOL_BF16)
-    return launch_phi_p<bf16_t>(pr, mode, bound, n_begin, n_count, items, item_count, item_stride, phi,
-                                phi_stride, keys, key_stride, st);
-  return launch_phi_p<float>(pr, mode, bound, n_begin, n_count, items, item_count, item_stride, phi,
-                             phi_stride, keys, key_stride, st);
+    return launch_phi_p<bf16_t>(pr, mode, bound, n_begin, n_count, items, item_count, item_stride, sbuf,
+                                s_pstride, s_bstride, phi, phi_stride, keys, key_stride, st);
+  return launch_phi_p<float>(pr, mode, bound, n_begin, n_count, items, item_count, item_stride, sbuf,
+                             s_pstride, s_bstride, phi, phi_stride, keys, key_stride, st);
 }
 
 template <typename T>

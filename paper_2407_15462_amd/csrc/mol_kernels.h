@@ -9,15 +9,36 @@ namespace mol {
 // Score of the pair-wise kernel: phi; phi restricted to items whose
 // max_p s_p can reach bound[b]; max_p s_p; -phi.
 enum GenMode { kGenPhi = 0, kGenBounded = 1, kGenMaxDot = 2, kGenNegPhi = 3 };
+// sbuf: NULL, or the component dot products of items n_begin + i laid out
+// as sbuf[p * s_pstride + b * s_bstride + i] (contiguous ranges only).
 hipError_t launch_phi_generic(const DevProb& pr, int mode, const float* bound, int n_begin, int n_count,
                               const int32_t* items, const int32_t* item_count, long item_stride,
+                              const float* sbuf, long s_pstride, long s_bstride,
                               float* phi, long phi_stride, uint64_t* keys, long key_stride,
                               hipStream_t st);
 hipError_t launch_dots_generic(const DevProb& pr, int n_begin, int n_count, uint64_t* keys,
                                long key_stride, hipStream_t st);
 
+// Component dot products on MFMA for the generic shapes (bf16, d % 32 == 0):
+// into a buffer s[p][b][i] (row stride dots_buffer_row(nt) floats, p stride
+// B * that) for the pair-wise gating kernel, or into per-component sort keys.
+enum DotsMode { kDotsToBuffer = 0, kDotsToKeys = 1 };
+bool dots_mfma_supported(const DevProb& pr);
+long dots_buffer_row(int nt);
+hipError_t launch_dots_mfma(const DevProb& pr, int n0, int nt, int mode, float* sbuf, long s_pstride,
+                            long s_bstride, uint64_t* keys, long key_stride, hipStream_t st);
+// the same into the buffer for per-query candidate lists (items [B][item_stride],
+// item_count [B], at most C per query): s[p][b][i] of candidate i
+hipError_t launch_dots_mfma_gather(const DevProb& pr, const int32_t* items, const int32_t* item_count,
+                                   long item_stride, int C, float* sbuf, long s_pstride, long s_bstride,
+                                   hipStream_t st);
+
 // Selection machinery over 64-bit sort keys.
 int segment_size_for(int L, int k);
+// Rows of L keys -> their top k (k <= 8192) by radix selection, one
+// workgroup per row (keys of a row distinct apart from empty ones).
+hipError_t launch_radix_topk(const uint64_t* in, long in_stride, int rows, long L, int k, uint64_t* out,
+                             long out_stride, hipStream_t st);
 hipError_t launch_segment_topk(const uint64_t* in, long in_stride, int rows, int L, int k,
                                uint64_t* out, long out_stride, hipStream_t st);
 hipError_t launch_decode(const uint64_t* keys, long key_stride, int rows, int k, float* score,
@@ -41,7 +62,8 @@ hipError_t launch_pick_bound(const float* scores, int stride, int col, float sig
 
 namespace mol {
 
-// Fused MFMA scoring (bf16, Pq = 8; (Px, d, H) in {(8,64,64), (4,64,64), (4,128,128)}).
+// Fused MFMA scoring (bf16, Pq = 8; (Px, d, H) in {(8,32,64), (8,64,64), (4,64,64),
+// (4,128,128)}).
 bool fused_supported(const DevProb& pr, int k);
 // max-component-dot epilogue: the same shapes with H ignored
 bool fused_maxdot_supported(const DevProb& pr, int k);
@@ -61,7 +83,7 @@ namespace mol {
 
 // Per-component top-k' with MFMA dots: a bucket-maximum scan, a per-list
 // starting threshold, and a threshold scan with staged merges
-// (bf16, d in {64, 128}, k' <= 1024).
+// (bf16, d in {32, 64, 128}, k' <= 1024).
 struct PerEmbdGrid {
   struct Scan {
     int R = 0, range_len = 0, G = 0;   // item ranges, items per range, vector groups

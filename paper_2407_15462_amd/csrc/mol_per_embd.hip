@@ -413,7 +413,7 @@ __global__ __launch_bounds__(256) void k_bucket_threshold(const float* __restric
 // ---------------------------------------------------------------------------
 bool per_embd_supported(const DevProb& pr, int kp) {
   if (pr.dtype != MOL_BF16) return false;
-  if (pr.d != 64 && pr.d != 128) return false;
+  if (pr.d != 32 && pr.d != 64 && pr.d != 128) return false;
   return kp <= 1024;
 }
 
@@ -479,6 +479,14 @@ static hipError_t launch_pe_d(const DevProb& pr, int kp, const PerEmbdGrid& g, f
 hipError_t launch_per_embd(const DevProb& pr, int kp, const PerEmbdGrid& g, float* bmax, float* thr,
                            uint64_t* lists, uint64_t* stg, hipStream_t st) {
   const int KL = per_embd_list_cap(kp);
+  if (pr.d == 32) {
+    switch (KL) {
+      case 128: return launch_pe_d<32, 128>(pr, kp, g, bmax, thr, lists, stg, st);
+      case 256: return launch_pe_d<32, 256>(pr, kp, g, bmax, thr, lists, stg, st);
+      case 512: return launch_pe_d<32, 512>(pr, kp, g, bmax, thr, lists, stg, st);
+      default: return launch_pe_d<32, 1024>(pr, kp, g, bmax, thr, lists, stg, st);
+    }
+  }
   if (pr.d == 64) {
     switch (KL) {
       case 128: return launch_pe_d<64, 128>(pr, kp, g, bmax, thr, lists, stg, st);

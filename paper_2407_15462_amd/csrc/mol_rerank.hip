@@ -111,7 +111,10 @@ int rerank_chunk(int C) { return C <= 1024 ? 256 : 1024; }
 template <bool NEG>
 static void launch_rerank_t(const DevProb& pr, dim3 grid, const int32_t* uniq, const int32_t* n_unique,
                             int C, int k, int chunk, int nchunks, uint64_t* partial, hipStream_t st) {
-  if (pr.Px == 8)
+  if (pr.Px == 8 && pr.d == 32)
+    hipLaunchKernelGGL((k_mol_rerank<8, 32, 64, NEG>), grid, dim3(64 * kWaves), 0, st, pr, uniq, n_unique, C,
+                       k, chunk, nchunks, partial);
+  else if (pr.Px == 8)
     hipLaunchKernelGGL((k_mol_rerank<8, 64, 64, NEG>), grid, dim3(64 * kWaves), 0, st, pr, uniq, n_unique, C,
                        k, chunk, nchunks, partial);
   else if (pr.d == 128)

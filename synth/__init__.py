@@ -4,6 +4,6 @@ This package only draws random numbers and lays them out; it holds none of
 the scoring or retrieval arithmetic.  Both the GPU library (through its
 Python binding) and the CPU oracle consume what it produces.
 """
-from .workloads import WORKLOADS, Workload, MolInputs, generate, to_numpy
+from .workloads import PAPER_METHODS, WORKLOADS, Workload, MolInputs, generate, to_numpy
 
-__all__ = ["WORKLOADS", "Workload", "MolInputs", "generate", "to_numpy"]
+__all__ = ["PAPER_METHODS", "WORKLOADS", "Workload", "MolInputs", "generate", "to_numpy"]

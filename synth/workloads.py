@@ -60,6 +60,7 @@ class Workload:
     kprime: int = 0       # per-component top-k' (approximate path)
     k_avg: int = 0        # averaged-embedding top-k (approximate path)
     gating_std: float = 0.1   # standard deviation of a_q, a_x, W1, b1, W2, b2
+    side_logits: bool = True  # per-query / per-item gating logits a_q, a_x (else zero)
     note: str = ""
 
     @property
@@ -101,7 +102,38 @@ WORKLOADS: Dict[str, Workload] = {
                  dtype="bf16", k=100, items="mixture", clusters=16384,
                  q_noise=0.2, kprime=256, k_avg=1024,
                  note="per-component top-256 and averaged top-1024, rerank"),
+        # Shapes of the paper's top-K retrieval benchmark (Section 4's workload
+        # table: items, P_q x P_x, d_P), measured on batches of 32 queries.
+        # The query noise gives a cosine of about 0.53 to the source item at
+        # every d (sigma = 1.6 / sqrt(d)).  The hidden width is not stated:
+        # H = 128 at d = 128, 64 otherwise.  The question-answering workload
+        # gates on the dot products alone (no per-query / per-item logits).
+        Workload("paper_ml20m", B=32, N=24186, Pq=8, Px=4, d=128, H=128,
+                 dtype="bf16", k=100, items="mixture", clusters=128,
+                 q_noise=1.6 / 128 ** 0.5,
+                 note="ML-20M shape: 24,186 items, 8 x 4 components, d = 128"),
+        Workload("paper_books", B=32, N=674044, Pq=8, Px=8, d=32, H=64,
+                 dtype="bf16", k=100, items="mixture", clusters=4096,
+                 q_noise=1.6 / 32 ** 0.5,
+                 note="Books shape: 674,044 items, 8 x 8 components, d = 32"),
+        Workload("paper_nq320k", B=32, N=109739, Pq=4, Px=4, d=768, H=64,
+                 dtype="bf16", k=100, items="mixture", clusters=512,
+                 q_noise=1.6 / 768 ** 0.5, side_logits=False,
+                 note="NQ320K shape: 109,739 items, 4 x 4 components, d = 768"),
     ]
+}
+
+# Method rows of the paper's top-K table for each of its workloads:
+# ("per_embd", N), ("avg", N), ("comb", N1, N2).
+PAPER_METHODS = {
+    "paper_ml20m": [("per_embd", 5), ("per_embd", 10), ("per_embd", 50), ("per_embd", 100),
+                    ("avg", 200), ("avg", 500), ("comb", 5, 200)],
+    "paper_books": [("per_embd", 5), ("per_embd", 50), ("per_embd", 100), ("per_embd", 200),
+                    ("avg", 200), ("avg", 500), ("avg", 1000), ("avg", 2000), ("avg", 4000),
+                    ("avg", 8000), ("comb", 5, 200), ("comb", 50, 500), ("comb", 100, 1000),
+                    ("comb", 200, 2000)],
+    "paper_nq320k": [("per_embd", 5), ("per_embd", 10), ("per_embd", 50), ("avg", 100),
+                     ("comb", 5, 100)],
 }
 
 # The 1M-item approximate workload reuses the exact one's data.
@@ -161,7 +193,7 @@ def generate(spec: Workload, seed: int = 0, device: str = "cpu") -> MolInputs:
                                 generator=_generator(device, *key, "cluster", c0))
             z = centres[cid] + 0.3 * z
         X[:, c0:c0 + n, :] = _unit(z).to(store).permute(1, 0, 2)
-        a_x[c0:c0 + n] = spec.gating_std * randn((n, P), "a_x", c0)
+        a_x[c0:c0 + n] = (spec.gating_std if spec.side_logits else 0.0) * randn((n, P), "a_x", c0)
 
     if spec.items == "mixture":
         src = torch.randint(0, N, (B,), device=device,
@@ -172,9 +204,10 @@ def generate(spec: Workload, seed: int = 0, device: str = "cpu") -> MolInputs:
         Q = _unit(randn((B, Pq, d), "queries")).to(store)
 
     sd = spec.gating_std
+    sd_side = sd if spec.side_logits else 0.0
     return MolInputs(
         spec=spec, Q=Q.contiguous(), X=X,
-        a_q=(sd * randn((B, P), "a_q")).contiguous(),
+        a_q=(sd_side * randn((B, P), "a_q")).contiguous(),
         a_x=a_x,
         W1=(sd * randn((H, P), "W1")).to(store).contiguous(),
         b1=(sd * randn((H,), "b1")).contiguous(),

@@ -161,7 +161,7 @@ def test_two_pass_bounded_and_maxdot_validation():
                                  None) == mol.MOL_EWORKSPACE
     assert lib.mol_topk_two_pass(ctypes.byref(_problem(a_q=None)), 10, 0, 256, 256, None, ws, big,
                                  None) == mol.MOL_EINVAL
-    # bounded: the bound array is required; k within [1, min(N, 1024)]
+    # bounded: the bound array is required; k within [1, min(N, 8192)]
     assert lib.mol_topk_exact_bounded(ctypes.byref(c), 10, None, 256, 256, ws, big, None) \
         == mol.MOL_EINVAL
     assert lib.mol_topk_exact_bounded(ctypes.byref(c), 0, 256, 256, 256, ws, big, None) \

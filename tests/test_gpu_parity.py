@@ -27,6 +27,11 @@ def _cases_small():
         ("hybrid_8m_shape_ragged", W["hybrid_8m"].scaled(B=9, N=3001, clusters=64)),
         # bf16 with P_q = 4: served by the generic kernels
         ("bf16_pq4_generic", dataclasses.replace(W["exact_32k"], Pq=4, B=11, N=2100, clusters=16)),
+        # the paper's top-K benchmark shapes at 32 queries: d = 32 (fused),
+        # d = 128 with P = 8 x 4 (fused), d = 768 with P = 4 x 4 (generic)
+        ("paper_books_shape", W["paper_books"].scaled(N=5003, clusters=64)),
+        ("paper_ml20m_shape", W["paper_ml20m"].scaled(N=3001, clusters=32)),
+        ("paper_nq320k_shape", W["paper_nq320k"].scaled(N=2011, clusters=16)),
     ]
 
 
@@ -111,6 +116,9 @@ def test_duplicate_items_tie_to_lower_index():
     ("small_p64_k600", W["exact_1m"].scaled(B=2, N=9001, clusters=32), 600),
     ("small_d128_k1024", W["hybrid_8m"].scaled(B=2, N=12003, clusters=32), 1024),
     ("f32", W["tiny_exact_f32"].scaled(B=4, N=2000), 50),
+    ("books_d32_k5", W["paper_books"].scaled(B=3, N=9001, clusters=32), 5),
+    ("books_d32_k200", W["paper_books"].scaled(B=3, N=9001, clusters=32), 200),
+    ("nq_d768_generic", W["paper_nq320k"].scaled(B=3, N=3001, clusters=16), 50),
 ])
 def test_topk_per_embd_matches_oracle(name, spec, kp):
     log(f"[per_embd] {name} B={spec.B} N={spec.N} P={spec.P} k'={kp}")
@@ -260,6 +268,70 @@ def test_rerank_matches_oracle(C, k):
         full[uniq] = phi
         check_topk_row(full, i[b, :kk], s[b, :kk], kk, f"rerank query {b}")
         assert np.all(i[b, kk:] == -1) and np.all(np.isneginf(s[b, kk:]))
+
+
+@pytest.mark.parametrize("name,spec,C", [
+    ("books_d32", W["paper_books"].scaled(B=5, N=4001, clusters=32), 1000),
+    ("nq_d768_generic", W["paper_nq320k"].scaled(B=5, N=2003, clusters=16), 600),
+])
+def test_rerank_paper_shapes(name, spec, C):
+    k = spec.k
+    log(f"[rerank] {name} C={C} k={k}")
+    inp = cuda_inputs(spec, seed=18)
+    prob = mol.Problem.from_inputs(inp)
+    g = torch.Generator(device="cuda").manual_seed(6)
+    cand = torch.randint(0, spec.N, (spec.B, C), device="cuda", generator=g, dtype=torch.int32)
+    s, i, nu = mol.rerank(prob, cand, k)
+    torch.cuda.synchronize()
+    op = oracle_problem(inp)
+    cand_np = cand.cpu().numpy()
+    s, i, nu = s.cpu().numpy(), i.cpu().numpy(), nu.cpu().numpy()
+    for b in range(spec.B):
+        uniq = mo.union_dedup([cand_np[b]])
+        assert nu[b] == len(uniq)
+        _, _, phi = mo.mol_terms(op, b, uniq)
+        full = np.full(spec.N, -np.inf)
+        full[uniq] = phi
+        check_topk_row(full, i[b], s[b], k, f"rerank_{name} query {b}")
+
+
+def test_radix_selection_long_rows_large_k_and_ties():
+    """Rows longer than the segmented sorts take (70,001 items of a d = 768
+    problem with one all-zero query vector: every key of its lists ties on
+    the score), and k above 1024 (TopKAvg, exact MoL top-k) go through the
+    radix selection."""
+    spec = W["paper_nq320k"].scaled(B=2, N=70001, clusters=64)
+    inp = cuda_inputs(spec, seed=41)
+    inp.Q[1, 2, :] = 0
+    log(f"[radix] per-component k'=300 B={spec.B} N={spec.N} d={spec.d}")
+    pe = mol.Problem(inp.Q, inp.X)
+    dots, ids = mol.topk_per_embd(pe, 300)
+    torch.cuda.synchronize()
+    op = oracle_problem(inp)
+    dots, ids = dots.cpu().numpy(), ids.cpu().numpy()
+    for b in range(spec.B):
+        s_all = mo.all_dots(op, b)
+        for p in range(spec.P):
+            check_topk_row(s_all[:, p], ids[b, p], dots[b, p], 300, f"radix b={b} p={p}")
+    for px in range(spec.Px):
+        assert ids[1, 2 * spec.Px + px].tolist() == list(range(300))
+    # TopKAvg with k' = 3000 on a d = 32 problem (generic MFMA dots + radix)
+    spec2 = W["paper_books"].scaled(B=4, N=20011, clusters=64)
+    inp2 = cuda_inputs(spec2, seed=42)
+    prob2 = mol.Problem.from_inputs(inp2)
+    q, x = mol.avg_embed(prob2)
+    d2, i2 = mol.topk_per_embd(mol.averaged_problem(prob2, q, x), 3000)
+    # exact MoL top-k with k = 1500 (the pair-wise path)
+    s3, i3 = mol.topk_exact(prob2, 1500)
+    torch.cuda.synchronize()
+    op2 = oracle_problem(inp2)
+    oavg = mo.averaged_problem(op2)
+    phi = mo.mol_scores(op2, list(range(spec2.B)))
+    d2, i2, s3, i3 = d2.cpu().numpy(), i2.cpu().numpy(), s3.cpu().numpy(), i3.cpu().numpy()
+    for b in range(spec2.B):
+        s = mo.all_dots(oavg, b)[:, 0]
+        check_topk_row(s, i2[b, 0], d2[b, 0], 3000, f"radix_avg b={b}")
+        check_topk_row(phi[b], i3[b], s3[b], 1500, f"radix_exact b={b}")
 
 
 def test_worked_example_through_the_abi():

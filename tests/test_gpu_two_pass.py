@@ -24,6 +24,8 @@ CASES = [
     ("hybrid_8m_shape_ragged", W["hybrid_8m"].scaled(B=9, N=3001, clusters=64)),
     ("tiny_exact_f32", W["tiny_exact_f32"]),
     ("bf16_pq4_generic", dataclasses.replace(W["exact_32k"], Pq=4, B=11, N=2100, clusters=16)),
+    ("paper_books_shape", W["paper_books"].scaled(N=3001, clusters=32)),
+    ("paper_nq320k_shape", W["paper_nq320k"].scaled(B=8, N=1500, clusters=16)),
 ]
 IDS = [c[0] for c in CASES]
 
