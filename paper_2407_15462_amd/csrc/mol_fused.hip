@@ -233,45 +233,61 @@ __global__ __launch_bounds__(64 * kWaves, 1) void k_mol_fused(
         s2[0][mu] = __uint_as_float(sw[0]);
         s2[1][mu] = __uint_as_float(sw[1]);
       }
-      // the two queries one after the other (keeps the register peak low)
       float phi[2];
-      bool offer[2];
+      bool offer[2] = {item_ok, item_ok};
+      // GEMM3 accumulator input of query qb: log2(e) a_x (the item's, from
+      // the stage) + log2(e) (a_q + b2) (the query's), at the lane's
+      // p = base(g) + 4 pt + i
+      auto gate_bias = [&](int qb, f32x4_t(&c0)[S::PT]) {
 #pragma unroll
-      for (int qb = 0; qb < 2; ++qb) {
-        offer[qb] = item_ok;
+        for (int pt = 0; pt < S::PT; ++pt) {
+          const float4 cb = *reinterpret_cast<const float4*>(sCb + (2 * wave + qb) * P + base + 4 * pt);
+          c0[pt] = f32x4_t{fmaf(axv[pt].x, kLog2e, cb.x), fmaf(axv[pt].y, kLog2e, cb.y),
+                           fmaf(axv[pt].z, kLog2e, cb.z), fmaf(axv[pt].w, kLog2e, cb.w)};
+        }
+      };
+      if constexpr (EPI == kEpiTopk || EPI == kEpiDense) {
+        // both queries' MLP chains in one call, free to interleave
+        f32x4_t c0[2][S::PT];
+        gate_bias(0, c0[0]);
+        gate_bias(1, c0[1]);
+        mlp.template phi<2>(s2, c0, phi);
+      }
+#pragma unroll
+      for (int qb = 0; qb < 2 && (EPI == kEpiBounded || EPI == kEpiMaxDot); ++qb) {
         if constexpr (EPI == kEpiBounded || EPI == kEpiMaxDot) {
-          // m = max_p s_p of the lane's item (and max_p |s_p| for the margin)
-          float m = s2[qb][0], mabs = fabsf(s2[qb][0]);
+          // m = max_p s_p of the lane's item
+          float m = s2[qb][0];
 #pragma unroll
-          for (int mu = 1; mu < S::RUN; ++mu) {
-            m = fmaxf(m, s2[qb][mu]);
-            if (EPI == kEpiBounded) mabs = fmaxf(mabs, fabsf(s2[qb][mu]));
-          }
+          for (int mu = 1; mu < S::RUN; ++mu) m = fmaxf(m, s2[qb][mu]);
           m = max_groups(m);
           if constexpr (EPI == kEpiMaxDot) {
             phi[qb] = m;
             continue;
           } else {
-            mabs = max_groups(mabs);
             const float floor = fmaxf(qbound[qb], top[qb].theta_score);
-            offer[qb] = item_ok && m + bound_margin(mabs) >= floor;
+            // |m| <= max_p |s_p|: passing with the margin of |m| is passing
+            bool pass = m + bound_margin(fabsf(m)) >= floor;
+            if (!__all(pass || !item_ok)) {
+              // the margin of max_p |s_p| decides the rest
+              float mabs = fabsf(s2[qb][0]);
+#pragma unroll
+              for (int mu = 1; mu < S::RUN; ++mu) mabs = fmaxf(mabs, fabsf(s2[qb][mu]));
+              mabs = max_groups(mabs);
+              pass = m + bound_margin(mabs) >= floor;
+            }
+            offer[qb] = item_ok && pass;
             phi[qb] = -__builtin_inff();
             if (!__any(offer[qb])) continue;   // no item of the group can qualify
           }
         }
-        if constexpr (MLP) {
+        if constexpr (EPI == kEpiBounded) {
+          // one query at a time: the other's chain may have been skipped
           float sq[1][S::RUN];
 #pragma unroll
           for (int mu = 0; mu < S::RUN; ++mu) sq[0][mu] = s2[qb][mu];
-          // GEMM3 accumulator input: log2(e) a_x (the item's, from the stage)
-          // + log2(e) (a_q + b2) (the query's), at the lane's p = base(g) + 4 pt + i
           f32x4_t c0[1][S::PT];
-#pragma unroll
-          for (int pt = 0; pt < S::PT; ++pt) {
-            const float4 cb = *reinterpret_cast<const float4*>(sCb + (2 * wave + qb) * P + base + 4 * pt);
-            c0[0][pt] = f32x4_t{fmaf(axv[pt].x, kLog2e, cb.x), fmaf(axv[pt].y, kLog2e, cb.y),
-                                fmaf(axv[pt].z, kLog2e, cb.z), fmaf(axv[pt].w, kLog2e, cb.w)};
-          }
+          gate_bias(qb, c0[0]);
           float pq[1];
           mlp.template phi<1>(sq, c0, pq);
           phi[qb] = pq[0];
