@@ -220,6 +220,27 @@ int mol_gap_bound(int32_t B, int32_t P, int32_t m, const float *dots,
                   int32_t k, const float *scores, float *out_S, float *out_SK,
                   float *out_bound, float *out_looser, void *stream);
 
+/* Gap certificate of the combined heuristic (Theorem 3).
+ * dots float32 [B][P][m], ids int32 [B][P][m]: per-component lists sorted
+ * descending (mol_topk_per_embd with kprime = m), m > kprime + k_avg;
+ * avg_ids int32 [B][k_avg]: the TopKAvg ids (negative = empty slot; may be
+ * NULL when k_avg == 0); scores float32 [B][k]: the MoL top-k (descending)
+ * over candidates that include the first kprime ids of every list and all
+ * of avg_ids.  Writes, per query b:
+ *   out_S[b]     = S', the largest s_p over items outside the union of the
+ *                  first kprime ids of list p and avg_ids, maximised over p
+ *                  (no item outside the candidates has a larger MoL score)
+ *   out_SK[b]    = scores[b][k - 1]
+ *   out_bound[b] = out_S[b] - out_SK[b]   (>= the gap of Definition 2)
+ * With k_avg == 0 it is Theorem 2's bound.  Any output may be NULL.  Pure
+ * device work, no workspace.  P <= 64, kprime >= 1, 0 <= k_avg <= 8192,
+ * 1 <= k <= 8192. */
+int mol_gap_bound_combined(int32_t B, int32_t P, int32_t m, const float *dots,
+                           const int32_t *ids, int32_t kprime,
+                           const int32_t *avg_ids, int32_t k_avg, int32_t k,
+                           const float *scores, float *out_S, float *out_SK,
+                           float *out_bound, void *stream);
+
 /* Kernel timing, a diagnostic for throughput measurements.
  * mol_timing_enable(1) makes every later call record a pair of HIP events on
  * its stream around its main kernel: the fused scoring kernel of mol_score,

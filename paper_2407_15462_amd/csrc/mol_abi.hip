@@ -721,6 +721,23 @@ int mol_gap_bound(int32_t B, int32_t P, int32_t m, const float* dots, int32_t k,
   return MOL_OK;
 }
 
+int mol_gap_bound_combined(int32_t B, int32_t P, int32_t m, const float* dots, const int32_t* ids,
+                           int32_t kprime, const int32_t* avg_ids, int32_t k_avg, int32_t k,
+                           const float* scores, float* out_S, float* out_SK, float* out_bound, void* stream) {
+  if (B < 1 || P < 1 || P > MOL_MAX_P) return fail(MOL_EINVAL, "B = %d, P = %d: need B >= 1, 1 <= P <= %d", B, P, MOL_MAX_P);
+  if (kprime < 1 || k_avg < 0 || k_avg > MOL_MAX_K)
+    return fail(MOL_EINVAL, "kprime = %d, k_avg = %d: need kprime >= 1, 0 <= k_avg <= %d", kprime, k_avg, MOL_MAX_K);
+  if (static_cast<long>(m) <= static_cast<long>(kprime) + k_avg)
+    return fail(MOL_EINVAL, "m = %d: the lists need more than kprime + k_avg = %d entries", m, kprime + k_avg);
+  if (k < 1 || k > MOL_MAX_K) return fail(MOL_EINVAL, "k = %d outside [1, %d]", k, MOL_MAX_K);
+  if (!dots || !ids || !scores) return fail(MOL_EINVAL, "dots, ids or scores is NULL");
+  if (k_avg > 0 && !avg_ids) return fail(MOL_EINVAL, "avg_ids is NULL with k_avg = %d", k_avg);
+  MOL_TRY_HIP(launch_gap_bound_combined(B, P, m, dots, ids, kprime, avg_ids, k_avg, k, scores, out_S, out_SK,
+                                        out_bound, static_cast<hipStream_t>(stream)),
+              "combined gap bound");
+  return MOL_OK;
+}
+
 int mol_timing_enable(int on) {
   TimingLog& t = timing_log();
   std::lock_guard<std::mutex> g(t.mu);

@@ -275,6 +275,86 @@ __global__ void k_gap_bound(int B, int P, int m, const float* __restrict__ dots,
   if (out_looser) out_looser[b] = Sk - SK;
 }
 
+// ---------------------------------------------------------------------------
+// Theorem 3 certificate of the combined candidates: one workgroup per query.
+// The TopKAvg ids A_b go into an LDS hash set; for every component list
+// (descending, m entries) the first entry at position >= kprime whose id is
+// outside A_b is the largest s_p over items outside (X_{kprime,p} U A_b),
+// since the list's first kprime entries are X_{kprime,p} itself.  S' is the
+// maximum over p; -inf when some list runs out before finding one (cannot
+// happen when m > kprime + k_avg).
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void k_gap_bound_combined(int P, int m, const float* __restrict__ dots,
+                                                            const int32_t* __restrict__ ids, int kprime,
+                                                            const int32_t* __restrict__ avg_ids, int k_avg,
+                                                            int cap_log2, int k, const float* __restrict__ scores,
+                                                            float* out_S, float* out_SK, float* out_bound) {
+  extern __shared__ int32_t set[];
+  __shared__ float s_best[4];
+  const int cap = 1 << cap_log2;
+  const long b = blockIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  for (int i = tid; i < cap; i += 256) set[i] = -1;
+  __syncthreads();
+  for (int i = tid; i < k_avg; i += 256) {
+    const int32_t id = avg_ids[b * k_avg + i];
+    if (id < 0) continue;
+    uint32_t h = (static_cast<uint32_t>(id) * 0x9E3779B1u) >> (32 - cap_log2);
+    for (int probe = 0; probe < cap; ++probe) {
+      const int32_t prev = atomicCAS(&set[h], -1, id);
+      if (prev == -1 || prev == id) break;
+      h = (h + 1) & (cap - 1);
+    }
+  }
+  __syncthreads();
+  auto in_set = [&](int32_t id) {
+    uint32_t h = (static_cast<uint32_t>(id) * 0x9E3779B1u) >> (32 - cap_log2);
+    for (int probe = 0; probe < cap; ++probe) {
+      const int32_t v = set[h];
+      if (v == id) return true;
+      if (v == -1) return false;
+      h = (h + 1) & (cap - 1);
+    }
+    return false;
+  };
+  float best = -__builtin_inff();
+  for (int p = wave; p < P; p += 4) {              // one wave per list
+    const long row = (b * P + p) * static_cast<long>(m);
+    for (int base = kprime; base < m; base += 64) {
+      const int pos = base + lane;
+      const bool outside = pos < m && !in_set(ids[row + pos]);
+      const uint64_t hit = __ballot(outside);
+      if (hit) {
+        const int first = __ffsll(static_cast<long long>(hit)) - 1;
+        best = fmaxf(best, dots[row + base + first]);
+        break;
+      }
+    }
+  }
+  if (lane == 0) s_best[wave] = best;
+  __syncthreads();
+  if (tid == 0) {
+    const float S = fmaxf(fmaxf(s_best[0], s_best[1]), fmaxf(s_best[2], s_best[3]));
+    const float SK = scores[b * k + (k - 1)];
+    if (out_S) out_S[b] = S;
+    if (out_SK) out_SK[b] = SK;
+    if (out_bound) out_bound[b] = S - SK;
+  }
+}
+
+hipError_t launch_gap_bound_combined(int B, int P, int m, const float* dots, const int32_t* ids, int kprime,
+                                     const int32_t* avg_ids, int k_avg, int k, const float* scores,
+                                     float* out_S, float* out_SK, float* out_bound, hipStream_t st) {
+  const int cap_log2 = dedup_cap_log2(k_avg);
+  const size_t smem = sizeof(int32_t) << cap_log2;
+  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_gap_bound_combined),
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(smem));
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_gap_bound_combined, dim3(B), dim3(256), smem, st, P, m, dots, ids, kprime, avg_ids,
+                     k_avg, cap_log2, k, scores, out_S, out_SK, out_bound);
+  return hipGetLastError();
+}
+
 // bound[b] = sign * scores[b][col] (Algorithm 1's threshold from the rerank
 // output over G).
 __global__ void k_pick_bound(const float* __restrict__ scores, int stride, int col, float sign, int B,

@@ -54,6 +54,9 @@ hipError_t launch_dedup(const int32_t* cand, int C, const int32_t* cand2, int C2
 hipError_t launch_gap_bound(int B, int P, int m, const float* dots, int k, const float* scores,
                             float* out_S, float* out_SK, float* out_bound, float* out_looser,
                             hipStream_t st);
+hipError_t launch_gap_bound_combined(int B, int P, int m, const float* dots, const int32_t* ids, int kprime,
+                                     const int32_t* avg_ids, int k_avg, int k, const float* scores,
+                                     float* out_S, float* out_SK, float* out_bound, hipStream_t st);
 hipError_t launch_avg_embed(const DevProb& pr, void* q_avg, void* x_avg, hipStream_t st);
 hipError_t launch_pick_bound(const float* scores, int stride, int col, float sign, int B, float* bound,
                              hipStream_t st);

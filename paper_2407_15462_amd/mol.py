@@ -24,7 +24,8 @@ MOL_TWO_PASS_MIN, MOL_TWO_PASS_KTH = 0, 1
 
 EXPORTS = ("mol_workspace_size", "mol_score", "mol_topk_exact", "mol_topk_exact_bounded",
            "mol_topk_two_pass", "mol_topk_maxdot", "mol_topk_per_embd",
-           "mol_rerank", "mol_avg_embed", "mol_gap_bound", "mol_timing_enable", "mol_timing_read",
+           "mol_rerank", "mol_avg_embed", "mol_gap_bound", "mol_gap_bound_combined",
+           "mol_timing_enable", "mol_timing_read",
            "mol_status_str", "mol_last_error")
 
 
@@ -71,6 +72,7 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "mol_rerank": [P, vp, i32, vp, i32, i32, vp, vp, vp, vp, sz, vp],
         "mol_avg_embed": [P, vp, vp, vp],
         "mol_gap_bound": [i32, i32, i32, vp, i32, vp, vp, vp, vp, vp, vp],
+        "mol_gap_bound_combined": [i32, i32, i32, vp, vp, i32, vp, i32, i32, vp, vp, vp, vp, vp],
         "mol_timing_enable": [ctypes.c_int],
         "mol_timing_read": [ctypes.c_int, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(i32)],
     }
@@ -198,6 +200,13 @@ def mol_gap_bound(B: int, P: int, m: int, dots, k: int, scores, out_S, out_SK, o
                                 _ptr(out_bound), _ptr(out_looser), _stream(stream)))
 
 
+def mol_gap_bound_combined(B: int, P: int, m: int, dots, ids, kprime: int, avg_ids, k_avg: int, k: int,
+                           scores, out_S, out_SK, out_bound, stream=None) -> None:
+    _check(load().mol_gap_bound_combined(B, P, m, _ptr(dots), _ptr(ids), kprime, _ptr(avg_ids), k_avg, k,
+                                         _ptr(scores), _ptr(out_S), _ptr(out_SK), _ptr(out_bound),
+                                         _stream(stream)))
+
+
 def mol_timing_enable(on: bool) -> None:
     _check(load().mol_timing_enable(1 if on else 0))
 
@@ -291,6 +300,19 @@ def gap_bound(dots: torch.Tensor, scores: torch.Tensor, stream=None):
     k = scores.shape[1]
     outs = [torch.empty((B,), dtype=torch.float32, device=dots.device) for _ in range(4)]
     mol_gap_bound(B, P, m, dots, k, scores, *outs, stream=stream)
+    return tuple(outs)
+
+
+def gap_bound_combined(dots: torch.Tensor, ids: torch.Tensor, kprime: int, avg_ids, scores: torch.Tensor,
+                       stream=None):
+    """Theorem 3 certificate from per-component lists dots / ids [B][P][m]
+    (m > kprime + k_avg), the TopKAvg ids [B][k_avg] (or None) and the
+    reranked scores [B][k]: (S', S_K, bound), each float32 [B]."""
+    B, P, m = dots.shape
+    k = scores.shape[1]
+    k_avg = 0 if avg_ids is None else avg_ids.shape[-1]
+    outs = [torch.empty((B,), dtype=torch.float32, device=dots.device) for _ in range(3)]
+    mol_gap_bound_combined(B, P, m, dots, ids, kprime, avg_ids, k_avg, k, scores, *outs, stream=stream)
     return tuple(outs)
 
 

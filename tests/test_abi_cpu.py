@@ -175,3 +175,24 @@ def test_two_pass_bounded_and_maxdot_validation():
     assert lib.mol_topk_maxdot(ctypes.byref(bare), 10, 256, 256, ws, 16, None) == mol.MOL_EWORKSPACE
     assert lib.mol_topk_maxdot(ctypes.byref(bare), 100001, 256, 256, ws, big, None) == mol.MOL_EINVAL
     assert lib.mol_topk_maxdot(ctypes.byref(bare), 10, None, 256, ws, big, None) == mol.MOL_EINVAL
+
+
+def test_combined_gap_bound_validation():
+    lib = mol.load()
+    ok = (4, 8, 40, 256, 256, 10, 256, 20, 5, 256, None, None, None, None)
+    args = list(ok)
+    # lists must hold more than kprime + k_avg entries
+    args[2] = 30
+    assert lib.mol_gap_bound_combined(*args) == mol.MOL_EINVAL
+    args = list(ok)
+    args[6] = None                     # avg_ids NULL with k_avg > 0
+    assert lib.mol_gap_bound_combined(*args) == mol.MOL_EINVAL
+    args = list(ok)
+    args[1] = 65                       # P > 64
+    assert lib.mol_gap_bound_combined(*args) == mol.MOL_EINVAL
+    args = list(ok)
+    args[8] = 0                        # k < 1
+    assert lib.mol_gap_bound_combined(*args) == mol.MOL_EINVAL
+    args = list(ok)
+    args[3] = None                     # dots NULL
+    assert lib.mol_gap_bound_combined(*args) == mol.MOL_EINVAL

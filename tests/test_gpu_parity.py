@@ -242,6 +242,51 @@ def test_gap_certificate_theorem2():
         log(f"[gap] b={b} S={S[b]:.5f} S_K={SK[b]:.5f} bound={bound[b]:.5f} gap={g:.5f}")
 
 
+def test_gap_certificate_theorem3_combined():
+    """Theorem 3: S' = the largest s_p over items outside (X_{k',p} U X'_K)
+    bounds every non-candidate's MoL score, so S' - S_K bounds the gap of the
+    combined heuristic.  S' is checked against a brute force over all items
+    with the GPU's own candidate sets."""
+    spec = W["hybrid_8m"].scaled(B=4, N=6007, clusters=16)
+    kp, kavg, k = 16, 40, 20
+    inp = cuda_inputs(spec, seed=30)
+    prob = mol.Problem.from_inputs(inp)
+    m = kp + kavg + 1
+    dots, ids = mol.topk_per_embd(mol.Problem(inp.Q, inp.X), m)
+    q, x = mol.avg_embed(prob)
+    _, avg_ids = mol.topk_per_embd(mol.averaged_problem(prob, q, x), kavg)
+    avg_ids = avg_ids.view(spec.B, kavg)
+    cand = ids[:, :, :kp].contiguous().view(spec.B, -1)
+    rs, ri, nu = mol.rerank(prob, cand, k, cand2=avg_ids)
+    S, SK, bound = mol.gap_bound_combined(dots, ids, kp, avg_ids, rs)
+    # with no averaged candidates it is Theorem 2's bound from (k'+1)-th values
+    S2, _, _ = mol.gap_bound_combined(dots, ids, kp, None, rs)
+    torch.cuda.synchronize()
+    op = oracle_problem(inp)
+    ids_np, avg_np, cand_np = ids.cpu().numpy(), avg_ids.cpu().numpy(), cand.cpu().numpy()
+    dots_np, ri = dots.cpu().numpy(), ri.cpu().numpy()
+    S, SK, bound, S2 = (t.cpu().numpy() for t in (S, SK, bound, S2))
+    for b in range(spec.B):
+        s_all = mo.all_dots(op, b)
+        S_want = -np.inf
+        for p in range(spec.P):
+            keep = np.ones(spec.N, dtype=bool)
+            keep[ids_np[b, p, :kp]] = False
+            keep[avg_np[b]] = False
+            S_want = max(S_want, s_all[keep, p].max())
+        assert abs(S[b] - S_want) <= TAU, f"b={b}: S' {S[b]} vs brute force {S_want}"
+        assert S2[b] == dots_np[b, :, kp].max()
+        uniq = mo.union_dedup([cand_np[b], avg_np[b]])
+        _, _, phi_c = mo.mol_terms(op, b, uniq)
+        assert abs(SK[b] - mo.kth_largest(phi_c, k)) <= TAU
+        phi_all = mo.mol_scores(op, [b])[0]
+        outside = np.setdiff1d(np.arange(spec.N), uniq)
+        assert phi_all[outside].max() <= S_want + 1e-12      # the theorem's premise
+        g = mo.gap(phi_all, ri[b], k)
+        assert g <= bound[b] + TAU, f"b={b}: gap {g} above the bound {bound[b]}"
+        log(f"[gap3] b={b} S'={S[b]:.5f} S_K={SK[b]:.5f} bound={bound[b]:.5f} gap={g:.5f}")
+
+
 @pytest.mark.parametrize("C,k", [(700, 100), (64, 100), (4096, 100)])
 def test_rerank_matches_oracle(C, k):
     spec = W["exact_1m"].scaled(B=7, N=3000, clusters=32)
