@@ -76,6 +76,7 @@ typedef enum {
 } mol_two_pass_mode;
 
 /* Limits of the kernel set. */
+#define MOL_MAX_B 65535   /* queries per call                                */
 #define MOL_MAX_P 64      /* Pq * Px                                        */
 #define MOL_MAX_H 256     /* gating MLP hidden width                         */
 #define MOL_MAX_D 1024    /* component embedding width                       */

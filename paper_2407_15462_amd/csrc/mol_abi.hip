@@ -108,6 +108,7 @@ int check_problem(const mol_problem* p, bool gating) {
     return fail(MOL_EINVAL, "sizes must be positive (B=%d N=%d Pq=%d Px=%d d=%d)", p->B, p->N,
                 p->Pq, p->Px, p->d);
   if (gating && p->H < 1) return fail(MOL_EINVAL, "H must be positive (H=%d)", p->H);
+  if (p->B > MOL_MAX_B) return fail(MOL_EUNSUPPORTED, "B = %d exceeds %d", p->B, MOL_MAX_B);
   if (p->dtype != MOL_F32 && p->dtype != MOL_BF16)
     return fail(MOL_EUNSUPPORTED, "dtype %d is not MOL_F32 or MOL_BF16", p->dtype);
   if (p->Pq > MOL_MAX_P || p->Px > MOL_MAX_P || p->Pq * p->Px > MOL_MAX_P)

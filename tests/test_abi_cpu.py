@@ -56,6 +56,7 @@ def test_status_strings_and_last_error():
     ("H", 0, mol.MOL_EINVAL), ("Pq", 40, mol.MOL_EUNSUPPORTED), ("d", 4096, mol.MOL_EUNSUPPORTED),
     ("H", 1000, mol.MOL_EUNSUPPORTED), ("dtype", 7, mol.MOL_EUNSUPPORTED),
     ("Q", None, mol.MOL_EINVAL), ("a_x", None, mol.MOL_EINVAL), ("W2", None, mol.MOL_EINVAL),
+    ("B", 65536, mol.MOL_EUNSUPPORTED),
 ])
 def test_problem_validation(field, value, status):
     rc, _ = _ws(_problem(**{field: value}), mol.MOL_OP_TOPK_EXACT, k=5)
