@@ -343,7 +343,8 @@ bool fused_maxdot_supported(const DevProb& pr, int k) {
 void fused_grid(const DevProb& pr, int n_count, int& R, int& range_len, int& G) {
   G = (pr.B + kQueriesPerWG - 1) / kQueriesPerWG;
   R = std::max(1, 256 / G);
-  const int max_r = std::max(1, n_count / 512);
+  // ranges of at least 128 items (4 tiles): small corpora still fill the chip
+  const int max_r = std::max(1, n_count / 128);
   R = std::min(R, max_r);
   range_len = (n_count + R - 1) / R;
   range_len = (range_len + kTile - 1) / kTile * kTile;

@@ -429,8 +429,9 @@ static void scan_grid(const DevProb& pr, int kp, bool scan2, PerEmbdGrid::Scan& 
   const int vec_wg = waves_for(per_embd_list_cap(kp)) * 32 * nb_for(pr.d, scan2);
   sc.G = (nvec + vec_wg - 1) / vec_wg;
   const int units = sc.G * pr.Px;
+  // about one workgroup per CU, with ranges of at least 512 items
   int R = std::max(1, (256 + units - 1) / units);
-  R = std::min(R, std::max(1, pr.N / 4096));
+  R = std::min(R, std::max(1, pr.N / 512));
   sc.range_len = (pr.N + R - 1) / R;
   sc.range_len = (sc.range_len + 127) / 128 * 128;
   sc.R = (pr.N + sc.range_len - 1) / sc.range_len;
