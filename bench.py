@@ -227,8 +227,10 @@ def main():
     if ms["exact"]:
         t = ms["exact"] / 1e3
         tk = kern[mol.MOL_OP_TOPK_EXACT] / 1e3
+        # the dots-only share of the work (2 P d of the 2 P d + 4 P H flop)
         out["exact"] = {"ms": ms["exact"], "kernel_ms": tk * 1e3, "queries_per_s": B / t,
-                        "items_scored_per_s": B * N / t}
+                        "items_scored_per_s": B * N / t,
+                        "mfma_frac_dots_only": B * N * 2.0 * P * d / tk / 1e12 / PEAK_BF16_TFLOPS}
         # algorithmic work of one launch: every (query, item) pair once,
         # 2 P d flops of component dots + 4 P H of the gating MLP
         ach = B * N * flops_pair / tk / 1e12
@@ -248,14 +250,21 @@ def main():
         # both scans of every per-component (and TopKAvg) list, per step
         tpe = kern_step[mol.MOL_OP_TOPK_PER_EMBD] / 1e3
         pe_flops = 2.0 * B * P * N * d + (2.0 * B * N * d if k_avg else 0.0)
+        # rerank: every unique candidate's P_x d bf16 components and P
+        # float32 item logits gathered once
+        uniq_total = float(rr_n.float().sum().item())
+        trr = kern[mol.MOL_OP_RERANK] / 1e3
         out["approx"] = {"ms_per_embd": ms["per_embd"], "ms_topk_avg": ms["topk_avg"] if k_avg else None,
                          "k_avg": k_avg or None, "ms_rerank": ms["rerank"],
                          "kernel_ms_per_embd_per_step": tpe * 1e3,
                          "kernel_ms_rerank": kern[mol.MOL_OP_RERANK],
                          "per_embd_mfma_frac": pe_flops / tpe / 1e12 / PEAK_BF16_TFLOPS,
+                         "reranked_pairs_per_s": uniq_total / trr,
+                         "rerank_gather_hbm_frac": uniq_total * (spec.Px * d * 2 + P * 4) / trr / 1e9
+                         / PEAK_HBM_GBS,
                          "queries_per_s": B / t,
                          "recall_at_100_vs_exact": recall,
-                         "candidates_per_query_mean": float(rr_n.float().mean().item())}
+                         "candidates_per_query_mean": uniq_total / B}
 
     if not args.no_cpu_baseline:
         nq = args.cpu_baseline_queries or max(1, (8 << 20) // spec.N)
