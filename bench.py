@@ -411,10 +411,19 @@ def cpu_baseline(inp, spec, nq):
         t0 = time.perf_counter()
         mo.exact_topk(op, list(range(nq)), spec.k)
         dt = time.perf_counter() - t0
+    model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
     return {"value": nq / dt, "unit": "queries/s", "cores": cores, "kind": "oracle",
             "sample": f"exact top-{spec.k} for {nq} of {spec.B} queries over all "
                       f"{spec.N} items (FP64 NumPy, BLAS threads={cores})",
-            "seconds": dt}
+            "seconds": dt, "host_cpus": os.cpu_count(), "cpu_model": model}
 
 
 if __name__ == "__main__":
