@@ -15,9 +15,10 @@ With --workload paper_ml20m / paper_books / paper_nq320k (the item counts,
 component counts and widths of the paper's top-K benchmark, 32 queries per
 call) it times each method row of the paper's table instead -- brute force,
 TopKPerEmbd(N), TopKAvg(N), CombTopK(N1, N2) -- plus the two-pass exact
-algorithm and the max-component heuristic: mean and standard deviation of the
-call latency over --steps warm runs (HIP events on the stream), and
-recall@100 against the brute-force result.
+algorithm and the max-component heuristic: mean, standard deviation and
+median of the call latency over --steps warm runs (HIP events on the
+stream), the mean latency of the same calls captured once into a HIP graph
+and replayed, and recall@100 against the brute-force result.
 Inputs are synthetic, seeded, and resident in HBM before timing starts.
 Prints one JSON line.
 """
@@ -352,6 +353,44 @@ def paper_table(spec, args):
         mol.mol_rerank(prob, mx_i, mx_n, None, 0, k, rr_s, rr_i, rr_n, ws_mr)
     rows.append((f"MaxTopK({mx_n})", maxdot_rerank))
 
+    def timed(run):
+        times = []
+        for _ in range(args.steps):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            run()
+            e1.record()
+            times.append((e0, e1))
+        torch.cuda.synchronize()
+        return [a.elapsed_time(b) for a, b in times]
+
+    def graph_latency(fn, outs):
+        """The method captured once into a HIP graph and replayed: mean
+        latency over --steps replays.  Every replay of a first batch is
+        checked against the eager outputs, with the outputs overwritten by
+        eager work in between."""
+        want = [t.clone() for t in outs]
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            fn()
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            fn()
+        for _ in range(3):
+            for t in outs:
+                t.fill_(-7)
+            torch.cuda.synchronize()
+            g.replay()
+            torch.cuda.synchronize()
+            for t, w in zip(outs, want):
+                if not torch.equal(t, w):
+                    raise RuntimeError("graph replay differs from the eager result")
+        ms = timed(g.replay)
+        return statistics.fmean(ms)
+
     # brute force first: its result is the recall reference of every row
     results = []
     exact_ids = None
@@ -362,27 +401,28 @@ def paper_table(spec, args):
         for _ in range(args.warmup):
             fn()
         torch.cuda.synchronize()
-        times = []
-        for _ in range(args.steps):
-            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            e0.record()
-            fn()
-            e1.record()
-            times.append((e0, e1))
-        torch.cuda.synchronize()
-        ms = [a.elapsed_time(b) for a, b in times]
-        got = (ex_i if label == "BruteForce" else tp_i if label.startswith("TwoPass") else rr_i).cpu()
+        ms = timed(fn)
+        outs = ((ex_s, ex_i) if label == "BruteForce" else (tp_s, tp_i) if label.startswith("TwoPass")
+                else (rr_s, rr_i))
+        got = outs[1].cpu()
         if exact_ids is None:
             exact_ids = got.clone()
         hits = sum(len(set(a.tolist()) & set(b.tolist())) for a, b in zip(got, exact_ids))
         mean = statistics.fmean(ms)
+        try:
+            graph_ms = graph_latency(fn, outs)
+        except RuntimeError as e:          # capture refused or replay mismatch: report, go on
+            graph_ms = None
+            print(f"# {label}: no graph latency ({e})", file=sys.stderr, flush=True)
         results.append({"method": label, "latency_ms": mean,
                         "latency_std_ms": statistics.stdev(ms) if len(ms) > 1 else 0.0,
+                        "latency_median_ms": statistics.median(ms),
+                        "graph_latency_ms": graph_ms,
                         "queries_per_s": B / (mean / 1e3),
                         "recall_at_100_vs_exact": hits / exact_ids.numel(),
                         "candidates_per_query_mean": None if label in ("BruteForce",) or
                         label.startswith("TwoPass") else float(rr_n.float().mean().item())})
-        print(f"# {label}: {mean:.3f} ms", file=sys.stderr, flush=True)
+        print(f"# {label}: {mean:.3f} ms (graph replay {graph_ms})", file=sys.stderr, flush=True)
     bf = results[0]["latency_ms"]
     print(json.dumps({
         "metric": "MoL top-100 latency per batch of 32 queries, paper top-K table shapes",

@@ -40,6 +40,10 @@ typedef float f32x16_t __attribute__((ext_vector_type(16)));
 // tiles' accumulators stay in registers: 4 in the bucket scan at d = 64,
 // 2 otherwise (the threshold scan also keeps staging state)
 constexpr int nb_for(int d, bool scan2) { return (d >= 128 || scan2) ? 2 : 4; }
+// small batches (at most 256 query vectors) use one block per wave, so that
+// no wave multiplies empty vector slots
+constexpr int kSmallVectors = 256;
+constexpr int nb_pick(int d, bool scan2, bool small) { return small ? 1 : nb_for(d, scan2); }
 // waves per workgroup: 8, or 4 for lists of 512 / 1024 keys, whose merge
 // sorts need 8 / 16 KB of LDS per wave
 constexpr int waves_for(int kl) { return kl >= 512 ? 4 : 8; }
@@ -52,10 +56,10 @@ __device__ __forceinline__ f32x16_t mfma32_bf16(uint4 a, uint4 b, f32x16_t c) {
                                                  __builtin_bit_cast(bf16x8_t, b), c, 0, 0, 0);
 }
 
-template <int D, int KL, bool SCAN2>
+template <int D, int KL, bool SCAN2, bool SMALL>
 struct EmbdShape {
   static constexpr int KD = D / 16;                    // K blocks (32x32x16)
-  static constexpr int NB = nb_for(D, SCAN2);
+  static constexpr int NB = nb_pick(D, SCAN2, SMALL);
   static constexpr int VEC_WAVE = 32 * NB;             // query vectors per wave
   static constexpr int WAVES = waves_for(KL);
   static constexpr int VEC_WG = WAVES * VEC_WAVE;
@@ -85,12 +89,12 @@ struct EmbdShape {
 // bmax: [nvec * Px][R][2][nbk] bucket maxima (scan 1 writes, scan 2 unused);
 // thr: [nvec * Px] starting thresholds (scan 2 reads);
 // lists: [nvec * Px][R][KL] keys; stg: [nvec * Px][R][2][SG] keys (scan 2).
-template <int D, int KL, bool SCAN2>
+template <int D, int KL, bool SCAN2, bool SMALL>
 __global__ __launch_bounds__(64 * waves_for(KL), 1) void k_topk_per_embd(
     DevProb pr, int kp, int R, int range_len, int G, int bucket_tiles, int nbk,
     float* __restrict__ bmax, const float* __restrict__ thr, uint64_t* __restrict__ lists,
     uint64_t* __restrict__ stg) {
-  using S = EmbdShape<D, KL, SCAN2>;
+  using S = EmbdShape<D, KL, SCAN2, SMALL>;
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   unsigned char* sX = smem;
   uint64_t* sSort = reinterpret_cast<uint64_t*>(smem + S::LDS_X);
@@ -411,6 +415,11 @@ __global__ __launch_bounds__(256) void k_bucket_threshold(const float* __restric
 }
 
 // ---------------------------------------------------------------------------
+// small-batch form (one 32-vector block per wave): lists of up to 256 keys
+bool per_embd_small(const DevProb& pr, int kp) {
+  return pr.B * pr.Pq <= kSmallVectors && per_embd_list_cap(kp) <= 256;
+}
+
 bool per_embd_supported(const DevProb& pr, int kp) {
   if (pr.dtype != MOL_BF16) return false;
   if (pr.d != 32 && pr.d != 64 && pr.d != 128) return false;
@@ -426,7 +435,7 @@ int per_embd_stage_cap(int kp) {
 
 static void scan_grid(const DevProb& pr, int kp, bool scan2, PerEmbdGrid::Scan& sc) {
   const int nvec = pr.B * pr.Pq;
-  const int vec_wg = waves_for(per_embd_list_cap(kp)) * 32 * nb_for(pr.d, scan2);
+  const int vec_wg = waves_for(per_embd_list_cap(kp)) * 32 * nb_pick(pr.d, scan2, per_embd_small(pr, kp));
   sc.G = (nvec + vec_wg - 1) / vec_wg;
   const int units = sc.G * pr.Px;
   // about one workgroup per CU, with ranges of at least 512 items
@@ -450,12 +459,12 @@ void per_embd_grid(const DevProb& pr, int kp, PerEmbdGrid& g) {
   }
 }
 
-template <int D, int KL, bool SCAN2>
+template <int D, int KL, bool SCAN2, bool SMALL>
 static hipError_t launch_pe_t(const DevProb& pr, int kp, const PerEmbdGrid& g, float* bmax, const float* thr,
                               uint64_t* lists, uint64_t* stg, hipStream_t st) {
-  using S = EmbdShape<D, KL, SCAN2>;
+  using S = EmbdShape<D, KL, SCAN2, SMALL>;
   const PerEmbdGrid::Scan& sc = SCAN2 ? g.s2 : g.s1;
-  auto kern = &k_topk_per_embd<D, KL, SCAN2>;
+  auto kern = &k_topk_per_embd<D, KL, SCAN2, SMALL>;
   hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                      hipFuncAttributeMaxDynamicSharedMemorySize, S::LDS_TOTAL);
   if (e != hipSuccess) return e;
@@ -464,17 +473,26 @@ static hipError_t launch_pe_t(const DevProb& pr, int kp, const PerEmbdGrid& g, f
   return hipGetLastError();
 }
 
-template <int D, int KL>
-static hipError_t launch_pe_d(const DevProb& pr, int kp, const PerEmbdGrid& g, float* bmax, float* thr,
+template <int D, int KL, bool SMALL>
+static hipError_t launch_pe_s(const DevProb& pr, int kp, const PerEmbdGrid& g, float* bmax, float* thr,
                               uint64_t* lists, uint64_t* stg, hipStream_t st) {
-  hipError_t e = launch_pe_t<D, KL, false>(pr, kp, g, bmax, thr, lists, stg, st);
+  hipError_t e = launch_pe_t<D, KL, false, SMALL>(pr, kp, g, bmax, thr, lists, stg, st);
   if (e != hipSuccess) return e;
   const int nlists = pr.B * pr.Pq * pr.Px;
   hipLaunchKernelGGL(k_bucket_threshold, dim3((nlists + 3) / 4), dim3(256), 0, st, bmax, nlists,
                      2 * g.s1.R * g.nbk, kp, thr);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  return launch_pe_t<D, KL, true>(pr, kp, g, bmax, thr, lists, stg, st);
+  return launch_pe_t<D, KL, true, SMALL>(pr, kp, g, bmax, thr, lists, stg, st);
+}
+
+template <int D, int KL>
+static hipError_t launch_pe_d(const DevProb& pr, int kp, const PerEmbdGrid& g, float* bmax, float* thr,
+                              uint64_t* lists, uint64_t* stg, hipStream_t st) {
+  if constexpr (KL <= 256) {
+    if (per_embd_small(pr, kp)) return launch_pe_s<D, KL, true>(pr, kp, g, bmax, thr, lists, stg, st);
+  }
+  return launch_pe_s<D, KL, false>(pr, kp, g, bmax, thr, lists, stg, st);
 }
 
 hipError_t launch_per_embd(const DevProb& pr, int kp, const PerEmbdGrid& g, float* bmax, float* thr,
