@@ -64,6 +64,22 @@ def test_topk_exact_matches_oracle(name, spec):
         check_topk_row(want[b], i[b], s[b], k, f"{name} query {b}")
 
 
+@pytest.mark.parametrize("k", [1, 128, 129, 500])
+def test_topk_exact_k_boundaries(k):
+    """k = 1 and k = 128 stay on the fused kernel's running lists; k = 129
+    and 500 take the pair-wise path (MFMA dots + pair-wise gating kernel)."""
+    spec = W["exact_1m"].scaled(B=6, N=4099, clusters=32)
+    log(f"[topk_exact] k={k} B={spec.B} N={spec.N}")
+    inp = cuda_inputs(spec, seed=19)
+    prob = mol.Problem.from_inputs(inp)
+    s, i = mol.topk_exact(prob, k)
+    torch.cuda.synchronize()
+    want = mo.mol_scores(oracle_problem(inp), list(range(spec.B)))
+    s, i = s.cpu().numpy(), i.cpu().numpy()
+    for b in range(spec.B):
+        check_topk_row(want[b], i[b], s[b], k, f"k_boundary k={k} query {b}")
+
+
 def test_topk_exact_full_32k_workload():
     spec = W["exact_32k"]
     log(f"[topk_exact] exact_32k full B={spec.B} N={spec.N}")
