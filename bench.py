@@ -204,7 +204,12 @@ def main():
     wall = time.perf_counter() - t_start
     mol.mol_timing_enable(False)
     ms_step = 1e3 * wall / args.steps
-    ms = {p: (sum(a.elapsed_time(b) for a, b in v) / len(v) if v else None) for p, v in seg.items()}
+    import statistics
+    seg_ms = {p: [a.elapsed_time(b) for a, b in v] for p, v in seg.items()}
+    ms = {p: (statistics.fmean(v) if v else None) for p, v in seg_ms.items()}
+
+    def spread(v):
+        return {"median": statistics.median(v), "std": statistics.stdev(v) if len(v) > 1 else 0.0}
     kern = {}          # main-kernel milliseconds per launch
     kern_step = {}     # main-kernel milliseconds per step (all launches of the op)
     for op in timed_ops:
@@ -229,7 +234,8 @@ def main():
         t = ms["exact"] / 1e3
         tk = kern[mol.MOL_OP_TOPK_EXACT] / 1e3
         # the dots-only share of the work (2 P d of the 2 P d + 4 P H flop)
-        out["exact"] = {"ms": ms["exact"], "kernel_ms": tk * 1e3, "queries_per_s": B / t,
+        out["exact"] = {"ms": ms["exact"], "ms_spread": spread(seg_ms["exact"]), "kernel_ms": tk * 1e3,
+                        "queries_per_s": B / t,
                         "items_scored_per_s": B * N / t,
                         "mfma_frac_dots_only": B * N * 2.0 * P * d / tk / 1e12 / PEAK_BF16_TFLOPS}
         # algorithmic work of one launch: every (query, item) pair once,
@@ -255,7 +261,9 @@ def main():
         # float32 item logits gathered once
         uniq_total = float(rr_n.float().sum().item())
         trr = kern[mol.MOL_OP_RERANK] / 1e3
-        out["approx"] = {"ms_per_embd": ms["per_embd"], "ms_topk_avg": ms["topk_avg"] if k_avg else None,
+        approx_ms = [a + b + c for a, b, c in zip(seg_ms["per_embd"], seg_ms["topk_avg"], seg_ms["rerank"])]
+        out["approx"] = {"ms": statistics.fmean(approx_ms), "ms_spread": spread(approx_ms),
+                         "ms_per_embd": ms["per_embd"], "ms_topk_avg": ms["topk_avg"] if k_avg else None,
                          "k_avg": k_avg or None, "ms_rerank": ms["rerank"],
                          "kernel_ms_per_embd_per_step": tpe * 1e3,
                          "kernel_ms_rerank": kern[mol.MOL_OP_RERANK],
