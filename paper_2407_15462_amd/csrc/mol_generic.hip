@@ -10,8 +10,11 @@ namespace mol {
 
 // ---------------------------------------------------------------------------
 // MoL score of one (query, item) pair, float32 (Eq. 1 with the two-layer
-// SiLU gating MLP of Appendix A.3).  Gating weights live in LDS as float32:
-// sW1 [H][P], sW2 [P][H], sb1 [H], sc [P] = a_q[b] + b2.
+// SiLU gating MLP of Appendix A.3).  Gating weights live in LDS as float32,
+// rows padded with zeros to PMAX so that a row is read as aligned 16-byte
+// vectors (every lane reads the same address: one broadcast per read):
+// sW1 [H][PMAX] = W1, sW2t [H][PMAX] = W2 transposed, sb1 [H],
+// sc [PMAX] = a_q[b] + b2.
 // ---------------------------------------------------------------------------
 template <typename T, int PMAX>
 __device__ __forceinline__ void pair_dots(const DevProb& pr, int b, long n, float (&s)[PMAX]) {
@@ -34,21 +37,23 @@ __device__ __forceinline__ void pair_dots(const DevProb& pr, int b, long n, floa
 
 template <int PMAX>
 __device__ __forceinline__ float pair_phi(const DevProb& pr, long n, const float (&s)[PMAX],
-                                          const float* sW1, const float* sW2,
+                                          const float* sW1, const float* sW2t,
                                           const float* sb1, const float* sc) {
+  constexpr float kLog2e = 1.4426950408889634f;
   const int P = pr.P, H = pr.H;
   float l[PMAX];
 #pragma unroll
   for (int p = 0; p < PMAX; ++p) l[p] = (p < P) ? sc[p] + pr.a_x[n * P + p] : 0.f;
   for (int j = 0; j < H; ++j) {
+    const float* w1 = sW1 + j * PMAX;
+    const float* w2 = sW2t + j * PMAX;
     float u = sb1[j];
 #pragma unroll
-    for (int p = 0; p < PMAX; ++p)
-      if (p < P) u = fmaf(sW1[j * P + p], s[p], u);
-    const float h = u / (1.f + expf(-u));
+    for (int p = 0; p < PMAX; ++p) u = fmaf(w1[p], s[p], u);   // padded slots are zero
+    // SiLU: u sigma(u), sigma(u) = 1 / (1 + e^-u)
+    const float h = u * __builtin_amdgcn_rcpf(1.f + __builtin_amdgcn_exp2f(-kLog2e * u));
 #pragma unroll
-    for (int p = 0; p < PMAX; ++p)
-      if (p < P) l[p] = fmaf(sW2[p * H + j], h, l[p]);
+    for (int p = 0; p < PMAX; ++p) l[p] = fmaf(w2[p], h, l[p]);
   }
   float m = l[0];
 #pragma unroll
@@ -58,12 +63,12 @@ __device__ __forceinline__ float pair_phi(const DevProb& pr, long n, const float
 #pragma unroll
   for (int p = 0; p < PMAX; ++p) {
     if (p < P) {
-      const float w = expf(l[p] - m);
+      const float w = __builtin_amdgcn_exp2f(kLog2e * (l[p] - m));
       den += w;
       num = fmaf(w, s[p], num);
     }
   }
-  return num / den;
+  return num * __builtin_amdgcn_rcpf(den);
 }
 
 // Grid: x over items (256 per block), y over queries.  Items are either the
@@ -86,17 +91,19 @@ __global__ __launch_bounds__(256) void k_phi_generic(
   extern __shared__ float smem[];
   const int P = pr.P, H = pr.H;
   float* sW1 = smem;
-  float* sW2 = sW1 + H * P;
-  float* sb1 = sW2 + P * H;
+  float* sW2t = sW1 + H * PMAX;
+  float* sb1 = sW2t + H * PMAX;
   float* sc = sb1 + H;
   const int b = blockIdx.y;
   if (mode != kGenMaxDot) {
-    for (int i = threadIdx.x; i < H * P; i += blockDim.x) {
-      sW1[i] = to_f32(static_cast<const T*>(pr.W1)[i]);
-      sW2[i] = to_f32(static_cast<const T*>(pr.W2)[i]);
+    for (int i = threadIdx.x; i < H * PMAX; i += blockDim.x) {
+      const int j = i / PMAX, p = i - (i / PMAX) * PMAX;
+      sW1[i] = p < P ? to_f32(static_cast<const T*>(pr.W1)[j * P + p]) : 0.f;
+      sW2t[i] = p < P ? to_f32(static_cast<const T*>(pr.W2)[p * H + j]) : 0.f;
     }
     for (int i = threadIdx.x; i < H; i += blockDim.x) sb1[i] = pr.b1[i];
-    for (int i = threadIdx.x; i < P; i += blockDim.x) sc[i] = pr.a_q[static_cast<long>(b) * P + i] + pr.b2[i];
+    for (int i = threadIdx.x; i < PMAX; i += blockDim.x)
+      sc[i] = i < P ? pr.a_q[static_cast<long>(b) * P + i] + pr.b2[i] : 0.f;
   }
   __syncthreads();
 
@@ -131,10 +138,10 @@ __global__ __launch_bounds__(256) void k_phi_generic(
       if (keys) keys[b * key_stride + i] = 0;
       return;
     } else {
-      v = pair_phi<PMAX>(pr, n, s, sW1, sW2, sb1, sc);
+      v = pair_phi<PMAX>(pr, n, s, sW1, sW2t, sb1, sc);
     }
   } else {
-    v = pair_phi<PMAX>(pr, n, s, sW1, sW2, sb1, sc);
+    v = pair_phi<PMAX>(pr, n, s, sW1, sW2t, sb1, sc);
     if (mode == kGenNegPhi) v = -v;
   }
   if (phi) phi[b * phi_stride + i] = v;
@@ -399,8 +406,8 @@ __global__ void k_avg_embed(const T* __restrict__ in, long sc, long sm, int ncom
 // ---------------------------------------------------------------------------
 // Host-side launchers.
 // ---------------------------------------------------------------------------
-static size_t phi_smem_bytes(const DevProb& pr) {
-  return sizeof(float) * (2 * static_cast<size_t>(pr.H) * pr.P + pr.H + pr.P);
+static size_t phi_smem_bytes(const DevProb& pr, int pmax) {
+  return sizeof(float) * (2 * static_cast<size_t>(pr.H) * pmax + pr.H + pmax);
 }
 
 template <typename T, int PMAX>
@@ -409,7 +416,7 @@ static hipError_t launch_phi_t(const DevProb& pr, int mode, const float* bound, 
                                const float* sbuf, long s_pstride, long s_bstride,
                                float* phi, long phi_stride, uint64_t* keys, long key_stride,
                                hipStream_t st) {
-  const size_t smem = mode == kGenMaxDot ? 0 : phi_smem_bytes(pr);
+  const size_t smem = mode == kGenMaxDot ? 0 : phi_smem_bytes(pr, PMAX);
   if (smem > 65536) {
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_phi_generic<T, PMAX>),
                                        hipFuncAttributeMaxDynamicSharedMemorySize,
