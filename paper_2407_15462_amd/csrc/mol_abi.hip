@@ -192,8 +192,8 @@ hipError_t pairwise_tile(const DevProb& pr, const StreamPlan& s, char* w, int mo
   const long pstride = s.sRow * pr.B;
   hipError_t e = launch_dots_mfma(pr, n0, nt, kDotsToBuffer, sbuf, pstride, s.sRow, nullptr, 0, st);
   if (e != hipSuccess) return e;
-  return launch_phi_generic(pr, mode, bound, n0, nt, nullptr, nullptr, 0, sbuf, pstride, s.sRow, nullptr, 0, A,
-                            strideA, st);
+  return (phi_mfma_supported(pr) ? launch_phi_mfma : launch_phi_generic)(
+      pr, mode, bound, n0, nt, nullptr, nullptr, 0, sbuf, pstride, s.sRow, nullptr, 0, A, strideA, st);
 }
 
 // Reduce rows of `len` keys held in buffer A (stride strideA) to the top k,
@@ -500,8 +500,9 @@ int run_rerank(const DevProb& pr, const int32_t* cand, int C, const int32_t* can
     if (sbuf)
       MOL_TRY_HIP(launch_dots_mfma_gather(pr, uniq, nu, CT, CT, sbuf, pstride, r.sRow, st), "rerank dots");
     MOL_TIMED_LAUNCH(timed_op, st,
-                     launch_phi_generic(pr, negate ? kGenNegPhi : kGenPhi, nullptr, 0, CT, uniq, nu, CT,
-                                        sbuf, pstride, r.sRow, nullptr, 0, A, r.s.strideA, st),
+                     (sbuf && phi_mfma_supported(pr) ? launch_phi_mfma : launch_phi_generic)(
+                         pr, negate ? kGenNegPhi : kGenPhi, nullptr, 0, CT, uniq, nu, CT, sbuf, pstride,
+                         r.sRow, nullptr, 0, A, r.s.strideA, st),
                      "rerank score");
     if ((rc = reduce_rows(r.s, w, CT, fin, k, st))) return rc;
   }

@@ -3,13 +3,13 @@
 // (any P_q, P_x <= 64, d a multiple of 32 up to 1024, bf16): the first step
 // of Eq. 1 / Eq. 2 as a plain GEMM, S_px = X_px Q^T per item component px.
 //
-// Workgroup: 4 waves on a 64-item x 64-vector output tile, each wave one
-// 32 x 32 block on 32x32x16 bf16 MFMAs.  The K dimension (d) is walked 32 at
-// a time through double-buffered LDS tiles [64 rows][32 K] whose 16-byte
-// chunks are XOR-swizzled by row so that a 16-lane group's 16 rows read
-// distinct bank slots.  In the result D[item][vector] lane (c = lane % 32,
-// h = lane / 32) holds vector c's dot products with items 8 j + 4 h + i
-// (j, i < 4): four runs of 4 consecutive items.
+// Workgroup: 4 waves on a 128-item x 64-vector output tile, each wave two
+// 32 x 32 blocks (64 items x 32 vectors) on 32x32x16 bf16 MFMAs.  The K
+// dimension (d) is walked 64 at a time through double-buffered LDS tiles
+// [rows][64 K] whose 16-byte chunks are XOR-swizzled by row.  In each block
+// D[item][vector] lane (c = lane % 32, h = lane / 32) holds vector c's dot
+// products with items 8 j + 4 h + i (j, i < 4): four runs of 4 consecutive
+// items.
 //
 // Gather form (items != NULL): block row y is query b and the tile's items
 // are b's candidates items[b * item_stride + i], i < item_count[b]; the
@@ -36,94 +36,143 @@ __device__ __forceinline__ f32x16_t mfma32x16_bf16(uint4 a, uint4 b, f32x16_t c)
                                                  __builtin_bit_cast(bf16x8_t, b), c, 0, 0, 0);
 }
 
-// physical 16-byte chunk of logical chunk ch in row r (rows of 4 chunks)
-__device__ __forceinline__ int dots_swz(int r, int ch) { return ch ^ ((r >> 2) & 3); }
+// physical 16-byte chunk of logical chunk ch in row r (rows of 8 chunks,
+// 128 B: two rows per 256 B of banks).  The 16 consecutive rows that one
+// 16-lane group reads at the same logical chunk land in 16 distinct 16-byte
+// bank slots: row parity picks the half, (r / 2) % 8 the slot within it.
+__device__ __forceinline__ int dots_swz8(int r, int ch) { return ch ^ ((r >> 1) & 7); }
 
 }  // namespace
 
-// Grid: x = 64-item tiles of [n0, n0 + nt), y = 64-vector tiles of the
-// B * P_q query vectors, z = item component px.
+// Grid: x = 128-item tiles of [n0, n0 + nt), y = 64-vector tiles of the
+// B * P_q query vectors (gather form: query b), z = item component px.
 template <int MODE>
 __global__ __launch_bounds__(256) void k_dots_mfma(DevProb pr, int n0, int nt, const int32_t* __restrict__ items,
                                                    const int32_t* __restrict__ item_count, long item_stride,
                                                    float* __restrict__ sbuf, long s_pstride, long s_bstride,
                                                    uint64_t* __restrict__ keys, long key_stride) {
-  __shared__ uint4 sA[2][64 * 4];   // items   [row][chunk], 4 KB per buffer
-  __shared__ uint4 sB[2][64 * 4];   // vectors [row][chunk]
+  constexpr int TI = 128, TV = 64, KS = 64, CH = KS / 8;   // tile items, vectors, K per step, chunks per row
+  // staging: items [2][TI][CH] (16 KB per buffer), then vectors [2][TV][CH]
+  // (8 KB per buffer); after the K loop the result tile [TV][TR] floats
+  constexpr int TR = TI + 4;
+  __shared__ uint4 smem[2 * TI * CH + 2 * TV * CH];
+  static_assert(TV * TR * 4 <= sizeof(smem), "result tile exceeds the staging area");
+  uint4* sA = smem;
+  uint4* sB = smem + 2 * TI * CH;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const bool gather = items != nullptr;
-  const int it0 = blockIdx.x * 64, px = blockIdx.z;
+  const int it0 = blockIdx.x * TI, px = blockIdx.z;
   // vectors of the tile: [v0, v1)
-  const int v0 = gather ? blockIdx.y * pr.Pq : blockIdx.y * 64;
+  const int v0 = gather ? blockIdx.y * pr.Pq : blockIdx.y * TV;
   const int v1 = gather ? v0 + pr.Pq : pr.B * pr.Pq;
   const int cnt = gather ? item_count[blockIdx.y] : nt;   // items of the row
   const int N = pr.N, D = pr.d;
   const bf16_t* X = static_cast<const bf16_t*>(pr.X);
   const bf16_t* Q = static_cast<const bf16_t*>(pr.Q);
 
-  // loader: thread t moves row t / 4, chunk t % 4 of both tiles
-  const int lr = tid >> 2, lc = tid & 3;
-  int item;
-  if (gather) {
-    // candidates past the count read item 0 (valid memory, never stored)
-    const int i = it0 + lr;
-    item = i < cnt ? items[blockIdx.y * item_stride + i] : 0;
-    item = min(max(item, 0), N - 1);
-  } else {
-    item = min(n0 + it0 + lr, N - 1);                // past the tile: a valid row, never stored
+  // loader: 4 item-row chunks and 2 vector-row chunks per thread and step
+  const bf16_t* xsrc[4];
+  int aslot[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int e = tid + 256 * i, r = e / CH, ch = e % CH;
+    int item;
+    if (gather) {
+      // candidates past the count read item 0 (valid memory, never stored)
+      const int pos = it0 + r;
+      item = pos < cnt ? items[blockIdx.y * item_stride + pos] : 0;
+      item = min(max(item, 0), N - 1);
+    } else {
+      item = min(n0 + it0 + r, N - 1);                // past the tile: a valid row, never stored
+    }
+    xsrc[i] = X + (static_cast<long>(px) * N + item) * D + 8 * ch;
+    aslot[i] = r * CH + dots_swz8(r, ch);
   }
-  const bool vok = v0 + lr < v1;
-  const bf16_t* xsrc = X + (static_cast<long>(px) * N + item) * D + 8 * lc;
-  const bf16_t* qsrc = Q + static_cast<long>(vok ? v0 + lr : 0) * D + 8 * lc;
-  const int lslot = lr * 4 + dots_swz(lr, lc);
+  const bf16_t* qsrc[2];
+  int bslot[2];
+  bool vok[2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int e = tid + 256 * i, r = e / CH, ch = e % CH;
+    vok[i] = v0 + r < v1;
+    qsrc[i] = Q + static_cast<long>(vok[i] ? v0 + r : 0) * D + 8 * ch;
+    bslot[i] = r * CH + dots_swz8(r, ch);
+  }
 
   const int c = lane & 31, h = lane >> 5;
-  const int wm = wave & 1, wn = wave >> 1;            // item half, vector half of the tile
-  const int ra = wm * 32 + c, rb = wn * 32 + c;       // A row (item), B row (vector)
-  f32x16_t acc = f32x16_t{};
+  const int wm = wave & 1, wn = wave >> 1;            // item half (64), vector half (32) of the tile
+  const int rb = wn * 32 + c;                         // B row (vector)
+  f32x16_t acc[2] = {f32x16_t{}, f32x16_t{}};
 
-  uint4 xa = *reinterpret_cast<const uint4*>(xsrc);
-  uint4 qb = vok ? *reinterpret_cast<const uint4*>(qsrc) : make_uint4(0, 0, 0, 0);
-  sA[0][lslot] = xa;
-  sB[0][lslot] = qb;
+  // every loader slot of a thread holds the same chunk (tid % 8); with d a
+  // multiple of 32 only, the upper half of the last K step reads zeros
+  const int kch = 8 * (tid % CH);
+  uint4 xa[4], qb[2];
+  auto load = [&](int k0) {
+    const bool kin = k0 + kch < D;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) xa[i] = kin ? *reinterpret_cast<const uint4*>(xsrc[i] + k0) : make_uint4(0, 0, 0, 0);
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+      qb[i] = kin && vok[i] ? *reinterpret_cast<const uint4*>(qsrc[i] + k0) : make_uint4(0, 0, 0, 0);
+  };
+  auto store = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) sA[buf * TI * CH + aslot[i]] = xa[i];
+#pragma unroll
+    for (int i = 0; i < 2; ++i) sB[buf * TV * CH + bslot[i]] = qb[i];
+  };
+  load(0);
+  store(0);
   __syncthreads();
-  const int nk = D / 32;
+  const int nk = (D + KS - 1) / KS;
   for (int kk = 0; kk < nk; ++kk) {
     const int cur = kk & 1;
     const bool more = kk + 1 < nk;
-    if (more) {
-      xa = *reinterpret_cast<const uint4*>(xsrc + 32 * (kk + 1));
-      qb = vok ? *reinterpret_cast<const uint4*>(qsrc + 32 * (kk + 1)) : make_uint4(0, 0, 0, 0);
-    }
+    if (more) load(KS * (kk + 1));
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {                  // two K blocks of 16
-      const uint4 a = sA[cur][ra * 4 + dots_swz(ra, 2 * kb + h)];
-      const uint4 b = sB[cur][rb * 4 + dots_swz(rb, 2 * kb + h)];
-      acc = mfma32x16_bf16(a, b, acc);
+    for (int kb = 0; kb < KS / 16; ++kb) {             // K blocks of 16
+      const uint4 b = sB[cur * TV * CH + rb * CH + dots_swz8(rb, 2 * kb + h)];
+#pragma unroll
+      for (int ib = 0; ib < 2; ++ib) {
+        const int ra = wm * 64 + ib * 32 + c;           // A row (item)
+        const uint4 a = sA[cur * TI * CH + ra * CH + dots_swz8(ra, 2 * kb + h)];
+        acc[ib] = mfma32x16_bf16(a, b, acc[ib]);
+      }
     }
-    if (more) {
-      sA[cur ^ 1][lslot] = xa;
-      sB[cur ^ 1][lslot] = qb;
-    }
+    if (more) store(cur ^ 1);
     __syncthreads();
   }
 
-  const int v = v0 + rb;
-  if (v >= v1) return;
-  const int b = v / pr.Pq, pq = v - (v / pr.Pq) * pr.Pq;
-  const int p = pq * pr.Px + px;
+  // The loop ended with a barrier: the staging area is free.  The tile goes
+  // through LDS (rows padded to TR floats) so that every global store
+  // instruction writes a contiguous run of one row.
+  float* sT = reinterpret_cast<float*>(smem);
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int i0 = it0 + wm * 32 + 8 * j + 4 * h;     // first of 4 consecutive items
+  for (int ib = 0; ib < 2; ++ib)
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      *reinterpret_cast<float4*>(sT + rb * TR + wm * 64 + ib * 32 + 8 * j + 4 * h) =
+          float4{acc[ib][4 * j + 0], acc[ib][4 * j + 1], acc[ib][4 * j + 2], acc[ib][4 * j + 3]};
+  __syncthreads();
+  // each wave writes 16 of the tile's vector rows
+  for (int rr = 0; rr < TV / 4; ++rr) {
+    const int r = wave * (TV / 4) + rr;
+    const int v = v0 + r;
+    if (v >= v1) break;                                // rows ascend: the rest are past the end too
+    const int b = v / pr.Pq, pq = v - (v / pr.Pq) * pr.Pq;
+    const int p = pq * pr.Px + px;
     if (MODE == kDotsToBuffer) {
-      // the buffer rows are padded to whole 64-item tiles
-      float4* dst = reinterpret_cast<float4*>(sbuf + p * s_pstride + b * s_bstride + i0);
-      *dst = float4{acc[4 * j + 0], acc[4 * j + 1], acc[4 * j + 2], acc[4 * j + 3]};
+      // the buffer rows are padded to whole 128-item tiles
+      const float2 val = *reinterpret_cast<const float2*>(sT + r * TR + 2 * lane);
+      *reinterpret_cast<float2*>(sbuf + p * s_pstride + b * s_bstride + it0 + 2 * lane) = val;
     } else {
       uint64_t* dst = keys + (static_cast<long>(b) * pr.P + p) * key_stride;
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
-        if (i0 + i < cnt) dst[i0 + i] = make_key(acc[4 * j + i], n0 + i0 + i);
+      for (int t = 0; t < 2; ++t) {
+        const int i = it0 + 64 * t + lane;
+        if (i < cnt) dst[i] = make_key(sT[r * TR + 64 * t + lane], n0 + i);
+      }
     }
   }
 }
@@ -132,13 +181,13 @@ bool dots_mfma_supported(const DevProb& pr) {
   return pr.dtype == MOL_BF16 && pr.d % 32 == 0 && pr.d <= MOL_MAX_D;
 }
 
-long dots_buffer_row(int nt) { return (static_cast<long>(nt) + 63) / 64 * 64; }
+long dots_buffer_row(int nt) { return (static_cast<long>(nt) + 127) / 128 * 128; }
 
 hipError_t launch_dots_mfma(const DevProb& pr, int n0, int nt, int mode, float* sbuf, long s_pstride,
                             long s_bstride, uint64_t* keys, long key_stride, hipStream_t st) {
   if (nt <= 0) return hipSuccess;
   const int nvec = pr.B * pr.Pq;
-  const dim3 grid((nt + 63) / 64, (nvec + 63) / 64, pr.Px);
+  const dim3 grid((nt + 127) / 128, (nvec + 63) / 64, pr.Px);
   if (mode == kDotsToBuffer)
     hipLaunchKernelGGL(k_dots_mfma<kDotsToBuffer>, grid, dim3(256), 0, st, pr, n0, nt, nullptr, nullptr, 0l,
                        sbuf, s_pstride, s_bstride, nullptr, 0l);
@@ -153,7 +202,7 @@ hipError_t launch_dots_mfma_gather(const DevProb& pr, const int32_t* items, cons
                                    hipStream_t st) {
   if (C <= 0) return hipSuccess;
   if (pr.Pq > 64) return hipErrorInvalidValue;
-  const dim3 grid((C + 63) / 64, pr.B, pr.Px);
+  const dim3 grid((C + 127) / 128, pr.B, pr.Px);
   hipLaunchKernelGGL(k_dots_mfma<kDotsToBuffer>, grid, dim3(256), 0, st, pr, 0, C, items, item_count,
                      item_stride, sbuf, s_pstride, s_bstride, nullptr, 0l);
   return hipGetLastError();

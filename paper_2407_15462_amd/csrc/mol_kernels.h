@@ -33,6 +33,14 @@ hipError_t launch_dots_mfma_gather(const DevProb& pr, const int32_t* items, cons
                                    long item_stride, int C, float* sbuf, long s_pstride, long s_bstride,
                                    hipStream_t st);
 
+// Pair-wise gating on MFMA over the dots buffer (bf16, P <= 64, H <= 128):
+// the same modes, arguments and outputs as launch_phi_generic with sbuf set.
+bool phi_mfma_supported(const DevProb& pr);
+hipError_t launch_phi_mfma(const DevProb& pr, int mode, const float* bound, int n_begin, int n_count,
+                           const int32_t* items, const int32_t* item_count, long item_stride,
+                           const float* sbuf, long s_pstride, long s_bstride, float* phi, long phi_stride,
+                           uint64_t* keys, long key_stride, hipStream_t st);
+
 // Selection machinery over 64-bit sort keys.
 int segment_size_for(int L, int k);
 // Rows of L keys -> their top k (k <= 8192) by radix selection, one

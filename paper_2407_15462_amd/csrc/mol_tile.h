@@ -294,6 +294,63 @@ struct MolMlp {
       for (int i = 0; i < 4; ++i) b1acc[jt][i] = -kLog2e * pr.b1[16 * jt + 4 * g + i];
   }
 
+  // The same for a problem with pr.P <= P components and pr.H <= H hidden
+  // units: the missing rows and columns of W1, b1 and W2 are zero, so the
+  // padded hidden units give h' = 0 and the padded components' logits keep
+  // their accumulator input (set to -inf by the caller: zero weight).
+  __device__ void load_padded(const DevProb& pr, int c, int g) {
+    const bf16_t* W1 = static_cast<const bf16_t*>(pr.W1);
+    const bf16_t* W2 = static_cast<const bf16_t*>(pr.W2);
+    const int Pr = pr.P, Hr = pr.H;
+    const int base = lane_base(g, PX);
+    // every read is unconditional, from a clamped in-range index, and masked
+    // afterwards: the reads are issued together instead of one branch (and
+    // one wait) each
+    auto w1 = [&](int j, int p) -> uint32_t {
+      const bf16_t w = W1[min(j, Hr - 1) * Pr + min(p, Pr - 1)];
+      const uint32_t keep = 0u - static_cast<uint32_t>((j < Hr) & (p < Pr));
+      return neg_bf16_to_f16_bits(w, kLog2e) & keep;
+    };
+    auto w2 = [&](int p, int j) -> uint32_t {
+      const bf16_t w = W2[min(p, Pr - 1) * Hr + min(j, Hr - 1)];
+      const uint32_t keep = 0u - static_cast<uint32_t>((j < Hr) & (p < Pr));
+      return neg_bf16_to_f16_bits(w, 1.f) & keep;
+    };
+#pragma unroll
+    for (int jt = 0; jt < JT; ++jt)
+#pragma unroll
+      for (int m = 0; m < KP; ++m) {
+        const int j = 16 * jt + c, p0 = base + 8 * m;
+        uint32_t w[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) w[e] = w1(j, p0 + 2 * e) | (w1(j, p0 + 2 * e + 1) << 16);
+        w1op[jt][m] = make_uint4(w[0], w[1], w[2], w[3]);
+      }
+#pragma unroll
+    for (int pt = 0; pt < PT; ++pt)
+#pragma unroll
+      for (int m = 0; m < KH; ++m) {
+        const int p = lane_base(c >> 2, PX) + 4 * pt + (c & 3);
+        uint32_t w[4];
+#pragma unroll
+        for (int e2 = 0; e2 < 4; ++e2) {
+          const int e0 = 2 * e2, e1 = 2 * e2 + 1;
+          const int j0 = 32 * m + 16 * (e0 >> 2) + 4 * g + (e0 & 3);
+          const int j1 = 32 * m + 16 * (e1 >> 2) + 4 * g + (e1 & 3);
+          w[e2] = w2(p, j0) | (w2(p, j1) << 16);
+        }
+        w2op[pt][m] = make_uint4(w[0], w[1], w[2], w[3]);
+      }
+#pragma unroll
+    for (int jt = 0; jt < JT; ++jt)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int j = 16 * jt + 4 * g + i;
+        const float b = pr.b1[min(j, Hr - 1)];
+        b1acc[jt][i] = j < Hr ? -kLog2e * b : 0.f;
+      }
+  }
+
   // Base-2 gating logits l' of one query for the lane's items (GEMM2 ->
   // SiLU -> GEMM3).  s: the lane's run of s values; c0: log2(e) (a_x + a_q
   // + b2) in the GEMM3 accumulator layout (element i of tile pt <-> p =
