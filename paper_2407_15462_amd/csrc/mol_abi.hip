@@ -339,9 +339,46 @@ PerEmbdPlan plan_per_embd(const DevProb& pr, int kp) {
   return f;
 }
 
+// Per-component top-k' for the shapes without the fused per-component
+// kernels, when the dots run on MFMA: a threshold from a sample, then one
+// pass that keeps only the keys reaching it.  The k'-th largest key of any
+// subset of a list is at most the list's k'-th largest key, so every key of
+// the list's top k' reaches the sample's k'-th key and the selection over
+// the kept keys is exact.  The kept-key rows hold every item, so nothing can
+// overflow; a sample with fewer than k' keys gives threshold 0 (keep all).
+struct ThreshPlan {
+  int rows = 0, tile_stride = 1;
+  long ns = 0;   // sample slots per row
+  size_t offCnt = 0, offSmp = 0, offTk = 0, offCand = 0, offFin = 0, bytes = 0;
+};
+constexpr int kThreshMinN = 1 << 14;               // shorter rows: the streamed path
+constexpr size_t kThreshMaxCand = size_t(2) << 30;  // kept-key rows, bytes
+
+bool use_thresh_per_embd(const DevProb& pr, int kp) {
+  return !per_embd_supported(pr, kp) && dots_mfma_supported(pr) && pr.N >= kThreshMinN &&
+         8ul * pr.B * pr.P * pr.N <= kThreshMaxCand;
+}
+
+ThreshPlan plan_thresh(const DevProb& pr, int kp) {
+  ThreshPlan t;
+  t.rows = pr.B * pr.P;
+  // a 1/8 sample where it still holds 16 k' items per list
+  t.tile_stride = static_cast<int>(std::max<long>(1, std::min<long>(8, pr.N / (16l * kp))));
+  t.ns = dots_sample_len(pr.N, t.tile_stride);
+  size_t off = 0;
+  t.offCnt = off;  off = align_up(off + 4ul * t.rows);
+  t.offSmp = off;  off = align_up(off + 8ul * t.rows * t.ns);
+  t.offTk = off;   off = align_up(off + 8ul * t.rows * kp);
+  t.offCand = off; off = align_up(off + 8ul * t.rows * pr.N);
+  t.offFin = off;  off = align_up(off + 8ul * t.rows * kp);
+  t.bytes = off;
+  return t;
+}
+
 size_t per_embd_ws_bytes(const DevProb& pr, int kp) {
-  return per_embd_supported(pr, kp) ? plan_per_embd(pr, kp).bytes
-                                    : plan_stream(pr.B * pr.P, pr.N, kp).bytes;
+  if (per_embd_supported(pr, kp)) return plan_per_embd(pr, kp).bytes;
+  if (use_thresh_per_embd(pr, kp)) return plan_thresh(pr, kp).bytes;
+  return plan_stream(pr.B * pr.P, pr.N, kp).bytes;
 }
 
 size_t exact_ws_bytes(const DevProb& pr, int k) {
@@ -462,6 +499,23 @@ int run_per_embd(const DevProb& pr, int kprime, float* out_dot, int32_t* out_idx
     MOL_TIMED_LAUNCH(timed_op, st, launch_per_embd(pr, kprime, f.g, bmax, thr, lists, stg, st),
                      "per-component top-k'");
     if ((rc = reduce_rows(f.s, w, static_cast<long>(f.g.s2.R) * f.KL, fin, kprime, st))) return rc;
+    MOL_TRY_HIP(launch_decode(fin, kprime, rows, kprime, out_dot, out_idx, st), "decode");
+    return MOL_OK;
+  }
+  if (use_thresh_per_embd(pr, kprime)) {
+    const ThreshPlan t = plan_thresh(pr, kprime);
+    uint32_t* counts = reinterpret_cast<uint32_t*>(w + t.offCnt);
+    uint64_t* smp = reinterpret_cast<uint64_t*>(w + t.offSmp);
+    uint64_t* tk = reinterpret_cast<uint64_t*>(w + t.offTk);
+    uint64_t* cand = reinterpret_cast<uint64_t*>(w + t.offCand);
+    uint64_t* fin = reinterpret_cast<uint64_t*>(w + t.offFin);
+    MOL_TRY_HIP(launch_fill(reinterpret_cast<uint64_t*>(counts), (rows + 1) / 2, 0ull, st), "clear counts");
+    MOL_TRY_HIP(launch_dots_mfma(pr, 0, pr.N, kDotsToKeys, nullptr, 0, 0, smp, t.ns, st, t.tile_stride),
+                "sample dots");
+    MOL_TRY_HIP(launch_radix_topk(smp, t.ns, rows, t.ns, kprime, tk, kprime, st), "sample top-k'");
+    MOL_TRY_HIP(launch_dots_mfma_candidates(pr, 0, pr.N, tk + (kprime - 1), kprime, cand, pr.N, counts, st),
+                "thresholded dots");
+    MOL_TRY_HIP(launch_radix_topk(cand, pr.N, rows, pr.N, kprime, fin, kprime, st, counts), "top-k'");
     MOL_TRY_HIP(launch_decode(fin, kprime, rows, kprime, out_dot, out_idx, st), "decode");
     return MOL_OK;
   }

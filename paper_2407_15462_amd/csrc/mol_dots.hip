@@ -17,10 +17,18 @@
 // spare at rerank sizes).
 //
 // Outputs, per mode:
-//   kDotsToBuffer  s[p][b][i] float32 (p = pq * P_x + px, i = item - n0),
-//                  the input of the pair-wise gating kernel;
-//   kDotsToKeys    keys[(b * P + p) * key_stride + i], the per-component
-//                  lists (TopKDotProduct) before selection.
+//   kDotsToBuffer      s[p][b][i] float32 (p = pq * P_x + px, i = item - n0),
+//                      the input of the pair-wise gating kernel;
+//   kDotsToKeys        keys[(b * P + p) * key_stride + i], the per-component
+//                      lists (TopKDotProduct) before selection.  With
+//                      tile_stride > 1 only every tile_stride-th 128-item
+//                      tile is computed (a sample), its keys stored
+//                      compactly (tile j at 128 j) and slots past the range
+//                      cleared to 0;
+//   kDotsToCandidates  the keys of list (b, p) that reach thr[(b * P + p) *
+//                      thr_stride] are appended to its row of `keys`, the
+//                      list's count advanced with one atomic add per wave
+//                      and row (the rows must hold every item).
 #include "mol_tile.h"
 
 namespace mol {
@@ -47,10 +55,13 @@ __device__ __forceinline__ int dots_swz8(int r, int ch) { return ch ^ ((r >> 1) 
 // Grid: x = 128-item tiles of [n0, n0 + nt), y = 64-vector tiles of the
 // B * P_q query vectors (gather form: query b), z = item component px.
 template <int MODE>
-__global__ __launch_bounds__(256) void k_dots_mfma(DevProb pr, int n0, int nt, const int32_t* __restrict__ items,
+__global__ __launch_bounds__(256) void k_dots_mfma(DevProb pr, int n0, int nt, int tile_stride,
+                                                   const int32_t* __restrict__ items,
                                                    const int32_t* __restrict__ item_count, long item_stride,
                                                    float* __restrict__ sbuf, long s_pstride, long s_bstride,
-                                                   uint64_t* __restrict__ keys, long key_stride) {
+                                                   uint64_t* __restrict__ keys, long key_stride,
+                                                   const uint64_t* __restrict__ thr, long thr_stride,
+                                                   uint32_t* __restrict__ counts) {
   constexpr int TI = 128, TV = 64, KS = 64, CH = KS / 8;   // tile items, vectors, K per step, chunks per row
   // staging: items [2][TI][CH] (16 KB per buffer), then vectors [2][TV][CH]
   // (8 KB per buffer); after the K loop the result tile [TV][TR] floats
@@ -61,7 +72,8 @@ __global__ __launch_bounds__(256) void k_dots_mfma(DevProb pr, int n0, int nt, c
   uint4* sB = smem + 2 * TI * CH;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const bool gather = items != nullptr;
-  const int it0 = blockIdx.x * TI, px = blockIdx.z;
+  const int it0 = blockIdx.x * TI * tile_stride, px = blockIdx.z;   // first item of the tile (range-relative)
+  const int ot0 = blockIdx.x * TI;                                   // its first output slot
   // vectors of the tile: [v0, v1)
   const int v0 = gather ? blockIdx.y * pr.Pq : blockIdx.y * TV;
   const int v1 = gather ? v0 + pr.Pq : pr.B * pr.Pq;
@@ -97,6 +109,17 @@ __global__ __launch_bounds__(256) void k_dots_mfma(DevProb pr, int n0, int nt, c
     vok[i] = v0 + r < v1;
     qsrc[i] = Q + static_cast<long>(vok[i] ? v0 + r : 0) * D + 8 * ch;
     bslot[i] = r * CH + dots_swz8(r, ch);
+  }
+
+  // candidates: the thresholds of the wave's 16 epilogue rows, read by
+  // lanes 0..15 now so that the reads complete during the K loop
+  uint64_t thr_lane = ~0ull;
+  if (MODE == kDotsToCandidates && lane < TV / 4) {
+    const int v = v0 + wave * (TV / 4) + lane;
+    if (v < v1) {
+      const int b = v / pr.Pq, pq = v - (v / pr.Pq) * pr.Pq;
+      thr_lane = thr[(static_cast<long>(b) * pr.P + pq * pr.Px + px) * thr_stride];
+    }
   }
 
   const int c = lane & 31, h = lane >> 5;
@@ -155,6 +178,52 @@ __global__ __launch_bounds__(256) void k_dots_mfma(DevProb pr, int n0, int nt, c
       *reinterpret_cast<float4*>(sT + rb * TR + wm * 64 + ib * 32 + 8 * j + 4 * h) =
           float4{acc[ib][4 * j + 0], acc[ib][4 * j + 1], acc[ib][4 * j + 2], acc[ib][4 * j + 3]};
   __syncthreads();
+  if (MODE == kDotsToCandidates) {
+    // Two passes over the wave's 16 rows: count the keys each row keeps
+    // (row rr's count lands in lane rr), reserve every row's slots with one
+    // atomic add per row issued by lanes 0..15 together, then store.
+    const int nrows = max(0, min(TV / 4, v1 - v0 - wave * (TV / 4)));
+    auto kept = [&](int rr, int t, uint64_t th, uint64_t& key) {
+      const int i = it0 + 64 * t + lane;
+      key = i < cnt ? make_key(sT[(wave * (TV / 4) + rr) * TR + 64 * t + lane], n0 + i) : 0ull;
+      return key != 0ull && key >= th;
+    };
+    uint32_t row_hits = 0;                              // lane rr: keys kept by row rr
+    for (int rr = 0; rr < nrows; ++rr) {
+      const uint64_t th = static_cast<uint64_t>(__shfl(static_cast<long long>(thr_lane), rr, 64));
+      uint32_t n = 0;
+#pragma unroll
+      for (int t = 0; t < 2; ++t) {
+        uint64_t key;
+        n += static_cast<uint32_t>(__popcll(__ballot(kept(rr, t, th, key))));
+      }
+      if (lane == rr) row_hits = n;
+    }
+    auto row_list = [&](int rr) {
+      const int v = v0 + wave * (TV / 4) + rr;
+      const int b = v / pr.Pq, pq = v - (v / pr.Pq) * pr.Pq;
+      return static_cast<long>(b) * pr.P + pq * pr.Px + px;
+    };
+    uint32_t row_base = 0;
+    if (lane < nrows && row_hits > 0) row_base = atomicAdd(counts + row_list(lane), row_hits);
+    for (int rr = 0; rr < nrows; ++rr) {
+      if (__shfl(row_hits, rr, 64) == 0u) continue;     // wave-uniform
+      const uint64_t th = static_cast<uint64_t>(__shfl(static_cast<long long>(thr_lane), rr, 64));
+      uint32_t pos = __shfl(row_base, rr, 64);
+      uint64_t* dst = keys + row_list(rr) * key_stride;
+#pragma unroll
+      for (int t = 0; t < 2; ++t) {
+        uint64_t key;
+        const bool hit = kept(rr, t, th, key);
+        const uint64_t mask = __ballot(hit);
+        const uint32_t below = __builtin_amdgcn_mbcnt_hi(static_cast<uint32_t>(mask >> 32),
+                                                         __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(mask), 0u));
+        if (hit) dst[pos + below] = key;
+        pos += static_cast<uint32_t>(__popcll(mask));
+      }
+    }
+    return;
+  }
   // each wave writes 16 of the tile's vector rows
   for (int rr = 0; rr < TV / 4; ++rr) {
     const int r = wave * (TV / 4) + rr;
@@ -171,7 +240,8 @@ __global__ __launch_bounds__(256) void k_dots_mfma(DevProb pr, int n0, int nt, c
 #pragma unroll
       for (int t = 0; t < 2; ++t) {
         const int i = it0 + 64 * t + lane;
-        if (i < cnt) dst[i] = make_key(sT[r * TR + 64 * t + lane], n0 + i);
+        if (i < cnt) dst[ot0 + 64 * t + lane] = make_key(sT[r * TR + 64 * t + lane], n0 + i);
+        else if (tile_stride > 1) dst[ot0 + 64 * t + lane] = 0ull;
       }
     }
   }
@@ -184,16 +254,34 @@ bool dots_mfma_supported(const DevProb& pr) {
 long dots_buffer_row(int nt) { return (static_cast<long>(nt) + 127) / 128 * 128; }
 
 hipError_t launch_dots_mfma(const DevProb& pr, int n0, int nt, int mode, float* sbuf, long s_pstride,
-                            long s_bstride, uint64_t* keys, long key_stride, hipStream_t st) {
+                            long s_bstride, uint64_t* keys, long key_stride, hipStream_t st, int tile_stride) {
+  if (nt <= 0) return hipSuccess;
+  if (tile_stride < 1 || (tile_stride > 1 && mode != kDotsToKeys)) return hipErrorInvalidValue;
+  const int nvec = pr.B * pr.Pq;
+  const int tiles = (nt + 127) / 128;
+  const dim3 grid((tiles + tile_stride - 1) / tile_stride, (nvec + 63) / 64, pr.Px);
+  if (mode == kDotsToBuffer)
+    hipLaunchKernelGGL(k_dots_mfma<kDotsToBuffer>, grid, dim3(256), 0, st, pr, n0, nt, 1, nullptr, nullptr, 0l,
+                       sbuf, s_pstride, s_bstride, nullptr, 0l, nullptr, 0l, nullptr);
+  else
+    hipLaunchKernelGGL(k_dots_mfma<kDotsToKeys>, grid, dim3(256), 0, st, pr, n0, nt, tile_stride, nullptr,
+                       nullptr, 0l, nullptr, 0l, 0l, keys, key_stride, nullptr, 0l, nullptr);
+  return hipGetLastError();
+}
+
+// keys per row of the keys form: nt (tile_stride 1: exactly the range's
+// keys are written), else whole sampled tiles (slots past the range cleared)
+long dots_sample_len(int nt, int tile_stride) {
+  return tile_stride == 1 ? nt : ((nt + 127) / 128 + tile_stride - 1) / tile_stride * 128l;
+}
+
+hipError_t launch_dots_mfma_candidates(const DevProb& pr, int n0, int nt, const uint64_t* thr, long thr_stride,
+                                       uint64_t* cand, long cand_stride, uint32_t* counts, hipStream_t st) {
   if (nt <= 0) return hipSuccess;
   const int nvec = pr.B * pr.Pq;
   const dim3 grid((nt + 127) / 128, (nvec + 63) / 64, pr.Px);
-  if (mode == kDotsToBuffer)
-    hipLaunchKernelGGL(k_dots_mfma<kDotsToBuffer>, grid, dim3(256), 0, st, pr, n0, nt, nullptr, nullptr, 0l,
-                       sbuf, s_pstride, s_bstride, nullptr, 0l);
-  else
-    hipLaunchKernelGGL(k_dots_mfma<kDotsToKeys>, grid, dim3(256), 0, st, pr, n0, nt, nullptr, nullptr, 0l,
-                       nullptr, 0l, 0l, keys, key_stride);
+  hipLaunchKernelGGL(k_dots_mfma<kDotsToCandidates>, grid, dim3(256), 0, st, pr, n0, nt, 1, nullptr, nullptr,
+                     0l, nullptr, 0l, 0l, cand, cand_stride, thr, thr_stride, counts);
   return hipGetLastError();
 }
 
@@ -203,8 +291,8 @@ hipError_t launch_dots_mfma_gather(const DevProb& pr, const int32_t* items, cons
   if (C <= 0) return hipSuccess;
   if (pr.Pq > 64) return hipErrorInvalidValue;
   const dim3 grid((C + 127) / 128, pr.B, pr.Px);
-  hipLaunchKernelGGL(k_dots_mfma<kDotsToBuffer>, grid, dim3(256), 0, st, pr, 0, C, items, item_count,
-                     item_stride, sbuf, s_pstride, s_bstride, nullptr, 0l);
+  hipLaunchKernelGGL(k_dots_mfma<kDotsToBuffer>, grid, dim3(256), 0, st, pr, 0, C, 1, items, item_count,
+                     item_stride, sbuf, s_pstride, s_bstride, nullptr, 0l, nullptr, 0l, nullptr);
   return hipGetLastError();
 }
 

@@ -22,11 +22,21 @@ hipError_t launch_dots_generic(const DevProb& pr, int n_begin, int n_count, uint
 // Component dot products on MFMA for the generic shapes (bf16, d % 32 == 0):
 // into a buffer s[p][b][i] (row stride dots_buffer_row(nt) floats, p stride
 // B * that) for the pair-wise gating kernel, or into per-component sort keys.
-enum DotsMode { kDotsToBuffer = 0, kDotsToKeys = 1 };
+// tile_stride > 1 (keys only): every tile_stride-th 128-item tile, keys
+// stored compactly, dots_sample_len(nt, tile_stride) slots per row (the
+// slots past the range cleared to 0); tile_stride 1 writes nt keys.
+// Candidates: the keys of list (b, p) at or above thr[(b * P + p) *
+// thr_stride] appended to its row of `cand` (which must hold nt keys),
+// counts[b * P + p] advanced (the counts start at zero).
+enum DotsMode { kDotsToBuffer = 0, kDotsToKeys = 1, kDotsToCandidates = 2 };
 bool dots_mfma_supported(const DevProb& pr);
 long dots_buffer_row(int nt);
+long dots_sample_len(int nt, int tile_stride);
 hipError_t launch_dots_mfma(const DevProb& pr, int n0, int nt, int mode, float* sbuf, long s_pstride,
-                            long s_bstride, uint64_t* keys, long key_stride, hipStream_t st);
+                            long s_bstride, uint64_t* keys, long key_stride, hipStream_t st,
+                            int tile_stride = 1);
+hipError_t launch_dots_mfma_candidates(const DevProb& pr, int n0, int nt, const uint64_t* thr, long thr_stride,
+                                       uint64_t* cand, long cand_stride, uint32_t* counts, hipStream_t st);
 // the same into the buffer for per-query candidate lists (items [B][item_stride],
 // item_count [B], at most C per query): s[p][b][i] of candidate i
 hipError_t launch_dots_mfma_gather(const DevProb& pr, const int32_t* items, const int32_t* item_count,
@@ -45,8 +55,9 @@ hipError_t launch_phi_mfma(const DevProb& pr, int mode, const float* bound, int 
 int segment_size_for(int L, int k);
 // Rows of L keys -> their top k (k <= 8192) by radix selection, one
 // workgroup per row (keys of a row distinct apart from empty ones).
+// row_len: NULL, or per-row key counts (row r reads min(row_len[r], L) keys).
 hipError_t launch_radix_topk(const uint64_t* in, long in_stride, int rows, long L, int k, uint64_t* out,
-                             long out_stride, hipStream_t st);
+                             long out_stride, hipStream_t st, const uint32_t* row_len = nullptr);
 hipError_t launch_segment_topk(const uint64_t* in, long in_stride, int rows, int L, int k,
                                uint64_t* out, long out_stride, hipStream_t st);
 hipError_t launch_decode(const uint64_t* keys, long key_stride, int rows, int k, float* score,

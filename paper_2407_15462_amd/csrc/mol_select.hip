@@ -30,14 +30,15 @@ __device__ __forceinline__ bool has_prefix(uint64_t key, uint64_t prefix, int sh
 }  // namespace
 
 __global__ __launch_bounds__(kSelThreads) void k_radix_topk(const uint64_t* __restrict__ in, long in_stride,
-                                                            long L, int k, uint64_t* __restrict__ out,
-                                                            long out_stride) {
+                                                            long L_all, int k, uint64_t* __restrict__ out,
+                                                            long out_stride, const uint32_t* __restrict__ row_len) {
   __shared__ uint64_t buf[kSelCap];
   __shared__ uint32_t hist[256];
   __shared__ uint32_t s_bin, s_above, s_nz, s_count;
   const int tid = threadIdx.x, lane = tid & 63;
   const long row = blockIdx.x;
   const uint64_t* src = in + row * in_stride;
+  const long L = row_len ? min(L_all, static_cast<long>(row_len[row])) : L_all;
 
   uint64_t prefix = 0;
   uint32_t kk = static_cast<uint32_t>(k);   // rank of T among the keys sharing the prefix
@@ -159,9 +160,10 @@ __global__ __launch_bounds__(kSelThreads) void k_radix_topk(const uint64_t* __re
 }
 
 hipError_t launch_radix_topk(const uint64_t* in, long in_stride, int rows, long L, int k, uint64_t* out,
-                             long out_stride, hipStream_t st) {
+                             long out_stride, hipStream_t st, const uint32_t* row_len) {
   if (k > kSelCap) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(k_radix_topk, dim3(rows), dim3(kSelThreads), 0, st, in, in_stride, L, k, out, out_stride);
+  hipLaunchKernelGGL(k_radix_topk, dim3(rows), dim3(kSelThreads), 0, st, in, in_stride, L, k, out, out_stride,
+                     row_len);
   return hipGetLastError();
 }
 

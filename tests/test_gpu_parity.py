@@ -135,6 +135,10 @@ def test_duplicate_items_tie_to_lower_index():
     ("books_d32_k5", W["paper_books"].scaled(B=3, N=9001, clusters=32), 5),
     ("books_d32_k200", W["paper_books"].scaled(B=3, N=9001, clusters=32), 200),
     ("nq_d768_generic", W["paper_nq320k"].scaled(B=3, N=3001, clusters=16), 50),
+    # long rows of the generic shapes: sampled threshold, then the kept keys
+    ("nq_d768_thresh", W["paper_nq320k"].scaled(B=3, N=20011, clusters=16), 50),
+    ("nq_d768_thresh_k1000", W["paper_nq320k"].scaled(B=2, N=16411, clusters=16), 1000),
+    ("pq4_d64_thresh", dataclasses.replace(W["exact_32k"], Pq=4, B=4, N=33001, clusters=32), 100),
 ])
 def test_topk_per_embd_matches_oracle(name, spec, kp):
     log(f"[per_embd] {name} B={spec.B} N={spec.N} P={spec.P} k'={kp}")
@@ -178,6 +182,37 @@ def test_topk_per_embd_adversarial_order_and_ties():
         s_all = mo.all_dots(op, b)
         for p in range(spec.P):
             check_topk_row(s_all[:, p], ids[b, p], dots[b, p], kp, f"adversarial b={b} p={p}")
+
+
+def test_thresholded_per_embd_adversarial_order_and_ties():
+    """Generic-shape lists (d = 768) long enough for the sampled threshold:
+    a tied block on top that lies wholly in tiles the sample skips (every
+    8th 128-item tile is sampled), and all-tied lists (a zero query vector).
+    The threshold then keeps many keys, and ties resolve to the lowest
+    item indices."""
+    spec = W["paper_nq320k"].scaled(B=3, N=17000, clusters=16)
+    kp = 50
+    inp = cuda_inputs(spec, seed=22)
+    blk0, blk1 = 128, 1024                            # tiles 1..7: none sampled
+    inp.X[0, blk0:blk1, :] = inp.Q[1, 0, :]
+    inp.Q[2, 3, :] = 0
+    log(f"[per_embd thresholded adversarial] B={spec.B} N={spec.N} k'={kp}")
+    prob = mol.Problem(inp.Q, inp.X)
+    dots, ids = mol.topk_per_embd(prob, kp)
+    torch.cuda.synchronize()
+    dots, ids = dots.cpu().numpy(), ids.cpu().numpy()
+    Px = spec.Px
+    assert ids[1, 0].tolist() == list(range(blk0, blk0 + kp))
+    assert np.all(dots[1, 0] == dots[1, 0, 0])
+    for px in range(Px):
+        p = 3 * Px + px
+        assert ids[2, p].tolist() == list(range(kp)), f"zero query, component {p}"
+        assert np.all(dots[2, p] == 0.0)
+    op = oracle_problem(inp)
+    for b in range(spec.B):
+        s_all = mo.all_dots(op, b)
+        for p in range(spec.P):
+            check_topk_row(s_all[:, p], ids[b, p], dots[b, p], kp, f"thresholded b={b} p={p}")
 
 
 def test_avg_embed_bit_exact_and_topk_avg():
