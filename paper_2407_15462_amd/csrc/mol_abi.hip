@@ -138,6 +138,8 @@ DevProb dev_prob(const mol_problem* p) {
 // rows longer than this are reduced by radix selection, shorter ones by
 // segmented sorts
 constexpr long kRadixRowMin = 1l << 15;
+constexpr long kRadixChunk = 1l << 14;   // keys per workgroup of the chunked first pass
+constexpr int kRadixFewRows = 128;       // rows below which long rows are chunked
 
 struct StreamPlan {
   int rows = 0, k = 0, T = 0;
@@ -202,12 +204,25 @@ int reduce_rows(const StreamPlan& s, char* ws, long len, uint64_t* out, long out
                 hipStream_t st) {
   uint64_t* bufs[2] = {reinterpret_cast<uint64_t*>(ws + s.offA), reinterpret_cast<uint64_t*>(ws + s.offB)};
   long strides[2] = {s.strideA, s.strideB};
+  int cur = 0;
+  // few long rows: a radix selection per 16K-key chunk first (more
+  // workgroups), then the rows of chunk lists are reduced as below.  The
+  // chunk lists fit the second buffer: chunks * k <= ceil(len / 4096) * k.
+  if (len > 2 * kRadixChunk && s.rows < kRadixFewRows && s.k <= 1024) {
+    const int chunks = static_cast<int>((len + kRadixChunk - 1) / kRadixChunk);
+    if (static_cast<long>(chunks) * s.k > strides[1]) return fail(MOL_EHIP, "internal: chunk lists too long");
+    MOL_TRY_HIP(launch_radix_topk_chunks(bufs[0], strides[0], s.rows, len, s.k, chunks, kRadixChunk, bufs[1], st),
+                "radix top-k per chunk");
+    // (rows of chunks * k keys at stride chunks * k)
+    strides[1] = static_cast<long>(chunks) * s.k;
+    len = strides[1];
+    cur = 1;
+  }
   // long rows or large k: one radix selection per row
   if (s.k > 1024 || len > kRadixRowMin) {
-    MOL_TRY_HIP(launch_radix_topk(bufs[0], strides[0], s.rows, len, s.k, out, out_stride, st), "radix top-k");
+    MOL_TRY_HIP(launch_radix_topk(bufs[cur], strides[cur], s.rows, len, s.k, out, out_stride, st), "radix top-k");
     return MOL_OK;
   }
-  int cur = 0;
   for (;;) {
     const int S = segment_size_for(static_cast<int>(len), s.k);
     const long nseg = (len + S - 1) / S;

@@ -58,6 +58,11 @@ int segment_size_for(int L, int k);
 // row_len: NULL, or per-row key counts (row r reads min(row_len[r], L) keys).
 hipError_t launch_radix_topk(const uint64_t* in, long in_stride, int rows, long L, int k, uint64_t* out,
                              long out_stride, hipStream_t st, const uint32_t* row_len = nullptr);
+// The same per chunk of chunk_len keys (chunks * chunk_len >= L): row r's
+// chunk j's top k at out[(r * chunks + j) * k], so a row's chunk lists are
+// one contiguous run of chunks * k keys.
+hipError_t launch_radix_topk_chunks(const uint64_t* in, long in_stride, int rows, long L, int k, int chunks,
+                                    long chunk_len, uint64_t* out, hipStream_t st);
 hipError_t launch_segment_topk(const uint64_t* in, long in_stride, int rows, int L, int k,
                                uint64_t* out, long out_stride, hipStream_t st);
 hipError_t launch_decode(const uint64_t* keys, long key_stride, int rows, int k, float* score,

@@ -1,6 +1,7 @@
 // Exact top-k of long rows of 64-bit sort keys by radix selection
 // (Definition 1's selection step for rows too long, or k too large, for the
-// segmented sorts): one workgroup per row.
+// segmented sorts): one workgroup per row, or per chunk of a row when the
+// rows are few (the chunks' top-k lists are then selected again).
 //
 // Keys of a row are distinct (the low word carries the item index) except
 // empty slots (key 0), which never count.  The k-th largest key T is found
@@ -31,14 +32,17 @@ __device__ __forceinline__ bool has_prefix(uint64_t key, uint64_t prefix, int sh
 
 __global__ __launch_bounds__(kSelThreads) void k_radix_topk(const uint64_t* __restrict__ in, long in_stride,
                                                             long L_all, int k, uint64_t* __restrict__ out,
-                                                            long out_stride, const uint32_t* __restrict__ row_len) {
+                                                            long out_stride, const uint32_t* __restrict__ row_len,
+                                                            int chunks, long chunk_len) {
   __shared__ uint64_t buf[kSelCap];
   __shared__ uint32_t hist[256];
   __shared__ uint32_t s_bin, s_above, s_nz, s_count;
   const int tid = threadIdx.x, lane = tid & 63;
-  const long row = blockIdx.x;
-  const uint64_t* src = in + row * in_stride;
-  const long L = row_len ? min(L_all, static_cast<long>(row_len[row])) : L_all;
+  // workgroup = (row, chunk j): keys [j chunk_len, (j + 1) chunk_len) of the row
+  const long row = blockIdx.x / chunks, j = blockIdx.x - (blockIdx.x / chunks) * chunks;
+  const long Lrow = row_len ? min(L_all, static_cast<long>(row_len[row])) : L_all;
+  const uint64_t* src = in + row * in_stride + j * chunk_len;
+  const long L = max(0l, min(chunk_len, Lrow - j * chunk_len));
 
   uint64_t prefix = 0;
   uint32_t kk = static_cast<uint32_t>(k);   // rank of T among the keys sharing the prefix
@@ -155,7 +159,7 @@ __global__ __launch_bounds__(kSelThreads) void k_radix_topk(const uint64_t* __re
       __syncthreads();
     }
   }
-  uint64_t* dst = out + row * out_stride;
+  uint64_t* dst = out + static_cast<long>(blockIdx.x) * out_stride;
   for (int i = tid; i < k; i += kSelThreads) dst[i] = i < static_cast<int>(n) ? buf[i] : 0ull;
 }
 
@@ -163,7 +167,15 @@ hipError_t launch_radix_topk(const uint64_t* in, long in_stride, int rows, long 
                              long out_stride, hipStream_t st, const uint32_t* row_len) {
   if (k > kSelCap) return hipErrorInvalidValue;
   hipLaunchKernelGGL(k_radix_topk, dim3(rows), dim3(kSelThreads), 0, st, in, in_stride, L, k, out, out_stride,
-                     row_len);
+                     row_len, 1, L);
+  return hipGetLastError();
+}
+
+hipError_t launch_radix_topk_chunks(const uint64_t* in, long in_stride, int rows, long L, int k, int chunks,
+                                    long chunk_len, uint64_t* out, hipStream_t st) {
+  if (k > kSelCap || chunks < 1 || static_cast<long>(chunks) * chunk_len < L) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_radix_topk, dim3(rows * chunks), dim3(kSelThreads), 0, st, in, in_stride, L, k, out,
+                     static_cast<long>(k), nullptr, chunks, chunk_len);
   return hipGetLastError();
 }
 

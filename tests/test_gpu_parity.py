@@ -430,6 +430,41 @@ def test_radix_selection_long_rows_large_k_and_ties():
         check_topk_row(phi[b], i3[b], s3[b], 1500, f"radix_exact b={b}")
 
 
+def test_radix_chunked_first_pass_few_long_rows():
+    """Few rows of more than 32K keys (k <= 1024) are first reduced per
+    16K-key chunk by separate workgroups, then per row: exact MoL top-k and
+    max-component top-k on a d = 768 shape with 40,001 items, and the
+    streamed per-component lists of a float32 problem, one list all-tied."""
+    spec = W["paper_nq320k"].scaled(B=3, N=40001, clusters=16)
+    inp = cuda_inputs(spec, seed=43)
+    log(f"[radix chunks] B={spec.B} N={spec.N} d={spec.d}")
+    prob = mol.Problem.from_inputs(inp)
+    s1, i1 = mol.topk_exact(prob, 100)
+    s2, i2 = mol.topk_exact(prob, 1000)
+    ms, mi = mol.topk_maxdot(mol.Problem(inp.Q, inp.X), 1000)
+    torch.cuda.synchronize()
+    op = oracle_problem(inp)
+    phi = mo.mol_scores(op, list(range(spec.B)))
+    for b in range(spec.B):
+        check_topk_row(phi[b], i1[b].cpu().numpy(), s1[b].cpu().numpy(), 100, f"radix_chunks k=100 b={b}")
+        check_topk_row(phi[b], i2[b].cpu().numpy(), s2[b].cpu().numpy(), 1000, f"radix_chunks k=1000 b={b}")
+        m = mo.all_dots(op, b).max(axis=1)
+        check_topk_row(m, mi[b].cpu().numpy(), ms[b].cpu().numpy(), 1000, f"radix_chunks maxdot b={b}")
+    spec2 = W["tiny_exact_f32"].scaled(B=2, N=40000)
+    inp2 = cuda_inputs(spec2, seed=44)
+    inp2.Q[1, 0, :] = 0
+    dots, ids = mol.topk_per_embd(mol.Problem(inp2.Q, inp2.X), 50)
+    torch.cuda.synchronize()
+    op2 = oracle_problem(inp2)
+    dots, ids = dots.cpu().numpy(), ids.cpu().numpy()
+    for b in range(spec2.B):
+        s_all = mo.all_dots(op2, b)
+        for p in range(spec2.P):
+            check_topk_row(s_all[:, p], ids[b, p], dots[b, p], 50, f"radix_chunks f32 b={b} p={p}")
+    for px in range(spec2.Px):
+        assert ids[1, px].tolist() == list(range(50))
+
+
 def test_worked_example_through_the_abi():
     """Appendix B's example run through the library: exact top-2 {a, d},
     TopKPerEmbedding(2) candidates {a, b, c}, rerank of those -> {a, b}."""
