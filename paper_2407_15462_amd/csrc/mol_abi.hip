@@ -401,7 +401,8 @@ size_t exact_ws_bytes(const DevProb& pr, int k) {
 }
 
 size_t maxdot_ws_bytes(const DevProb& pr, int k) {
-  return fused_maxdot_supported(pr, k) ? plan_fused_exact(pr, k).bytes : plan_pairwise(pr, k).bytes;
+  if (fused_maxdot_supported(pr, k)) return plan_fused_exact(pr, k).bytes;
+  return dots_maxkeys_supported(pr) ? plan_stream(pr.B, pr.N, k).bytes : plan_pairwise(pr, k).bytes;
 }
 
 // Algorithm 1 workspace: per-component lists, the rerank output over G,
@@ -492,6 +493,14 @@ int run_maxdot(const DevProb& pr, int k, float* out_score, int32_t* out_idx, cha
     if ((rc = reduce_rows(f.s, w, static_cast<long>(f.R) * k, fin, k, st))) return rc;
     MOL_TRY_HIP(launch_decode(fin, k, pr.B, k, out_score, out_idx, st), "decode");
     return MOL_OK;
+  }
+  if (dots_maxkeys_supported(pr)) {
+    // max-component keys straight from the dots GEMM (no dots buffer)
+    const StreamPlan s = plan_stream(pr.B, pr.N, k);
+    auto tile = [&](int n0, int nt, uint64_t* A, long strideA) {
+      return launch_dots_mfma_maxkeys(pr, n0, nt, A, strideA, st);
+    };
+    return stream_topk(s, pr.N, w, tile, out_score, out_idx, st);
   }
   const StreamPlan s = plan_pairwise(pr, k);
   auto tile = [&](int n0, int nt, uint64_t* A, long strideA) {

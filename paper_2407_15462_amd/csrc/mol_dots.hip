@@ -25,6 +25,9 @@
 //                      tile is computed (a sample), its keys stored
 //                      compactly (tile j at 128 j) and slots past the range
 //                      cleared to 0;
+//   kDotsToMaxKeys     keys[b * key_stride + i] of m = max_p s_p (the
+//                      components walked inside the workgroup; P_q divides
+//                      64): the max-component score of every item;
 //   kDotsToCandidates  the keys of list (b, p) that reach thr[(b * P + p) *
 //                      thr_stride] are appended to its row of `keys`, the
 //                      list's count advanced with one atomic add per wave
@@ -131,10 +134,12 @@ __global__ __launch_bounds__(256) void k_dots_mfma(DevProb pr, int n0, int nt, i
   // multiple of 32 only, the upper half of the last K step reads zeros
   const int kch = 8 * (tid % CH);
   uint4 xa[4], qb[2];
+  long xoff = 0;                                      // component offset (max-dot form: px walked here)
   auto load = [&](int k0) {
     const bool kin = k0 + kch < D;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) xa[i] = kin ? *reinterpret_cast<const uint4*>(xsrc[i] + k0) : make_uint4(0, 0, 0, 0);
+    for (int i = 0; i < 4; ++i)
+      xa[i] = kin ? *reinterpret_cast<const uint4*>(xsrc[i] + xoff + k0) : make_uint4(0, 0, 0, 0);
 #pragma unroll
     for (int i = 0; i < 2; ++i)
       qb[i] = kin && vok[i] ? *reinterpret_cast<const uint4*>(qsrc[i] + k0) : make_uint4(0, 0, 0, 0);
@@ -145,26 +150,45 @@ __global__ __launch_bounds__(256) void k_dots_mfma(DevProb pr, int n0, int nt, i
 #pragma unroll
     for (int i = 0; i < 2; ++i) sB[buf * TV * CH + bslot[i]] = qb[i];
   };
-  load(0);
-  store(0);
-  __syncthreads();
   const int nk = (D + KS - 1) / KS;
-  for (int kk = 0; kk < nk; ++kk) {
-    const int cur = kk & 1;
-    const bool more = kk + 1 < nk;
-    if (more) load(KS * (kk + 1));
-#pragma unroll
-    for (int kb = 0; kb < KS / 16; ++kb) {             // K blocks of 16
-      const uint4 b = sB[cur * TV * CH + rb * CH + dots_swz8(rb, 2 * kb + h)];
-#pragma unroll
-      for (int ib = 0; ib < 2; ++ib) {
-        const int ra = wm * 64 + ib * 32 + c;           // A row (item)
-        const uint4 a = sA[cur * TI * CH + ra * CH + dots_swz8(ra, 2 * kb + h)];
-        acc[ib] = mfma32x16_bf16(a, b, acc[ib]);
-      }
-    }
-    if (more) store(cur ^ 1);
+  // max-dot form: every component of the items in turn, keeping the
+  // elementwise maximum of the dot tiles
+  f32x16_t run[2] = {f32x16_t{}, f32x16_t{}};
+  const int npx = MODE == kDotsToMaxKeys ? pr.Px : 1;
+  for (int cx = 0; cx < npx; ++cx) {
+    xoff = MODE == kDotsToMaxKeys ? static_cast<long>(cx) * N * D : 0l;
+    acc[0] = f32x16_t{};
+    acc[1] = f32x16_t{};
+    load(0);
+    store(0);
     __syncthreads();
+    for (int kk = 0; kk < nk; ++kk) {
+      const int cur = kk & 1;
+      const bool more = kk + 1 < nk;
+      if (more) load(KS * (kk + 1));
+#pragma unroll
+      for (int kb = 0; kb < KS / 16; ++kb) {             // K blocks of 16
+        const uint4 b = sB[cur * TV * CH + rb * CH + dots_swz8(rb, 2 * kb + h)];
+#pragma unroll
+        for (int ib = 0; ib < 2; ++ib) {
+          const int ra = wm * 64 + ib * 32 + c;           // A row (item)
+          const uint4 a = sA[cur * TI * CH + ra * CH + dots_swz8(ra, 2 * kb + h)];
+          acc[ib] = mfma32x16_bf16(a, b, acc[ib]);
+        }
+      }
+      if (more) store(cur ^ 1);
+      __syncthreads();
+    }
+    if (MODE == kDotsToMaxKeys) {
+#pragma unroll
+      for (int ib = 0; ib < 2; ++ib)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) run[ib][e] = cx == 0 ? acc[ib][e] : fmaxf(run[ib][e], acc[ib][e]);
+    }
+  }
+  if (MODE == kDotsToMaxKeys) {
+    acc[0] = run[0];
+    acc[1] = run[1];
   }
 
   // The loop ended with a barrier: the staging area is free.  The tile goes
@@ -178,6 +202,24 @@ __global__ __launch_bounds__(256) void k_dots_mfma(DevProb pr, int n0, int nt, i
       *reinterpret_cast<float4*>(sT + rb * TR + wm * 64 + ib * 32 + 8 * j + 4 * h) =
           float4{acc[ib][4 * j + 0], acc[ib][4 * j + 1], acc[ib][4 * j + 2], acc[ib][4 * j + 3]};
   __syncthreads();
+  if (MODE == kDotsToMaxKeys) {
+    // m = max over the tile's P_q rows of each query (64 % P_q == 0, so a
+    // query's rows are one run of the tile); wave w takes queries w, w+4, ...
+    const int nq = TV / pr.Pq, b0 = v0 / pr.Pq;
+    for (int qi = wave; qi < nq; qi += 4) {
+      const int b = b0 + qi;
+      if (b >= pr.B) break;                            // wave-uniform; queries ascend
+      uint64_t* dst = keys + static_cast<long>(b) * key_stride;
+#pragma unroll
+      for (int t = 0; t < 2; ++t) {
+        const int i = it0 + 64 * t + lane;
+        float m = sT[(qi * pr.Pq) * TR + 64 * t + lane];
+        for (int pq = 1; pq < pr.Pq; ++pq) m = fmaxf(m, sT[(qi * pr.Pq + pq) * TR + 64 * t + lane]);
+        if (i < cnt) dst[i] = make_key(m, n0 + i);
+      }
+    }
+    return;
+  }
   if (MODE == kDotsToCandidates) {
     // Two passes over the wave's 16 rows: count the keys each row keeps
     // (row rr's count lands in lane rr), reserve every row's slots with one
@@ -271,6 +313,18 @@ hipError_t launch_dots_mfma(const DevProb& pr, int n0, int nt, int mode, float* 
 
 // keys per row of the keys form: nt (tile_stride 1: exactly the range's
 // keys are written), else whole sampled tiles (slots past the range cleared)
+bool dots_maxkeys_supported(const DevProb& pr) { return dots_mfma_supported(pr) && 64 % pr.Pq == 0; }
+
+hipError_t launch_dots_mfma_maxkeys(const DevProb& pr, int n0, int nt, uint64_t* keys, long key_stride,
+                                    hipStream_t st) {
+  if (nt <= 0) return hipSuccess;
+  if (!dots_maxkeys_supported(pr)) return hipErrorInvalidValue;
+  const dim3 grid((nt + 127) / 128, (pr.B * pr.Pq + 63) / 64, 1);
+  hipLaunchKernelGGL(k_dots_mfma<kDotsToMaxKeys>, grid, dim3(256), 0, st, pr, n0, nt, 1, nullptr, nullptr, 0l,
+                     nullptr, 0l, 0l, keys, key_stride, nullptr, 0l, nullptr);
+  return hipGetLastError();
+}
+
 long dots_sample_len(int nt, int tile_stride) {
   return tile_stride == 1 ? nt : ((nt + 127) / 128 + tile_stride - 1) / tile_stride * 128l;
 }

@@ -28,7 +28,11 @@ hipError_t launch_dots_generic(const DevProb& pr, int n_begin, int n_count, uint
 // Candidates: the keys of list (b, p) at or above thr[(b * P + p) *
 // thr_stride] appended to its row of `cand` (which must hold nt keys),
 // counts[b * P + p] advanced (the counts start at zero).
-enum DotsMode { kDotsToBuffer = 0, kDotsToKeys = 1, kDotsToCandidates = 2 };
+enum DotsMode { kDotsToBuffer = 0, kDotsToKeys = 1, kDotsToCandidates = 2, kDotsToMaxKeys = 3 };
+// max_p s_p of every (query, item) as sort keys [B][key_stride] (P_q divides 64)
+bool dots_maxkeys_supported(const DevProb& pr);
+hipError_t launch_dots_mfma_maxkeys(const DevProb& pr, int n0, int nt, uint64_t* keys, long key_stride,
+                                    hipStream_t st);
 bool dots_mfma_supported(const DevProb& pr);
 long dots_buffer_row(int nt);
 long dots_sample_len(int nt, int tile_stride);
