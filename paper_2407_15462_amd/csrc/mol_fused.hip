@@ -294,13 +294,15 @@ __global__ __launch_bounds__(64 * kWaves, 1) void k_mol_fused(
           __builtin_amdgcn_sched_barrier(0);
         }
       }
+      // phi[qb] is valid in the lanes of rows 2 qb and 2 qb + 1 (the two-query
+      // chain leaves each query's result there; the other forms in every lane)
 #pragma unroll
       for (int qb = 0; qb < 2; ++qb) {
         const int b = qwv + qb;
         if constexpr (DENSE) {
-          if (g == 0 && item_ok && b < pr.B) phi_out[b * phi_stride + (item - n_begin)] = phi[qb];
+          if (g == 2 * qb && item_ok && b < pr.B) phi_out[b * phi_stride + (item - n_begin)] = phi[qb];
         } else {
-          top[qb].offer_score(phi[qb], item, g == 0 && offer[qb], lane);
+          top[qb].offer_score(phi[qb], item, g == 2 * qb && offer[qb], lane);
         }
       }
     }

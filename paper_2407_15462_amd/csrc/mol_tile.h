@@ -414,14 +414,34 @@ struct MolMlp {
     num = n[0] + n[1];
   }
 
-  // phi for the lane's item under NQ queries.  The queries' chains are
-  // independent and branch-free, so they can be interleaved; a query whose
-  // max-free sum left [2^-60, 2^60] (logits far from zero) is redone with
-  // the row maximum subtracted.
-  // c0[q]: log2(e) (a_x + a_q + b2) of query q in the GEMM3 accumulator
-  // layout.
+  // Sums over the 4 lanes {c, c+16, c+32, c+48} of an item of two (den,
+  // num) pairs a and b: three swaps, no copies.  The rows of 16 lanes end
+  // up holding a's sums (rows 0, 1) and b's (rows 2, 3); each lane returns
+  // the pair of its rows.  The additions pair rows (0 + 1) + (2 + 3), as
+  // sum_groups does.
+  __device__ static void row_sums(float da, float na, float db, float nb, float& den, float& num) {
+    auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(da), __float_as_uint(na), false, false);
+    const float sa = __uint_as_float(a[0]) + __uint_as_float(a[1]);   // rows: da01, na01, da23, na23
+    auto b = __builtin_amdgcn_permlane16_swap(__float_as_uint(db), __float_as_uint(nb), false, false);
+    const float sb = __uint_as_float(b[0]) + __uint_as_float(b[1]);   // rows: db01, nb01, db23, nb23
+    auto u = __builtin_amdgcn_permlane32_swap(__float_as_uint(sa), __float_as_uint(sb), false, false);
+    const float t = __uint_as_float(u[0]) + __uint_as_float(u[1]);    // rows: da, na, db, nb
+    const uint32_t tb = __float_as_uint(t);
+    auto v = __builtin_amdgcn_permlane16_swap(tb, tb, false, false);
+    den = __uint_as_float(v[0]);                                       // rows: da, da, db, db
+    num = __uint_as_float(v[1]);                                       // rows: na, na, nb, nb
+  }
+
+  // phi for the lane's item under NQ (1 or 2) queries: out[q] is valid in
+  // the lanes of query q's rows (NQ = 2: rows 0-1 for query 0, rows 2-3 for
+  // query 1; NQ = 1: every lane).  The queries' chains are independent and
+  // branch-free, so they can be interleaved; a query whose max-free sum left
+  // [2^-60, 2^60] (logits far from zero) is redone with the row maximum
+  // subtracted.  c0[q]: log2(e) (a_x + a_q + b2) of query q in the GEMM3
+  // accumulator layout.
   template <int NQ>
   __device__ void phi(const float (&s)[NQ][RUN], const f32x4_t (&c0)[NQ][PT], float (&out)[NQ]) const {
+    static_assert(NQ == 1 || NQ == 2, "one or two queries per call");
     float den[NQ], num[NQ];
 #pragma unroll
     for (int q = 0; q < NQ; ++q) {
@@ -429,17 +449,15 @@ struct MolMlp {
       logits(s[q], c0[q], lg);
       weights(lg, s[q], 0.f, den[q], num[q]);
     }
-    bool ok = true;
-#pragma unroll
-    for (int q = 0; q < NQ; ++q) {
-      den[q] = sum_groups(den[q]);
-      num[q] = sum_groups(num[q]);
-      ok = ok && den[q] >= 0x1p-60f && den[q] <= 0x1p60f;
-    }
+    float D, Nm;
+    row_sums(den[0], num[0], den[NQ - 1], num[NQ - 1], D, Nm);
+    const bool ok = D >= 0x1p-60f && D <= 0x1p60f;
     if (!__all(ok)) {
+      const uint64_t okm = __ballot(ok);
 #pragma unroll
       for (int q = 0; q < NQ; ++q) {
-        if (__all(den[q] >= 0x1p-60f && den[q] <= 0x1p60f)) continue;
+        const uint64_t rows = NQ == 1 ? ~0ull : q == 0 ? 0x00000000FFFFFFFFull : 0xFFFFFFFF00000000ull;
+        if ((okm & rows) == rows) continue;
         f32x4_t lg[PT];
         logits(s[q], c0[q], lg);
         float mx = -__builtin_inff();
@@ -448,12 +466,12 @@ struct MolMlp {
 #pragma unroll
           for (int i = 0; i < 4; ++i) mx = fmaxf(mx, lg[pt][i]);
         weights(lg, s[q], max_groups(mx), den[q], num[q]);
-        den[q] = sum_groups(den[q]);
-        num[q] = sum_groups(num[q]);
       }
+      row_sums(den[0], num[0], den[NQ - 1], num[NQ - 1], D, Nm);
     }
+    const float v = Nm * __builtin_amdgcn_rcpf(D);
 #pragma unroll
-    for (int q = 0; q < NQ; ++q) out[q] = num[q] * __builtin_amdgcn_rcpf(den[q]);
+    for (int q = 0; q < NQ; ++q) out[q] = v;
   }
 };
 
