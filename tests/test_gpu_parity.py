@@ -139,6 +139,8 @@ def test_duplicate_items_tie_to_lower_index():
     ("nq_d768_thresh", W["paper_nq320k"].scaled(B=3, N=20011, clusters=16), 50),
     ("nq_d768_thresh_k1000", W["paper_nq320k"].scaled(B=2, N=16411, clusters=16), 1000),
     ("pq4_d64_thresh", dataclasses.replace(W["exact_32k"], Pq=4, B=4, N=33001, clusters=32), 100),
+    # the smallest rows that take the sampled threshold, one query, k' at the limit
+    ("nq_d768_thresh_kmax", W["paper_nq320k"].scaled(B=1, N=16384, clusters=16), 8192),
 ])
 def test_topk_per_embd_matches_oracle(name, spec, kp):
     log(f"[per_embd] {name} B={spec.B} N={spec.N} P={spec.P} k'={kp}")
