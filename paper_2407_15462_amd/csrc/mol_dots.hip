@@ -55,9 +55,13 @@ __device__ __forceinline__ int dots_swz8(int r, int ch) { return ch ^ ((r >> 1) 
 
 }  // namespace
 
-// Grid: x = 128-item tiles of [n0, n0 + nt), y = 64-vector tiles of the
+// Grid: x = 128-item tiles of [n0, n0 + nt), y = TV-vector tiles of the
 // B * P_q query vectors (gather form: query b), z = item component px.
-template <int MODE>
+// TV = 64 or 128 vectors per tile: each of the 4 waves owns 64 items x TV/2
+// vectors (TV/64 pairs of 32 x 32 blocks); with TV = 128 the items are read
+// once for twice as many vectors.  The result tile leaves through LDS in
+// halves of 64 vector rows.
+template <int MODE, int TV>
 __global__ __launch_bounds__(256) void k_dots_mfma(DevProb pr, int n0, int nt, int tile_stride,
                                                    const int32_t* __restrict__ items,
                                                    const int32_t* __restrict__ item_count, long item_stride,
@@ -65,12 +69,15 @@ __global__ __launch_bounds__(256) void k_dots_mfma(DevProb pr, int n0, int nt, i
                                                    uint64_t* __restrict__ keys, long key_stride,
                                                    const uint64_t* __restrict__ thr, long thr_stride,
                                                    uint32_t* __restrict__ counts) {
-  constexpr int TI = 128, TV = 64, KS = 64, CH = KS / 8;   // tile items, vectors, K per step, chunks per row
-  // staging: items [2][TI][CH] (16 KB per buffer), then vectors [2][TV][CH]
-  // (8 KB per buffer); after the K loop the result tile [TV][TR] floats
+  constexpr int TI = 128, KS = 64, CH = KS / 8;   // tile items, K per step, chunks per row
+  constexpr int NBV = TV / 64;                    // 32-vector blocks per wave
+  constexpr int BL = TV * CH / 256;               // vector-row chunks per thread and step
+  constexpr int HALVES = TV / 64;                 // 64-row halves of the result tile
+  // staging: items [2][TI][CH] (16 KB per buffer), then vectors [2][TV][CH];
+  // after the K loop one 64-row half of the result tile [64][TR] floats
   constexpr int TR = TI + 4;
   __shared__ uint4 smem[2 * TI * CH + 2 * TV * CH];
-  static_assert(TV * TR * 4 <= sizeof(smem), "result tile exceeds the staging area");
+  static_assert(64 * TR * 4 <= sizeof(smem), "result half-tile exceeds the staging area");
   uint4* sA = smem;
   uint4* sB = smem + 2 * TI * CH;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -85,7 +92,7 @@ __global__ __launch_bounds__(256) void k_dots_mfma(DevProb pr, int n0, int nt, i
   const bf16_t* X = static_cast<const bf16_t*>(pr.X);
   const bf16_t* Q = static_cast<const bf16_t*>(pr.Q);
 
-  // loader: 4 item-row chunks and 2 vector-row chunks per thread and step
+  // loader: 4 item-row chunks and BL vector-row chunks per thread and step
   const bf16_t* xsrc[4];
   int aslot[4];
 #pragma unroll
@@ -103,37 +110,46 @@ __global__ __launch_bounds__(256) void k_dots_mfma(DevProb pr, int n0, int nt, i
     xsrc[i] = X + (static_cast<long>(px) * N + item) * D + 8 * ch;
     aslot[i] = r * CH + dots_swz8(r, ch);
   }
-  const bf16_t* qsrc[2];
-  int bslot[2];
-  bool vok[2];
+  const bf16_t* qsrc[BL];
+  int bslot[BL];
+  bool vok[BL];
 #pragma unroll
-  for (int i = 0; i < 2; ++i) {
+  for (int i = 0; i < BL; ++i) {
     const int e = tid + 256 * i, r = e / CH, ch = e % CH;
     vok[i] = v0 + r < v1;
     qsrc[i] = Q + static_cast<long>(vok[i] ? v0 + r : 0) * D + 8 * ch;
     bslot[i] = r * CH + dots_swz8(r, ch);
   }
 
-  // candidates: the thresholds of the wave's 16 epilogue rows, read by
-  // lanes 0..15 now so that the reads complete during the K loop
-  uint64_t thr_lane = ~0ull;
-  if (MODE == kDotsToCandidates && lane < TV / 4) {
-    const int v = v0 + wave * (TV / 4) + lane;
-    if (v < v1) {
-      const int b = v / pr.Pq, pq = v - (v / pr.Pq) * pr.Pq;
-      thr_lane = thr[(static_cast<long>(b) * pr.P + pq * pr.Px + px) * thr_stride];
+  // candidates: the thresholds of the wave's 16 epilogue rows of each half,
+  // read by lanes 0..15 now so that the reads complete during the K loop
+  uint64_t thr_lane[HALVES];
+#pragma unroll
+  for (int hv = 0; hv < HALVES; ++hv) {
+    thr_lane[hv] = ~0ull;
+    if (MODE == kDotsToCandidates && lane < 16) {
+      const int v = v0 + 64 * hv + wave * 16 + lane;
+      if (v < v1) {
+        const int b = v / pr.Pq, pq = v - (v / pr.Pq) * pr.Pq;
+        thr_lane[hv] = thr[(static_cast<long>(b) * pr.P + pq * pr.Px + px) * thr_stride];
+      }
     }
   }
 
   const int c = lane & 31, h = lane >> 5;
-  const int wm = wave & 1, wn = wave >> 1;            // item half (64), vector half (32) of the tile
-  const int rb = wn * 32 + c;                         // B row (vector)
-  f32x16_t acc[2] = {f32x16_t{}, f32x16_t{}};
+  const int wm = wave & 1, wn = wave >> 1;            // item half (64), vector half (TV/2) of the tile
+  f32x16_t acc[2][NBV];
+  auto zero_acc = [&]() {
+#pragma unroll
+    for (int ib = 0; ib < 2; ++ib)
+#pragma unroll
+      for (int jb = 0; jb < NBV; ++jb) acc[ib][jb] = f32x16_t{};
+  };
 
   // every loader slot of a thread holds the same chunk (tid % 8); with d a
   // multiple of 32 only, the upper half of the last K step reads zeros
   const int kch = 8 * (tid % CH);
-  uint4 xa[4], qb[2];
+  uint4 xa[4], qb[BL];
   long xoff = 0;                                      // component offset (max-dot form: px walked here)
   auto load = [&](int k0) {
     const bool kin = k0 + kch < D;
@@ -141,24 +157,23 @@ __global__ __launch_bounds__(256) void k_dots_mfma(DevProb pr, int n0, int nt, i
     for (int i = 0; i < 4; ++i)
       xa[i] = kin ? *reinterpret_cast<const uint4*>(xsrc[i] + xoff + k0) : make_uint4(0, 0, 0, 0);
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int i = 0; i < BL; ++i)
       qb[i] = kin && vok[i] ? *reinterpret_cast<const uint4*>(qsrc[i] + k0) : make_uint4(0, 0, 0, 0);
   };
   auto store = [&](int buf) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) sA[buf * TI * CH + aslot[i]] = xa[i];
 #pragma unroll
-    for (int i = 0; i < 2; ++i) sB[buf * TV * CH + bslot[i]] = qb[i];
+    for (int i = 0; i < BL; ++i) sB[buf * TV * CH + bslot[i]] = qb[i];
   };
   const int nk = (D + KS - 1) / KS;
   // max-dot form: every component of the items in turn, keeping the
   // elementwise maximum of the dot tiles
-  f32x16_t run[2] = {f32x16_t{}, f32x16_t{}};
+  f32x16_t run[2][NBV];
   const int npx = MODE == kDotsToMaxKeys ? pr.Px : 1;
   for (int cx = 0; cx < npx; ++cx) {
     xoff = MODE == kDotsToMaxKeys ? static_cast<long>(cx) * N * D : 0l;
-    acc[0] = f32x16_t{};
-    acc[1] = f32x16_t{};
+    zero_acc();
     load(0);
     store(0);
     __syncthreads();
@@ -168,12 +183,18 @@ __global__ __launch_bounds__(256) void k_dots_mfma(DevProb pr, int n0, int nt, i
       if (more) load(KS * (kk + 1));
 #pragma unroll
       for (int kb = 0; kb < KS / 16; ++kb) {             // K blocks of 16
-        const uint4 b = sB[cur * TV * CH + rb * CH + dots_swz8(rb, 2 * kb + h)];
+        uint4 bv[NBV];
+#pragma unroll
+        for (int jb = 0; jb < NBV; ++jb) {
+          const int rb = wn * (TV / 2) + jb * 32 + c;    // B row (vector)
+          bv[jb] = sB[cur * TV * CH + rb * CH + dots_swz8(rb, 2 * kb + h)];
+        }
 #pragma unroll
         for (int ib = 0; ib < 2; ++ib) {
           const int ra = wm * 64 + ib * 32 + c;           // A row (item)
           const uint4 a = sA[cur * TI * CH + ra * CH + dots_swz8(ra, 2 * kb + h)];
-          acc[ib] = mfma32x16_bf16(a, b, acc[ib]);
+#pragma unroll
+          for (int jb = 0; jb < NBV; ++jb) acc[ib][jb] = mfma32x16_bf16(a, bv[jb], acc[ib][jb]);
         }
       }
       if (more) store(cur ^ 1);
@@ -183,107 +204,120 @@ __global__ __launch_bounds__(256) void k_dots_mfma(DevProb pr, int n0, int nt, i
 #pragma unroll
       for (int ib = 0; ib < 2; ++ib)
 #pragma unroll
-        for (int e = 0; e < 16; ++e) run[ib][e] = cx == 0 ? acc[ib][e] : fmaxf(run[ib][e], acc[ib][e]);
+        for (int jb = 0; jb < NBV; ++jb)
+#pragma unroll
+          for (int e = 0; e < 16; ++e)
+            run[ib][jb][e] = cx == 0 ? acc[ib][jb][e] : fmaxf(run[ib][jb][e], acc[ib][jb][e]);
     }
   }
   if (MODE == kDotsToMaxKeys) {
-    acc[0] = run[0];
-    acc[1] = run[1];
+#pragma unroll
+    for (int ib = 0; ib < 2; ++ib)
+#pragma unroll
+      for (int jb = 0; jb < NBV; ++jb) acc[ib][jb] = run[ib][jb];
   }
 
-  // The loop ended with a barrier: the staging area is free.  The tile goes
-  // through LDS (rows padded to TR floats) so that every global store
-  // instruction writes a contiguous run of one row.
+  // The loop ended with a barrier: the staging area is free.  Each 64-row
+  // half of the tile goes through LDS (rows padded to TR floats) so that
+  // every global store instruction writes a contiguous run of one row.
   float* sT = reinterpret_cast<float*>(smem);
 #pragma unroll
-  for (int ib = 0; ib < 2; ++ib)
+  for (int hv = 0; hv < HALVES; ++hv) {
+    if (hv > 0) __syncthreads();                       // the previous half has been written out
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
-      *reinterpret_cast<float4*>(sT + rb * TR + wm * 64 + ib * 32 + 8 * j + 4 * h) =
-          float4{acc[ib][4 * j + 0], acc[ib][4 * j + 1], acc[ib][4 * j + 2], acc[ib][4 * j + 3]};
-  __syncthreads();
-  if (MODE == kDotsToMaxKeys) {
-    // m = max over the tile's P_q rows of each query (64 % P_q == 0, so a
-    // query's rows are one run of the tile); wave w takes queries w, w+4, ...
-    const int nq = TV / pr.Pq, b0 = v0 / pr.Pq;
-    for (int qi = wave; qi < nq; qi += 4) {
-      const int b = b0 + qi;
-      if (b >= pr.B) break;                            // wave-uniform; queries ascend
-      uint64_t* dst = keys + static_cast<long>(b) * key_stride;
+    for (int jb = 0; jb < NBV; ++jb) {
+      const int row = wn * (TV / 2) + jb * 32 - 64 * hv;   // first tile row of block jb, in this half
+      if (row < 0 || row >= 64) continue;                  // wave-uniform
 #pragma unroll
-      for (int t = 0; t < 2; ++t) {
+      for (int ib = 0; ib < 2; ++ib)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          *reinterpret_cast<float4*>(sT + (row + c) * TR + wm * 64 + ib * 32 + 8 * j + 4 * h) =
+              float4{acc[ib][jb][4 * j + 0], acc[ib][jb][4 * j + 1], acc[ib][jb][4 * j + 2], acc[ib][jb][4 * j + 3]};
+    }
+    __syncthreads();
+    const int vh = v0 + 64 * hv;                       // first vector of the half
+    if (MODE == kDotsToMaxKeys) {
+      // m = max over each query's P_q rows (P_q divides 64, so a query's rows
+      // are one run of the half); wave w takes queries w, w+4, ...
+      const int nq = 64 / pr.Pq, b0 = vh / pr.Pq;
+      for (int qi = wave; qi < nq; qi += 4) {
+        const int b = b0 + qi;
+        if (b >= pr.B) break;                            // wave-uniform; queries ascend
+        uint64_t* dst = keys + static_cast<long>(b) * key_stride;
+#pragma unroll
+        for (int t = 0; t < 2; ++t) {
+          const int i = it0 + 64 * t + lane;
+          float m = sT[(qi * pr.Pq) * TR + 64 * t + lane];
+          for (int pq = 1; pq < pr.Pq; ++pq) m = fmaxf(m, sT[(qi * pr.Pq + pq) * TR + 64 * t + lane]);
+          if (i < cnt) dst[i] = make_key(m, n0 + i);
+        }
+      }
+    } else if (MODE == kDotsToCandidates) {
+      // Two passes over the wave's 16 rows: count the keys each row keeps
+      // (row rr's count lands in lane rr), reserve every row's slots with
+      // one atomic add per row issued by lanes 0..15 together, then store.
+      const int nrows = max(0, min(16, v1 - vh - wave * 16));
+      auto kept = [&](int rr, int t, uint64_t th, uint64_t& key) {
         const int i = it0 + 64 * t + lane;
-        float m = sT[(qi * pr.Pq) * TR + 64 * t + lane];
-        for (int pq = 1; pq < pr.Pq; ++pq) m = fmaxf(m, sT[(qi * pr.Pq + pq) * TR + 64 * t + lane]);
-        if (i < cnt) dst[i] = make_key(m, n0 + i);
-      }
-    }
-    return;
-  }
-  if (MODE == kDotsToCandidates) {
-    // Two passes over the wave's 16 rows: count the keys each row keeps
-    // (row rr's count lands in lane rr), reserve every row's slots with one
-    // atomic add per row issued by lanes 0..15 together, then store.
-    const int nrows = max(0, min(TV / 4, v1 - v0 - wave * (TV / 4)));
-    auto kept = [&](int rr, int t, uint64_t th, uint64_t& key) {
-      const int i = it0 + 64 * t + lane;
-      key = i < cnt ? make_key(sT[(wave * (TV / 4) + rr) * TR + 64 * t + lane], n0 + i) : 0ull;
-      return key != 0ull && key >= th;
-    };
-    uint32_t row_hits = 0;                              // lane rr: keys kept by row rr
-    for (int rr = 0; rr < nrows; ++rr) {
-      const uint64_t th = static_cast<uint64_t>(__shfl(static_cast<long long>(thr_lane), rr, 64));
-      uint32_t n = 0;
+        key = i < cnt ? make_key(sT[(wave * 16 + rr) * TR + 64 * t + lane], n0 + i) : 0ull;
+        return key != 0ull && key >= th;
+      };
+      uint32_t row_hits = 0;                              // lane rr: keys kept by row rr
+      for (int rr = 0; rr < nrows; ++rr) {
+        const uint64_t th = static_cast<uint64_t>(__shfl(static_cast<long long>(thr_lane[hv]), rr, 64));
+        uint32_t n = 0;
 #pragma unroll
-      for (int t = 0; t < 2; ++t) {
-        uint64_t key;
-        n += static_cast<uint32_t>(__popcll(__ballot(kept(rr, t, th, key))));
+        for (int t = 0; t < 2; ++t) {
+          uint64_t key;
+          n += static_cast<uint32_t>(__popcll(__ballot(kept(rr, t, th, key))));
+        }
+        if (lane == rr) row_hits = n;
       }
-      if (lane == rr) row_hits = n;
-    }
-    auto row_list = [&](int rr) {
-      const int v = v0 + wave * (TV / 4) + rr;
-      const int b = v / pr.Pq, pq = v - (v / pr.Pq) * pr.Pq;
-      return static_cast<long>(b) * pr.P + pq * pr.Px + px;
-    };
-    uint32_t row_base = 0;
-    if (lane < nrows && row_hits > 0) row_base = atomicAdd(counts + row_list(lane), row_hits);
-    for (int rr = 0; rr < nrows; ++rr) {
-      if (__shfl(row_hits, rr, 64) == 0u) continue;     // wave-uniform
-      const uint64_t th = static_cast<uint64_t>(__shfl(static_cast<long long>(thr_lane), rr, 64));
-      uint32_t pos = __shfl(row_base, rr, 64);
-      uint64_t* dst = keys + row_list(rr) * key_stride;
+      auto row_list = [&](int rr) {
+        const int v = vh + wave * 16 + rr;
+        const int b = v / pr.Pq, pq = v - (v / pr.Pq) * pr.Pq;
+        return static_cast<long>(b) * pr.P + pq * pr.Px + px;
+      };
+      uint32_t row_base = 0;
+      if (lane < nrows && row_hits > 0) row_base = atomicAdd(counts + row_list(lane), row_hits);
+      for (int rr = 0; rr < nrows; ++rr) {
+        if (__shfl(row_hits, rr, 64) == 0u) continue;     // wave-uniform
+        const uint64_t th = static_cast<uint64_t>(__shfl(static_cast<long long>(thr_lane[hv]), rr, 64));
+        uint32_t pos = __shfl(row_base, rr, 64);
+        uint64_t* dst = keys + row_list(rr) * key_stride;
 #pragma unroll
-      for (int t = 0; t < 2; ++t) {
-        uint64_t key;
-        const bool hit = kept(rr, t, th, key);
-        const uint64_t mask = __ballot(hit);
-        const uint32_t below = __builtin_amdgcn_mbcnt_hi(static_cast<uint32_t>(mask >> 32),
-                                                         __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(mask), 0u));
-        if (hit) dst[pos + below] = key;
-        pos += static_cast<uint32_t>(__popcll(mask));
+        for (int t = 0; t < 2; ++t) {
+          uint64_t key;
+          const bool hit = kept(rr, t, th, key);
+          const uint64_t mask = __ballot(hit);
+          const uint32_t below = __builtin_amdgcn_mbcnt_hi(static_cast<uint32_t>(mask >> 32),
+                                                           __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(mask), 0u));
+          if (hit) dst[pos + below] = key;
+          pos += static_cast<uint32_t>(__popcll(mask));
+        }
       }
-    }
-    return;
-  }
-  // each wave writes 16 of the tile's vector rows
-  for (int rr = 0; rr < TV / 4; ++rr) {
-    const int r = wave * (TV / 4) + rr;
-    const int v = v0 + r;
-    if (v >= v1) break;                                // rows ascend: the rest are past the end too
-    const int b = v / pr.Pq, pq = v - (v / pr.Pq) * pr.Pq;
-    const int p = pq * pr.Px + px;
-    if (MODE == kDotsToBuffer) {
-      // the buffer rows are padded to whole 128-item tiles
-      const float2 val = *reinterpret_cast<const float2*>(sT + r * TR + 2 * lane);
-      *reinterpret_cast<float2*>(sbuf + p * s_pstride + b * s_bstride + it0 + 2 * lane) = val;
     } else {
-      uint64_t* dst = keys + (static_cast<long>(b) * pr.P + p) * key_stride;
+      // each wave writes 16 of the half's vector rows
+      for (int rr = 0; rr < 16; ++rr) {
+        const int r = wave * 16 + rr;
+        const int v = vh + r;
+        if (v >= v1) break;                                // rows ascend: the rest are past the end too
+        const int b = v / pr.Pq, pq = v - (v / pr.Pq) * pr.Pq;
+        const int p = pq * pr.Px + px;
+        if (MODE == kDotsToBuffer) {
+          // the buffer rows are padded to whole 128-item tiles
+          const float2 val = *reinterpret_cast<const float2*>(sT + r * TR + 2 * lane);
+          *reinterpret_cast<float2*>(sbuf + p * s_pstride + b * s_bstride + it0 + 2 * lane) = val;
+        } else {
+          uint64_t* dst = keys + (static_cast<long>(b) * pr.P + p) * key_stride;
 #pragma unroll
-      for (int t = 0; t < 2; ++t) {
-        const int i = it0 + 64 * t + lane;
-        if (i < cnt) dst[ot0 + 64 * t + lane] = make_key(sT[r * TR + 64 * t + lane], n0 + i);
-        else if (tile_stride > 1) dst[ot0 + 64 * t + lane] = 0ull;
+          for (int t = 0; t < 2; ++t) {
+            const int i = it0 + 64 * t + lane;
+            if (i < cnt) dst[ot0 + 64 * t + lane] = make_key(sT[r * TR + 64 * t + lane], n0 + i);
+            else if (tile_stride > 1) dst[ot0 + 64 * t + lane] = 0ull;
+          }
+        }
       }
     }
   }
@@ -295,36 +329,55 @@ bool dots_mfma_supported(const DevProb& pr) {
 
 long dots_buffer_row(int nt) { return (static_cast<long>(nt) + 127) / 128 * 128; }
 
+// 128-vector tiles when there are at least 128 query vectors
+static int dots_tv(const DevProb& pr) { return pr.B * pr.Pq >= 128 ? 128 : 64; }
+
+template <int MODE>
+static void dots_launch(int tv, dim3 grid, hipStream_t st, const DevProb& pr, int n0, int nt, int tile_stride,
+                        const int32_t* items, const int32_t* item_count, long item_stride, float* sbuf,
+                        long s_pstride, long s_bstride, uint64_t* keys, long key_stride, const uint64_t* thr,
+                        long thr_stride, uint32_t* counts) {
+  if (tv == 128)
+    hipLaunchKernelGGL((k_dots_mfma<MODE, 128>), grid, dim3(256), 0, st, pr, n0, nt, tile_stride, items,
+                       item_count, item_stride, sbuf, s_pstride, s_bstride, keys, key_stride, thr, thr_stride,
+                       counts);
+  else
+    hipLaunchKernelGGL((k_dots_mfma<MODE, 64>), grid, dim3(256), 0, st, pr, n0, nt, tile_stride, items,
+                       item_count, item_stride, sbuf, s_pstride, s_bstride, keys, key_stride, thr, thr_stride,
+                       counts);
+}
+
 hipError_t launch_dots_mfma(const DevProb& pr, int n0, int nt, int mode, float* sbuf, long s_pstride,
                             long s_bstride, uint64_t* keys, long key_stride, hipStream_t st, int tile_stride) {
   if (nt <= 0) return hipSuccess;
   if (tile_stride < 1 || (tile_stride > 1 && mode != kDotsToKeys)) return hipErrorInvalidValue;
-  const int nvec = pr.B * pr.Pq;
+  const int tv = dots_tv(pr);
   const int tiles = (nt + 127) / 128;
-  const dim3 grid((tiles + tile_stride - 1) / tile_stride, (nvec + 63) / 64, pr.Px);
+  const dim3 grid((tiles + tile_stride - 1) / tile_stride, (pr.B * pr.Pq + tv - 1) / tv, pr.Px);
   if (mode == kDotsToBuffer)
-    hipLaunchKernelGGL(k_dots_mfma<kDotsToBuffer>, grid, dim3(256), 0, st, pr, n0, nt, 1, nullptr, nullptr, 0l,
-                       sbuf, s_pstride, s_bstride, nullptr, 0l, nullptr, 0l, nullptr);
+    dots_launch<kDotsToBuffer>(tv, grid, st, pr, n0, nt, 1, nullptr, nullptr, 0l, sbuf, s_pstride, s_bstride,
+                               nullptr, 0l, nullptr, 0l, nullptr);
   else
-    hipLaunchKernelGGL(k_dots_mfma<kDotsToKeys>, grid, dim3(256), 0, st, pr, n0, nt, tile_stride, nullptr,
-                       nullptr, 0l, nullptr, 0l, 0l, keys, key_stride, nullptr, 0l, nullptr);
+    dots_launch<kDotsToKeys>(tv, grid, st, pr, n0, nt, tile_stride, nullptr, nullptr, 0l, nullptr, 0l, 0l, keys,
+                             key_stride, nullptr, 0l, nullptr);
   return hipGetLastError();
 }
 
-// keys per row of the keys form: nt (tile_stride 1: exactly the range's
-// keys are written), else whole sampled tiles (slots past the range cleared)
 bool dots_maxkeys_supported(const DevProb& pr) { return dots_mfma_supported(pr) && 64 % pr.Pq == 0; }
 
 hipError_t launch_dots_mfma_maxkeys(const DevProb& pr, int n0, int nt, uint64_t* keys, long key_stride,
                                     hipStream_t st) {
   if (nt <= 0) return hipSuccess;
   if (!dots_maxkeys_supported(pr)) return hipErrorInvalidValue;
-  const dim3 grid((nt + 127) / 128, (pr.B * pr.Pq + 63) / 64, 1);
-  hipLaunchKernelGGL(k_dots_mfma<kDotsToMaxKeys>, grid, dim3(256), 0, st, pr, n0, nt, 1, nullptr, nullptr, 0l,
-                     nullptr, 0l, 0l, keys, key_stride, nullptr, 0l, nullptr);
+  const int tv = dots_tv(pr);
+  const dim3 grid((nt + 127) / 128, (pr.B * pr.Pq + tv - 1) / tv, 1);
+  dots_launch<kDotsToMaxKeys>(tv, grid, st, pr, n0, nt, 1, nullptr, nullptr, 0l, nullptr, 0l, 0l, keys, key_stride,
+                              nullptr, 0l, nullptr);
   return hipGetLastError();
 }
 
+// keys per row of the keys form: nt (tile_stride 1: exactly the range's
+// keys are written), else whole sampled tiles (slots past the range cleared)
 long dots_sample_len(int nt, int tile_stride) {
   return tile_stride == 1 ? nt : ((nt + 127) / 128 + tile_stride - 1) / tile_stride * 128l;
 }
@@ -332,10 +385,10 @@ long dots_sample_len(int nt, int tile_stride) {
 hipError_t launch_dots_mfma_candidates(const DevProb& pr, int n0, int nt, const uint64_t* thr, long thr_stride,
                                        uint64_t* cand, long cand_stride, uint32_t* counts, hipStream_t st) {
   if (nt <= 0) return hipSuccess;
-  const int nvec = pr.B * pr.Pq;
-  const dim3 grid((nt + 127) / 128, (nvec + 63) / 64, pr.Px);
-  hipLaunchKernelGGL(k_dots_mfma<kDotsToCandidates>, grid, dim3(256), 0, st, pr, n0, nt, 1, nullptr, nullptr,
-                     0l, nullptr, 0l, 0l, cand, cand_stride, thr, thr_stride, counts);
+  const int tv = dots_tv(pr);
+  const dim3 grid((nt + 127) / 128, (pr.B * pr.Pq + tv - 1) / tv, pr.Px);
+  dots_launch<kDotsToCandidates>(tv, grid, st, pr, n0, nt, 1, nullptr, nullptr, 0l, nullptr, 0l, 0l, cand,
+                                 cand_stride, thr, thr_stride, counts);
   return hipGetLastError();
 }
 
@@ -345,8 +398,8 @@ hipError_t launch_dots_mfma_gather(const DevProb& pr, const int32_t* items, cons
   if (C <= 0) return hipSuccess;
   if (pr.Pq > 64) return hipErrorInvalidValue;
   const dim3 grid((C + 127) / 128, pr.B, pr.Px);
-  hipLaunchKernelGGL(k_dots_mfma<kDotsToBuffer>, grid, dim3(256), 0, st, pr, 0, C, 1, items, item_count,
-                     item_stride, sbuf, s_pstride, s_bstride, nullptr, 0l, nullptr, 0l, nullptr);
+  dots_launch<kDotsToBuffer>(64, grid, st, pr, 0, C, 1, items, item_count, item_stride, sbuf, s_pstride, s_bstride,
+                             nullptr, 0l, nullptr, 0l, nullptr);
   return hipGetLastError();
 }
 

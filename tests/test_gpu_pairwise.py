@@ -31,6 +31,9 @@ SHAPES = [
     ("p64_h128_d64", 8, 8, 64, 128, True),   # P_q = 8 but (P_x, d, H) unfused
     ("p16_h160_d64", 4, 4, 64, 160, True),
 ]
+# (name, B): enough queries for 128-vector tiles of the dots GEMM, with a
+# ragged last tile
+MANY = [("b40_pq4", 40), ("b33_pq4", 33)]
 
 
 def _spec(Pq, Px, d, H, side):
@@ -68,3 +71,54 @@ def test_pairwise_shapes(name, Pq, Px, d, H, side):
         check_topk_row(full, ri[b], rs[b], k, f"pairwise_rerank {name} query {b}")
         m = mo.all_dots(op, b).max(axis=1)
         check_topk_row(m, mi[b], ms[b], k, f"pairwise_maxdot {name} query {b}")
+
+
+@pytest.mark.parametrize("name,B", MANY, ids=[m[0] for m in MANY])
+def test_pairwise_many_queries(name, B):
+    """The same checks with 132 to 160 query vectors: the dots GEMM takes
+    128-vector tiles (the rerank's per-query tiles stay at 64)."""
+    spec = dataclasses.replace(_spec(4, 4, 64, 64, True), B=B, N=2131)
+    k = 50
+    log(f"[pairwise many] {name} B={spec.B} N={spec.N} P={spec.P}")
+    inp = cuda_inputs(spec, seed=62)
+    prob = mol.Problem.from_inputs(inp)
+    s, i = mol.topk_exact(prob, k)
+    g = torch.Generator(device="cuda").manual_seed(10)
+    cand = torch.randint(0, spec.N, (spec.B, 200), device="cuda", generator=g, dtype=torch.int32)
+    rs, ri, rn = mol.rerank(prob, cand, k)
+    ms, mi = mol.topk_maxdot(mol.Problem(inp.Q, inp.X), k)
+    bs, bi = mol.topk_exact_bounded(prob, k, s[:, k - 1].contiguous())
+    torch.cuda.synchronize()
+    assert torch.equal(bi, i) and torch.equal(bs, s), f"{name}: bounded pass differs from brute force"
+    op = oracle_problem(inp)
+    phi = mo.mol_scores(op, list(range(spec.B)))
+    s, i = s.cpu().numpy(), i.cpu().numpy()
+    rs, ri = rs.cpu().numpy(), ri.cpu().numpy()
+    ms, mi = ms.cpu().numpy(), mi.cpu().numpy()
+    cand = cand.cpu().numpy()
+    for b in range(spec.B):
+        check_topk_row(phi[b], i[b], s[b], k, f"pairwise {name} query {b}")
+        uniq = mo.union_dedup([cand[b]])
+        full = np.full(spec.N, -np.inf)
+        full[uniq] = phi[b][uniq]
+        check_topk_row(full, ri[b], rs[b], k, f"pairwise_rerank {name} query {b}")
+        m = mo.all_dots(op, b).max(axis=1)
+        check_topk_row(m, mi[b], ms[b], k, f"pairwise_maxdot {name} query {b}")
+
+
+def test_thresholded_lists_many_queries():
+    """Per-component lists through the sampled threshold with 136 query
+    vectors (128-vector tiles of the sample and kept-key passes); d = 96 has
+    no fused per-component kernel."""
+    spec = dataclasses.replace(_spec(4, 4, 96, 64, True), B=34, N=16500)
+    kp = 20
+    log(f"[thresholded many] B={spec.B} N={spec.N} k'={kp}")
+    inp = cuda_inputs(spec, seed=63)
+    dots, ids = mol.topk_per_embd(mol.Problem(inp.Q, inp.X), kp)
+    torch.cuda.synchronize()
+    op = oracle_problem(inp)
+    dots, ids = dots.cpu().numpy(), ids.cpu().numpy()
+    for b in range(spec.B):
+        s_all = mo.all_dots(op, b)
+        for p in range(spec.P):
+            check_topk_row(s_all[:, p], ids[b, p], dots[b, p], kp, f"thresholded_many b={b} p={p}")
