@@ -258,20 +258,21 @@ __global__ __launch_bounds__(256) void k_dots_mfma(DevProb pr, int n0, int nt, i
       // (row rr's count lands in lane rr), reserve every row's slots with
       // one atomic add per row issued by lanes 0..15 together, then store.
       const int nrows = max(0, min(16, v1 - vh - wave * 16));
-      auto kept = [&](int rr, int t, uint64_t th, uint64_t& key) {
+      // a key reaches th iff its score beats th's, or ties it with an index
+      // that keeps the key at or above th: the float compare decides almost
+      // every item, and the key is formed only for the kept ones
+      auto kept = [&](int rr, int t, uint64_t th, float ts) {
         const int i = it0 + 64 * t + lane;
-        key = i < cnt ? make_key(sT[(wave * 16 + rr) * TR + 64 * t + lane], n0 + i) : 0ull;
-        return key != 0ull && key >= th;
+        const float v = sT[(wave * 16 + rr) * TR + 64 * t + lane];
+        return i < cnt && v >= ts && (v > ts || make_key(v, n0 + i) >= th);
       };
       uint32_t row_hits = 0;                              // lane rr: keys kept by row rr
       for (int rr = 0; rr < nrows; ++rr) {
         const uint64_t th = static_cast<uint64_t>(__shfl(static_cast<long long>(thr_lane[hv]), rr, 64));
+        const float ts = key_score(th);
         uint32_t n = 0;
 #pragma unroll
-        for (int t = 0; t < 2; ++t) {
-          uint64_t key;
-          n += static_cast<uint32_t>(__popcll(__ballot(kept(rr, t, th, key))));
-        }
+        for (int t = 0; t < 2; ++t) n += static_cast<uint32_t>(__popcll(__ballot(kept(rr, t, th, ts))));
         if (lane == rr) row_hits = n;
       }
       auto row_list = [&](int rr) {
@@ -284,16 +285,19 @@ __global__ __launch_bounds__(256) void k_dots_mfma(DevProb pr, int n0, int nt, i
       for (int rr = 0; rr < nrows; ++rr) {
         if (__shfl(row_hits, rr, 64) == 0u) continue;     // wave-uniform
         const uint64_t th = static_cast<uint64_t>(__shfl(static_cast<long long>(thr_lane[hv]), rr, 64));
+        const float ts = key_score(th);
         uint32_t pos = __shfl(row_base, rr, 64);
         uint64_t* dst = keys + row_list(rr) * key_stride;
 #pragma unroll
         for (int t = 0; t < 2; ++t) {
-          uint64_t key;
-          const bool hit = kept(rr, t, th, key);
+          const bool hit = kept(rr, t, th, ts);
           const uint64_t mask = __ballot(hit);
           const uint32_t below = __builtin_amdgcn_mbcnt_hi(static_cast<uint32_t>(mask >> 32),
                                                            __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(mask), 0u));
-          if (hit) dst[pos + below] = key;
+          if (hit) {
+            const int i = it0 + 64 * t + lane;
+            dst[pos + below] = make_key(sT[(wave * 16 + rr) * TR + 64 * t + lane], n0 + i);
+          }
           pos += static_cast<uint32_t>(__popcll(mask));
         }
       }
