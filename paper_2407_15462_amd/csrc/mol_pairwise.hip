@@ -19,6 +19,10 @@
 // run p = base(g) + mu, mu < 2 PXV, of the padded layout.  Modes and
 // outputs are those of the one-thread-per-pair kernel (GenMode); the
 // max-component mode, which has no gating chain, is left to that kernel.
+// PXV = 2 stands for P' = 16: the K = 16 gating chain (MolMlp16), whose lane
+// runs are p = 4 g + mu, mu < 4.
+#include <type_traits>
+
 #include "mol_tile.h"
 
 namespace mol {
@@ -43,12 +47,12 @@ __global__ __launch_bounds__(256) void k_phi_mfma(
     const int32_t* __restrict__ items, const int32_t* __restrict__ item_count, long item_stride,
     const float* __restrict__ sbuf, long s_pstride, long s_bstride,
     float* __restrict__ phi, long phi_stride, uint64_t* __restrict__ keys, long key_stride) {
-  using Mlp = MolMlp<PXV, HV>;
+  using Mlp = std::conditional_t<PXV == 2, MolMlp16<HV>, MolMlp<PXV, HV>>;
   constexpr int RUN = Mlp::RUN, PT = Mlp::PT;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int c = lane & 15, g = lane >> 4;
   const int P = pr.P;
-  const int base = lane_base(g, PXV);
+  const int base = Mlp::base(g);
   const int b0 = blockIdx.y * kPairQB, nq = min(kPairQB, pr.B - b0);
 
   Mlp mlp;
@@ -232,7 +236,11 @@ hipError_t launch_phi_mfma(const DevProb& pr, int mode, const float* bound, int 
   launch_phi_mfma_t<PXV, HV>(grid, pr, mode, bound, n_begin, n_count, static_cast<int>(steps), items,     \
                              item_count, item_stride, sbuf,                                                \
                              s_pstride, s_bstride, phi, phi_stride, keys, key_stride, st)
-  if (pr.P <= 32) {
+  if (pr.P <= 16) {
+    if (pr.H <= 32) MOL_PHI_MFMA(2, 32);
+    else if (pr.H <= 64) MOL_PHI_MFMA(2, 64);
+    else MOL_PHI_MFMA(2, 128);
+  } else if (pr.P <= 32) {
     if (pr.H <= 32) MOL_PHI_MFMA(4, 32);
     else if (pr.H <= 64) MOL_PHI_MFMA(4, 64);
     else MOL_PHI_MFMA(4, 128);

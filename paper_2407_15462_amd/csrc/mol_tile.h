@@ -240,6 +240,25 @@ struct WaveTopk {
   }
 };
 
+// Sums over the 4 lanes {c, c+16, c+32, c+48} of an item of two (den,
+// num) pairs a and b: three swaps, no copies.  The rows of 16 lanes end
+// up holding a's sums (rows 0, 1) and b's (rows 2, 3); each lane returns
+// the pair of its rows.  The additions pair rows (0 + 1) + (2 + 3), as
+// sum_groups does.
+__device__ __forceinline__ void row_sums(float da, float na, float db, float nb, float& den, float& num) {
+  auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(da), __float_as_uint(na), false, false);
+  const float sa = __uint_as_float(a[0]) + __uint_as_float(a[1]);   // rows: da01, na01, da23, na23
+  auto b = __builtin_amdgcn_permlane16_swap(__float_as_uint(db), __float_as_uint(nb), false, false);
+  const float sb = __uint_as_float(b[0]) + __uint_as_float(b[1]);   // rows: db01, nb01, db23, nb23
+  auto u = __builtin_amdgcn_permlane32_swap(__float_as_uint(sa), __float_as_uint(sb), false, false);
+  const float t = __uint_as_float(u[0]) + __uint_as_float(u[1]);    // rows: da, na, db, nb
+  const uint32_t tb = __float_as_uint(t);
+  auto v = __builtin_amdgcn_permlane16_swap(tb, tb, false, false);
+  den = __uint_as_float(v[0]);                                       // rows: da, da, db, db
+  num = __uint_as_float(v[1]);                                       // rows: na, na, nb, nb
+}
+
+
 // Per-wave constants of the gating MLP in MFMA operand layouts.
 template <int PX, int H>
 struct MolMlp {
@@ -250,6 +269,8 @@ struct MolMlp {
   static constexpr int KH = H / 32;   // K blocks of GEMM3
   static constexpr int PT = P / 16;   // output tiles of GEMM3
   static_assert(PT <= 4, "a_q + b2 operand holds at most 4 tiles");
+  // first component of the run held by lane group g
+  __device__ static int base(int g) { return lane_base(g, PX); }
   uint4 w1op[JT][KP];
   uint4 w2op[PT][KH];
   f32x4_t b1acc[JT];
@@ -414,24 +435,6 @@ struct MolMlp {
     num = n[0] + n[1];
   }
 
-  // Sums over the 4 lanes {c, c+16, c+32, c+48} of an item of two (den,
-  // num) pairs a and b: three swaps, no copies.  The rows of 16 lanes end
-  // up holding a's sums (rows 0, 1) and b's (rows 2, 3); each lane returns
-  // the pair of its rows.  The additions pair rows (0 + 1) + (2 + 3), as
-  // sum_groups does.
-  __device__ static void row_sums(float da, float na, float db, float nb, float& den, float& num) {
-    auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(da), __float_as_uint(na), false, false);
-    const float sa = __uint_as_float(a[0]) + __uint_as_float(a[1]);   // rows: da01, na01, da23, na23
-    auto b = __builtin_amdgcn_permlane16_swap(__float_as_uint(db), __float_as_uint(nb), false, false);
-    const float sb = __uint_as_float(b[0]) + __uint_as_float(b[1]);   // rows: db01, nb01, db23, nb23
-    auto u = __builtin_amdgcn_permlane32_swap(__float_as_uint(sa), __float_as_uint(sb), false, false);
-    const float t = __uint_as_float(u[0]) + __uint_as_float(u[1]);    // rows: da, na, db, nb
-    const uint32_t tb = __float_as_uint(t);
-    auto v = __builtin_amdgcn_permlane16_swap(tb, tb, false, false);
-    den = __uint_as_float(v[0]);                                       // rows: da, da, db, db
-    num = __uint_as_float(v[1]);                                       // rows: na, na, nb, nb
-  }
-
   // phi for the lane's item under NQ (1 or 2) queries: out[q] is valid in
   // the lanes of query q's rows (NQ = 2: rows 0-1 for query 0, rows 2-3 for
   // query 1; NQ = 1: every lane).  The queries' chains are independent and
@@ -465,6 +468,146 @@ struct MolMlp {
         for (int pt = 0; pt < PT; ++pt)
 #pragma unroll
           for (int i = 0; i < 4; ++i) mx = fmaxf(mx, lg[pt][i]);
+        weights(lg, s[q], max_groups(mx), den[q], num[q]);
+      }
+      row_sums(den[0], num[0], den[NQ - 1], num[NQ - 1], D, Nm);
+    }
+    const float v = Nm * __builtin_amdgcn_rcpf(D);
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) out[q] = v;
+  }
+};
+
+
+// The gating chain for P <= 16 components: GEMM2 on 16x16x16 f16 MFMAs
+// (K = 16 = P'), so lane (c, g) holds item c's components p = 4 g + e,
+// e < 4, and GEMM3 has one output tile whose row 4 g + i is p = 4 g + i:
+// no padding of P to 32.  Same interface as MolMlp (pr.P <= 16, pr.H <= H).
+typedef _Float16 f16x4_t __attribute__((ext_vector_type(4)));
+template <int H>
+struct MolMlp16 {
+  static constexpr int P = 16;
+  static constexpr int RUN = 4;
+  static constexpr int JT = H / 16;   // output tiles of GEMM2
+  static constexpr int KH = H / 32;   // K blocks of GEMM3
+  static constexpr int PT = 1;        // output tiles of GEMM3
+  uint2 w1op[JT];
+  uint4 w2op[KH];
+  f32x4_t b1acc[JT];
+  __device__ static int base(int g) { return 4 * g; }
+
+  __device__ void load_padded(const DevProb& pr, int c, int g) {
+    const bf16_t* W1 = static_cast<const bf16_t*>(pr.W1);
+    const bf16_t* W2 = static_cast<const bf16_t*>(pr.W2);
+    const int Pr = pr.P, Hr = pr.H;
+    // unconditional reads from clamped indices, masked afterwards
+    auto w1 = [&](int j, int p) -> uint32_t {
+      const bf16_t w = W1[min(j, Hr - 1) * Pr + min(p, Pr - 1)];
+      const uint32_t keep = 0u - static_cast<uint32_t>((j < Hr) & (p < Pr));
+      return neg_bf16_to_f16_bits(w, kLog2e) & keep;
+    };
+    auto w2 = [&](int p, int j) -> uint32_t {
+      const bf16_t w = W2[min(p, Pr - 1) * Hr + min(j, Hr - 1)];
+      const uint32_t keep = 0u - static_cast<uint32_t>((j < Hr) & (p < Pr));
+      return neg_bf16_to_f16_bits(w, 1.f) & keep;
+    };
+    // W1' = -log2(e) W1: row j = 16 jt + c, K slot 4 g + e <-> p = 4 g + e
+#pragma unroll
+    for (int jt = 0; jt < JT; ++jt) {
+      const int j = 16 * jt + c;
+      w1op[jt] = make_uint2(w1(j, 4 * g) | (w1(j, 4 * g + 1) << 16), w1(j, 4 * g + 2) | (w1(j, 4 * g + 3) << 16));
+    }
+    // -W2: row c <-> p = c; K slot 8 g + e of block m <-> j as in MolMlp
+#pragma unroll
+    for (int m = 0; m < KH; ++m) {
+      uint32_t w[4];
+#pragma unroll
+      for (int e2 = 0; e2 < 4; ++e2) {
+        const int e0 = 2 * e2, e1 = 2 * e2 + 1;
+        const int j0 = 32 * m + 16 * (e0 >> 2) + 4 * g + (e0 & 3);
+        const int j1 = 32 * m + 16 * (e1 >> 2) + 4 * g + (e1 & 3);
+        w[e2] = w2(c, j0) | (w2(c, j1) << 16);
+      }
+      w2op[m] = make_uint4(w[0], w[1], w[2], w[3]);
+    }
+#pragma unroll
+    for (int jt = 0; jt < JT; ++jt)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int j = 16 * jt + 4 * g + i;
+        const float b = pr.b1[min(j, Hr - 1)];
+        b1acc[jt][i] = j < Hr ? -kLog2e * b : 0.f;
+      }
+  }
+
+  __device__ void logits(const float (&s)[RUN], const f32x4_t (&c0)[PT], f32x4_t (&lg)[PT]) const {
+    const uint2 sop = make_uint2(pack_f16(s[0], s[1]), pack_f16(s[2], s[3]));
+    f32x4_t u[JT];
+    mfma_priority_begin();
+#pragma unroll
+    for (int jt = 0; jt < JT; ++jt)
+      u[jt] = __builtin_amdgcn_mfma_f32_16x16x16f16(__builtin_bit_cast(f16x4_t, w1op[jt]),
+                                                    __builtin_bit_cast(f16x4_t, sop), b1acc[jt], 0, 0, 0);
+    mfma_priority_end();
+    uint4 hop[KH];
+#pragma unroll
+    for (int m = 0; m < KH; ++m) {
+      float hv[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float x = u[2 * m + (e >> 2)][e & 3];
+        hv[e] = x * __builtin_amdgcn_rcpf(1.f + __builtin_amdgcn_exp2f(x));
+      }
+      hop[m] = make_uint4(pack_f16(hv[0], hv[1]), pack_f16(hv[2], hv[3]), pack_f16(hv[4], hv[5]),
+                          pack_f16(hv[6], hv[7]));
+    }
+    mfma_priority_begin();
+    lg[0] = c0[0];
+#pragma unroll
+    for (int m = 0; m < KH; ++m) lg[0] = mfma_f16(w2op[m], hop[m], lg[0]);
+    mfma_priority_end();
+  }
+
+  __device__ static void weights(const f32x4_t (&lg)[PT], const float (&s)[RUN], float shift, float& den,
+                                 float& num) {
+    float d[2], n[2];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const float w = __builtin_amdgcn_exp2f(lg[0][i] - shift);
+      if (i < 2) {
+        d[i] = w;
+        n[i] = w * s[i];
+      } else {
+        d[i & 1] += w;
+        n[i & 1] = fmaf(w, s[i], n[i & 1]);
+      }
+    }
+    den = d[0] + d[1];
+    num = n[0] + n[1];
+  }
+
+  template <int NQ>
+  __device__ void phi(const float (&s)[NQ][RUN], const f32x4_t (&c0)[NQ][PT], float (&out)[NQ]) const {
+    static_assert(NQ == 1 || NQ == 2, "one or two queries per call");
+    float den[NQ], num[NQ];
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) {
+      f32x4_t lg[PT];
+      logits(s[q], c0[q], lg);
+      weights(lg, s[q], 0.f, den[q], num[q]);
+    }
+    float D, Nm;
+    row_sums(den[0], num[0], den[NQ - 1], num[NQ - 1], D, Nm);
+    const bool ok = D >= 0x1p-60f && D <= 0x1p60f;
+    if (!__all(ok)) {
+      const uint64_t okm = __ballot(ok);
+#pragma unroll
+      for (int q = 0; q < NQ; ++q) {
+        const uint64_t rows = NQ == 1 ? ~0ull : q == 0 ? 0x00000000FFFFFFFFull : 0xFFFFFFFF00000000ull;
+        if ((okm & rows) == rows) continue;
+        f32x4_t lg[PT];
+        logits(s[q], c0[q], lg);
+        float mx = fmaxf(fmaxf(lg[0][0], lg[0][1]), fmaxf(lg[0][2], lg[0][3]));
         weights(lg, s[q], max_groups(mx), den[q], num[q]);
       }
       row_sums(den[0], num[0], den[NQ - 1], num[NQ - 1], D, Nm);

@@ -1,6 +1,6 @@
 """GPU parity of the pair-wise path (MFMA dot products into a buffer, then
-the gating MLP on matrix cores, zero-padded to 32 or 64 components and 32,
-64 or 128 hidden units) on shapes the fused kernels do not take: brute-force
+the gating MLP on matrix cores, zero-padded to 16, 32 or 64 components and
+32, 64 or 128 hidden units) on shapes the fused kernels do not take: brute-force
 top-k, rerank of candidate lists, the max-component top-k and the bounded
 second pass of Algorithm 1, against the FP64 oracle (MI355X only)."""
 import dataclasses
@@ -22,6 +22,7 @@ BASE = synth.WORKLOADS["exact_32k"]
 # (one thread per pair)
 SHAPES = [
     ("p12_h32_d64", 3, 4, 64, 32, True),
+    ("p8_h128_d64", 2, 4, 64, 128, False),
     ("p16_h48_d96", 4, 4, 96, 48, True),
     ("p32_h64_d64", 4, 8, 64, 64, False),
     ("p24_h100_d128", 2, 12, 128, 100, True),
