@@ -247,11 +247,14 @@ __global__ __launch_bounds__(64 * kWaves, 1) void k_mol_fused(
         }
       };
       if constexpr (EPI == kEpiTopk || EPI == kEpiDense) {
-        // both queries' MLP chains in one call, free to interleave
+        // both queries' MLP chains in one call: interleaved by hand where the
+        // matrix chains are short against the SiLU work (H <= 64), else
+        // left to the compiler with raised priority around each chain
         f32x4_t c0[2][S::PT];
         gate_bias(0, c0[0]);
         gate_bias(1, c0[1]);
-        mlp.template phi<2>(s2, c0, phi);
+        if constexpr (H <= 64) mlp.template phi2_interleaved<4>(s2, c0, phi);
+        else mlp.template phi<2>(s2, c0, phi);
       }
 #pragma unroll
       for (int qb = 0; qb < 2 && (EPI == kEpiBounded || EPI == kEpiMaxDot); ++qb) {

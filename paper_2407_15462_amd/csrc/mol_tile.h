@@ -372,26 +372,24 @@ struct MolMlp {
       }
   }
 
-  // Base-2 gating logits l' of one query for the lane's items (GEMM2 ->
-  // SiLU -> GEMM3).  s: the lane's run of s values; c0: log2(e) (a_x + a_q
-  // + b2) in the GEMM3 accumulator layout (element i of tile pt <-> p =
-  // base(g) + 4 pt + i).
-  __device__ void logits(const float (&s)[RUN], const f32x4_t (&c0)[PT], f32x4_t (&lg)[PT]) const {
-    uint4 sop[KP];
+  // The stages of the chain for one query, without scheduling fences.
+  // s: the lane's run of s values; c0: log2(e) (a_x + a_q + b2) in the
+  // GEMM3 accumulator layout (element i of tile pt <-> p = base(g) + 4 pt + i).
+  __device__ static void pack_s(const float (&s)[RUN], uint4 (&sop)[KP]) {
 #pragma unroll
     for (int m = 0; m < KP; ++m)
       sop[m] = make_uint4(pack_f16(s[8 * m + 0], s[8 * m + 1]), pack_f16(s[8 * m + 2], s[8 * m + 3]),
                           pack_f16(s[8 * m + 4], s[8 * m + 5]), pack_f16(s[8 * m + 6], s[8 * m + 7]));
-    f32x4_t u[JT];
-    mfma_priority_begin();
+  }
+  __device__ void gemm2(const uint4 (&sop)[KP], f32x4_t (&u)[JT]) const {
 #pragma unroll
     for (int jt = 0; jt < JT; ++jt) {
       u[jt] = b1acc[jt];
 #pragma unroll
       for (int m = 0; m < KP; ++m) u[jt] = mfma_f16(w1op[jt][m], sop[m], u[jt]);
     }
-    mfma_priority_end();
-    uint4 hop[KH];
+  }
+  __device__ static void silu(const f32x4_t (&u)[JT], uint4 (&hop)[KH]) {
 #pragma unroll
     for (int m = 0; m < KH; ++m) {
       float hv[8];
@@ -403,13 +401,29 @@ struct MolMlp {
       hop[m] = make_uint4(pack_f16(hv[0], hv[1]), pack_f16(hv[2], hv[3]), pack_f16(hv[4], hv[5]),
                           pack_f16(hv[6], hv[7]));
     }
-    mfma_priority_begin();
+  }
+  __device__ void gemm3(const uint4 (&hop)[KH], const f32x4_t (&c0)[PT], f32x4_t (&lg)[PT]) const {
 #pragma unroll
     for (int pt = 0; pt < PT; ++pt) {
       lg[pt] = c0[pt];
 #pragma unroll
       for (int m = 0; m < KH; ++m) lg[pt] = mfma_f16(w2op[pt][m], hop[m], lg[pt]);
     }
+  }
+
+  // Base-2 gating logits l' of one query for the lane's items (GEMM2 ->
+  // SiLU -> GEMM3), each matrix chain issued at raised wave priority.
+  __device__ void logits(const float (&s)[RUN], const f32x4_t (&c0)[PT], f32x4_t (&lg)[PT]) const {
+    uint4 sop[KP];
+    pack_s(s, sop);
+    f32x4_t u[JT];
+    mfma_priority_begin();
+    gemm2(sop, u);
+    mfma_priority_end();
+    uint4 hop[KH];
+    silu(u, hop);
+    mfma_priority_begin();
+    gemm3(hop, c0, lg);
     mfma_priority_end();
   }
 
@@ -433,6 +447,55 @@ struct MolMlp {
       }
     den = d[0] + d[1];
     num = n[0] + n[1];
+  }
+
+  // phi of two queries (out[q] valid in the lanes of rows 2q, 2q + 1), with
+  // the two chains software-pipelined in one scheduling region: query 1's
+  // GEMM2 issues between query 0's SiLU instructions, query 0's GEMM3
+  // between query 1's, and query 1's GEMM3 between query 0's softmax terms,
+  // so that each wave keeps its matrix core busy under its own vector ALU
+  // work.  VA is the number of vector ALU instructions placed after each
+  // matrix instruction.  The arithmetic is that of phi<2> (the same
+  // instructions on the same operands), so the results are bit-identical;
+  // a query whose sum left [2^-60, 2^60] is redone by phi<2>.
+  template <int VA>
+  __device__ void phi2_interleaved(const float (&s)[2][RUN], const f32x4_t (&c0)[2][PT], float (&out)[2]) const {
+    uint4 sop[2][KP];
+    f32x4_t u[2][JT];
+    uint4 hop[2][KH];
+    f32x4_t lg[2][PT];
+    float den[2], num[2];
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      pack_s(s[q], sop[q]);
+      gemm2(sop[q], u[q]);
+    }
+#pragma unroll
+    for (int q = 0; q < 2; ++q) silu(u[q], hop[q]);
+#pragma unroll
+    for (int q = 0; q < 2; ++q) gemm3(hop[q], c0[q], lg[q]);
+#pragma unroll
+    for (int q = 0; q < 2; ++q) weights(lg[q], s[q], 0.f, den[q], num[q]);
+    // issue order: query 0's GEMM2 (JT KP matrix instructions), then the
+    // three interleaved runs of JT KP, PT KH and PT KH matrix instructions,
+    // each followed by VA vector ALU (transcendentals included) instructions
+    constexpr int kMfma = 0x008, kValu = 0x002 | 0x400;
+    __builtin_amdgcn_sched_group_barrier(kMfma, JT * KP, 0);
+#pragma unroll
+    for (int i = 0; i < JT * KP + 2 * PT * KH; ++i) {
+      __builtin_amdgcn_sched_group_barrier(kMfma, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(kValu, VA, 0);
+    }
+    float D, Nm;
+    row_sums(den[0], num[0], den[1], num[1], D, Nm);
+    const bool ok = D >= 0x1p-60f && D <= 0x1p60f;
+    if (!__all(ok)) {
+      phi<2>(s, c0, out);
+      return;
+    }
+    const float v = Nm * __builtin_amdgcn_rcpf(D);
+    out[0] = v;
+    out[1] = v;
   }
 
   // phi for the lane's item under NQ (1 or 2) queries: out[q] is valid in
