@@ -253,7 +253,7 @@ __global__ __launch_bounds__(64 * kWaves, 1) void k_mol_fused(
         f32x4_t c0[2][S::PT];
         gate_bias(0, c0[0]);
         gate_bias(1, c0[1]);
-        if constexpr (H <= 64) mlp.template phi2_interleaved<4>(s2, c0, phi);
+        if constexpr (H <= 64) mlp.template phi2_interleaved<5>(s2, c0, phi);
         else mlp.template phi<2>(s2, c0, phi);
       }
 #pragma unroll
