@@ -235,6 +235,7 @@ __global__ __launch_bounds__(64 * kWaves, 1) void k_mol_fused(
       }
       float phi[2];
       bool offer[2] = {item_ok, item_ok};
+      bool need[2] = {true, true};   // bounded form: the query's chain runs
       // GEMM3 accumulator input of query qb: log2(e) a_x (the item's, from
       // the stage) + log2(e) (a_q + b2) (the query's), at the lane's
       // p = base(g) + 4 pt + i
@@ -281,20 +282,32 @@ __global__ __launch_bounds__(64 * kWaves, 1) void k_mol_fused(
             }
             offer[qb] = item_ok && pass;
             phi[qb] = -__builtin_inff();
-            if (!__any(offer[qb])) continue;   // no item of the group can qualify
+            need[qb] = __any(offer[qb]);   // some item of the group can qualify
           }
         }
-        if constexpr (EPI == kEpiBounded) {
-          // one query at a time: the other's chain may have been skipped
-          float sq[1][S::RUN];
+      }
+      if constexpr (EPI == kEpiBounded) {
+        if (need[0] && need[1]) {
+          // both chains run: as one two-query call (the same arithmetic)
+          f32x4_t c0[2][S::PT];
+          gate_bias(0, c0[0]);
+          gate_bias(1, c0[1]);
+          if constexpr (H <= 64) mlp.template phi2_interleaved<5>(s2, c0, phi);
+          else mlp.template phi<2>(s2, c0, phi);
+        } else {
 #pragma unroll
-          for (int mu = 0; mu < S::RUN; ++mu) sq[0][mu] = s2[qb][mu];
-          f32x4_t c0[1][S::PT];
-          gate_bias(qb, c0[0]);
-          float pq[1];
-          mlp.template phi<1>(sq, c0, pq);
-          phi[qb] = pq[0];
-          __builtin_amdgcn_sched_barrier(0);
+          for (int qb = 0; qb < 2; ++qb) {
+            if (!need[qb]) continue;
+            float sq[1][S::RUN];
+#pragma unroll
+            for (int mu = 0; mu < S::RUN; ++mu) sq[0][mu] = s2[qb][mu];
+            f32x4_t c0[1][S::PT];
+            gate_bias(qb, c0[0]);
+            float pq[1];
+            mlp.template phi<1>(sq, c0, pq);
+            phi[qb] = pq[0];
+            __builtin_amdgcn_sched_barrier(0);
+          }
         }
       }
       // phi[qb] is valid in the lanes of rows 2 qb and 2 qb + 1 (the two-query
