@@ -31,7 +31,8 @@
 //   kDotsToCandidates  the keys of list (b, p) that reach thr[(b * P + p) *
 //                      thr_stride] are appended to its row of `keys`, the
 //                      list's count advanced with one atomic add per wave
-//                      and row (the rows must hold every item).
+//                      and list, straight from the accumulators (the rows
+//                      must hold every item).
 #include "mol_tile.h"
 
 namespace mol {
@@ -121,23 +122,27 @@ __global__ __launch_bounds__(256) void k_dots_mfma(DevProb pr, int n0, int nt, i
     bslot[i] = r * CH + dots_swz8(r, ch);
   }
 
-  // candidates: the thresholds of the wave's 16 epilogue rows of each half,
-  // read by lanes 0..15 now so that the reads complete during the K loop
-  uint64_t thr_lane[HALVES];
+  const int c = lane & 31, h = lane >> 5;
+  const int wm = wave & 1, wn = wave >> 1;            // item half (64), vector half (TV/2) of the tile
+  // candidates: the thresholds of the lane's lists (vector wn TV/2 + 32 jb +
+  // c of each block column jb, component px), read now so that the reads
+  // complete during the K loop
+  uint64_t thr_v[NBV];
+  long list_v[NBV];
 #pragma unroll
-  for (int hv = 0; hv < HALVES; ++hv) {
-    thr_lane[hv] = ~0ull;
-    if (MODE == kDotsToCandidates && lane < 16) {
-      const int v = v0 + 64 * hv + wave * 16 + lane;
+  for (int jb = 0; jb < NBV; ++jb) {
+    thr_v[jb] = ~0ull;
+    list_v[jb] = 0;
+    if (MODE == kDotsToCandidates) {
+      const int v = v0 + wn * (TV / 2) + jb * 32 + c;
       if (v < v1) {
         const int b = v / pr.Pq, pq = v - (v / pr.Pq) * pr.Pq;
-        thr_lane[hv] = thr[(static_cast<long>(b) * pr.P + pq * pr.Px + px) * thr_stride];
+        list_v[jb] = static_cast<long>(b) * pr.P + pq * pr.Px + px;
+        thr_v[jb] = thr[list_v[jb] * thr_stride];
       }
     }
   }
 
-  const int c = lane & 31, h = lane >> 5;
-  const int wm = wave & 1, wn = wave >> 1;            // item half (64), vector half (TV/2) of the tile
   f32x16_t acc[2][NBV];
   auto zero_acc = [&]() {
 #pragma unroll
@@ -217,6 +222,48 @@ __global__ __launch_bounds__(256) void k_dots_mfma(DevProb pr, int n0, int nt, i
       for (int jb = 0; jb < NBV; ++jb) acc[ib][jb] = run[ib][jb];
   }
 
+  if constexpr (MODE == kDotsToCandidates) {
+    // Straight from the accumulators: lane (c, h) of block (ib, jb) holds
+    // list jb's scores of items wm 64 + 32 ib + 8 j + 4 h + i (j, i < 4).
+    // A key reaches th iff its score beats th's, or ties it with an index
+    // that keeps the key at or above th: the float compare decides almost
+    // every item, and the key is formed only for the kept ones.  The two
+    // lanes of a list (h = 0, 1) reserve their slots with one atomic add.
+#pragma unroll
+    for (int jb = 0; jb < NBV; ++jb) {
+      const uint64_t th = thr_v[jb];
+      const float ts = key_score(th);
+      auto kept = [&](int ib, int e) {
+        const int i = it0 + wm * 64 + ib * 32 + 8 * (e >> 2) + 4 * h + (e & 3);
+        const float v = acc[ib][jb][e];
+        return i < cnt && v >= ts && (v > ts || make_key(v, n0 + i) >= th);
+      };
+      uint32_t n = 0;
+#pragma unroll
+      for (int ib = 0; ib < 2; ++ib)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) n += kept(ib, e) ? 1u : 0u;
+      const uint32_t n_other = static_cast<uint32_t>(__shfl_xor(static_cast<int>(n), 32, 64));
+      if (__ballot(n > 0) == 0ull) continue;               // no lane keeps a key (wave-uniform)
+      uint32_t base = 0;
+      if (h == 0 && n + n_other > 0) base = atomicAdd(counts + list_v[jb], n + n_other);
+      const uint32_t base0 = static_cast<uint32_t>(__shfl_xor(static_cast<int>(base), 32, 64));
+      uint32_t pos = h == 0 ? base : base0 + n_other;
+      uint64_t* dst = keys + list_v[jb] * key_stride;
+      if (n > 0) {
+#pragma unroll
+        for (int ib = 0; ib < 2; ++ib)
+#pragma unroll
+          for (int e = 0; e < 16; ++e)
+            if (kept(ib, e)) {
+              const int i = it0 + wm * 64 + ib * 32 + 8 * (e >> 2) + 4 * h + (e & 3);
+              dst[pos++] = make_key(acc[ib][jb][e], n0 + i);
+            }
+      }
+    }
+    return;
+  }
+
   // The loop ended with a barrier: the staging area is free.  Each 64-row
   // half of the tile goes through LDS (rows padded to TR floats) so that
   // every global store instruction writes a contiguous run of one row.
@@ -251,54 +298,6 @@ __global__ __launch_bounds__(256) void k_dots_mfma(DevProb pr, int n0, int nt, i
           float m = sT[(qi * pr.Pq) * TR + 64 * t + lane];
           for (int pq = 1; pq < pr.Pq; ++pq) m = fmaxf(m, sT[(qi * pr.Pq + pq) * TR + 64 * t + lane]);
           if (i < cnt) dst[i] = make_key(m, n0 + i);
-        }
-      }
-    } else if (MODE == kDotsToCandidates) {
-      // Two passes over the wave's 16 rows: count the keys each row keeps
-      // (row rr's count lands in lane rr), reserve every row's slots with
-      // one atomic add per row issued by lanes 0..15 together, then store.
-      const int nrows = max(0, min(16, v1 - vh - wave * 16));
-      // a key reaches th iff its score beats th's, or ties it with an index
-      // that keeps the key at or above th: the float compare decides almost
-      // every item, and the key is formed only for the kept ones
-      auto kept = [&](int rr, int t, uint64_t th, float ts) {
-        const int i = it0 + 64 * t + lane;
-        const float v = sT[(wave * 16 + rr) * TR + 64 * t + lane];
-        return i < cnt && v >= ts && (v > ts || make_key(v, n0 + i) >= th);
-      };
-      uint32_t row_hits = 0;                              // lane rr: keys kept by row rr
-      for (int rr = 0; rr < nrows; ++rr) {
-        const uint64_t th = static_cast<uint64_t>(__shfl(static_cast<long long>(thr_lane[hv]), rr, 64));
-        const float ts = key_score(th);
-        uint32_t n = 0;
-#pragma unroll
-        for (int t = 0; t < 2; ++t) n += static_cast<uint32_t>(__popcll(__ballot(kept(rr, t, th, ts))));
-        if (lane == rr) row_hits = n;
-      }
-      auto row_list = [&](int rr) {
-        const int v = vh + wave * 16 + rr;
-        const int b = v / pr.Pq, pq = v - (v / pr.Pq) * pr.Pq;
-        return static_cast<long>(b) * pr.P + pq * pr.Px + px;
-      };
-      uint32_t row_base = 0;
-      if (lane < nrows && row_hits > 0) row_base = atomicAdd(counts + row_list(lane), row_hits);
-      for (int rr = 0; rr < nrows; ++rr) {
-        if (__shfl(row_hits, rr, 64) == 0u) continue;     // wave-uniform
-        const uint64_t th = static_cast<uint64_t>(__shfl(static_cast<long long>(thr_lane[hv]), rr, 64));
-        const float ts = key_score(th);
-        uint32_t pos = __shfl(row_base, rr, 64);
-        uint64_t* dst = keys + row_list(rr) * key_stride;
-#pragma unroll
-        for (int t = 0; t < 2; ++t) {
-          const bool hit = kept(rr, t, th, ts);
-          const uint64_t mask = __ballot(hit);
-          const uint32_t below = __builtin_amdgcn_mbcnt_hi(static_cast<uint32_t>(mask >> 32),
-                                                           __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(mask), 0u));
-          if (hit) {
-            const int i = it0 + 64 * t + lane;
-            dst[pos + below] = make_key(sT[(wave * 16 + rr) * TR + 64 * t + lane], n0 + i);
-          }
-          pos += static_cast<uint32_t>(__popcll(mask));
         }
       }
     } else {
