@@ -331,6 +331,11 @@ __global__ __launch_bounds__(64 * waves_for(KL), 1) void k_topk_per_embd(
   f32x16_t accA[S::NB], accB[S::NB];
   const int nfull = (nr1 - nr0) / 32;             // tiles holding items only
   int j = 0;
+  // every global load issued so far (thresholds, query operands) completes
+  // here, once: the loop's first use of a threshold would otherwise carry a
+  // compiler-inserted vmcnt(0), executed on every iteration, that also waits
+  // for the LDS ring's prefetch copies
+  __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
   if (ntiles > 0) mma(0, accA);
   for (; j + 2 < nfull; j += 2) {
     mma(j + 1, accB);
