@@ -123,3 +123,30 @@ def test_thresholded_lists_many_queries():
         s_all = mo.all_dots(op, b)
         for p in range(spec.P):
             check_topk_row(s_all[:, p], ids[b, p], dots[b, p], kp, f"thresholded_many b={b} p={p}")
+
+
+def test_pairwise_softmax_redo_far_logits():
+    """Reading R13 on the pair-wise gating kernel (P = 12 and 16 padded to
+    16): items and queries whose base-2 logits sit far from zero take the
+    redo with the row maximum subtracted."""
+    for Pq, Px in ((3, 4), (4, 4)):
+        spec = dataclasses.replace(_spec(Pq, Px, 64, 64, True), N=1531)
+        P = spec.P
+        log(f"[pairwise redo] B={spec.B} N={spec.N} P={P}")
+        inp = cuda_inputs(spec, seed=72)
+        inp.a_x[0:50] = 50.0
+        inp.a_x[50:100] = 100.0        # past the float32 range without the redo
+        inp.a_x[100:150] = -50.0
+        inp.a_x[150:200] = -100.0
+        rows = torch.arange(200, 300, device="cuda")
+        inp.a_x[rows, rows % P] = 60.0
+        inp.a_q[1] = 45.0
+        prob = mol.Problem.from_inputs(inp)
+        k = 50
+        s, i = mol.topk_exact(prob, k)
+        torch.cuda.synchronize()
+        op = oracle_problem(inp)
+        phi = mo.mol_scores(op, list(range(spec.B)))
+        s, i = s.cpu().numpy(), i.cpu().numpy()
+        for b in range(spec.B):
+            check_topk_row(phi[b], i[b], s[b], k, f"pairwise redo P={P} query {b}")

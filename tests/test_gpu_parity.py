@@ -488,3 +488,48 @@ def test_worked_example_through_the_abi():
     assert nu.item() == 3
     assert [names[j] for j in ri.cpu().numpy()[0]] == ["a", "b"]
     assert abs(rs[0, 1].item() - float(expect["Theorem 2 S_K"][0])) < 1e-6
+
+
+@pytest.mark.parametrize("name,spec", [
+    ("p64_h64", W["exact_1m"].scaled(B=6, N=1200, clusters=16)),       # two-query pipelined chain
+    ("p32_h64", W["exact_32k"].scaled(B=6, N=1200, clusters=16)),      # pipelined chain, P_x = 4
+    ("p32_h128_d128", W["hybrid_8m"].scaled(B=6, N=1200, clusters=16)),  # two-query chain, H = 128
+], ids=lambda v: v if isinstance(v, str) else "")
+def test_softmax_redo_far_logits(name, spec):
+    """Reading R13: the softmax sums skip the max subtraction only while they
+    stay inside [2^-60, 2^60]; items whose base-2 logits all sit near +-72 or
+    +-144 (past the float32 range), items with one dominant logit, and whole
+    queries shifted by +-45 take the redo with the row maximum subtracted.  Queries 0 and 1 share a wave, so
+    one query redoes while the other does not."""
+    log(f"[softmax redo] {name} B={spec.B} N={spec.N} P={spec.P} H={spec.H}")
+    inp = cuda_inputs(spec, seed=71)
+    P = spec.P
+    # 2^(log2(e) 100) overflows float32 and 2^(-log2(e) 100) underflows it:
+    # without the redo those rows would give inf / inf or 0 / 0
+    inp.a_x[0:48] = 50.0
+    inp.a_x[48:96] = 100.0
+    inp.a_x[96:144] = -50.0
+    inp.a_x[144:192] = -100.0
+    rows = torch.arange(192, 288, device="cuda")
+    inp.a_x[rows, rows % P] = 60.0
+    inp.a_q[1] = 45.0
+    inp.a_q[4] = -45.0
+    prob = mol.Problem.from_inputs(inp)
+    k = 50
+    phi = mol.score(prob)
+    s, i = mol.topk_exact(prob, k)
+    bs, bi = mol.topk_exact_bounded(prob, k, s[:, k - 1].contiguous())
+    g = torch.Generator(device="cuda").manual_seed(5)
+    cand = torch.randint(0, spec.N, (spec.B, 400), device="cuda", generator=g, dtype=torch.int32)
+    rs, ri, rn = mol.rerank(prob, cand, k)
+    torch.cuda.synchronize()
+    assert torch.equal(bi, i) and torch.equal(bs, s), f"{name}: bounded pass differs from brute force"
+    want = mo.mol_scores(oracle_problem(inp), list(range(spec.B)))
+    check_scores(phi.cpu().numpy(), want, what="redo_phi")
+    s, i, rs, ri, cand = s.cpu().numpy(), i.cpu().numpy(), rs.cpu().numpy(), ri.cpu().numpy(), cand.cpu().numpy()
+    for b in range(spec.B):
+        check_topk_row(want[b], i[b], s[b], k, f"redo {name} query {b}")
+        uniq = mo.union_dedup([cand[b]])
+        full = np.full(spec.N, -np.inf)
+        full[uniq] = want[b][uniq]
+        check_topk_row(full, ri[b], rs[b], k, f"redo_rerank {name} query {b}")
