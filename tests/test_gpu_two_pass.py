@@ -114,6 +114,24 @@ def test_bounded_topk(name, spec):
         if len(got) < k:    # padding only when fewer than k items may qualify
             assert surely.sum() <= len(got)
             assert np.all(i[b][len(got):] == -1) and np.all(np.isneginf(s[b][len(got):]))
+    # mixed bounds in one call (query b: -inf, the k-th score, mid, above
+    # every m for b % 4 = 0..3): the two queries of a wave differ in whether
+    # their gating chains run, so both the two-query and the one-query forms
+    # of the scan are taken
+    kth_s = want_s[:, k - 1].cpu().numpy()
+    mixed = np.array([(-np.inf, kth_s[b], mid[b], top[b])[b % 4] for b in queries], dtype=np.float32)
+    s_x, i_x = mol.topk_exact_bounded(prob, k, torch.tensor(mixed, device="cuda"))
+    torch.cuda.synchronize()
+    s_x, i_x = s_x.cpu().numpy(), i_x.cpu().numpy()
+    ws, wi = want_s.cpu().numpy(), want_i.cpu().numpy()
+    for b in queries:
+        if b % 4 < 2:
+            assert np.array_equal(i_x[b], wi[b]) and np.array_equal(s_x[b], ws[b]), f"{name} mixed query {b}"
+        elif b % 4 == 2:
+            assert np.array_equal(i_x[b], i[b]) and np.array_equal(s_x[b], s[b]), f"{name} mixed query {b}"
+        else:
+            assert np.all(i_x[b] == -1) and np.all(np.isneginf(s_x[b])), f"{name} mixed query {b}"
+
 
 
 @pytest.mark.parametrize("name,spec", CASES, ids=IDS)
