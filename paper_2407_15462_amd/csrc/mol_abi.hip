@@ -305,9 +305,9 @@ struct FusedExactPlan {
   size_t offFinal = 0, bytes = 0;
 };
 
-FusedExactPlan plan_fused_exact(const DevProb& pr, int k) {
+FusedExactPlan plan_fused_exact(const DevProb& pr, int k, bool maxdot = false) {
   FusedExactPlan f;
-  fused_grid(pr, pr.N, f.R, f.range_len, f.G);
+  fused_grid(pr, pr.N, f.R, f.range_len, f.G, maxdot);
   StreamPlan& s = f.s;
   s.rows = pr.B;
   s.k = k;
@@ -401,7 +401,7 @@ size_t exact_ws_bytes(const DevProb& pr, int k) {
 }
 
 size_t maxdot_ws_bytes(const DevProb& pr, int k) {
-  if (fused_maxdot_supported(pr, k)) return plan_fused_exact(pr, k).bytes;
+  if (fused_maxdot_supported(pr, k)) return plan_fused_exact(pr, k, true).bytes;
   return dots_maxkeys_supported(pr) ? plan_stream(pr.B, pr.N, k).bytes : plan_pairwise(pr, k).bytes;
 }
 
@@ -485,7 +485,7 @@ int run_maxdot(const DevProb& pr, int k, float* out_score, int32_t* out_idx, cha
                hipStream_t st) {
   int rc;
   if (fused_maxdot_supported(pr, k)) {
-    const FusedExactPlan f = plan_fused_exact(pr, k);
+    const FusedExactPlan f = plan_fused_exact(pr, k, true);
     uint64_t* partial = reinterpret_cast<uint64_t*>(w + f.s.offA);
     uint64_t* fin = reinterpret_cast<uint64_t*>(w + f.offFinal);
     MOL_TIMED_LAUNCH(timed_op, st, launch_fused_maxdot(pr, k, f.R, f.range_len, f.G, partial, st),

@@ -38,7 +38,11 @@ enum FusedEpi { kEpiTopk = 0, kEpiDense = 1, kEpiBounded = 2, kEpiMaxDot = 3 };
 
 constexpr int kWaves = 8;
 constexpr int kQueriesPerWG = 2 * kWaves;
-constexpr int kTile = 32;        // items per LDS stage (two 16-item steps)
+// items per LDS stage: two 16-item steps with the gating MLP; one step in
+// the max-dot form, whose smaller ring (with no a_x stream) lets two
+// workgroups share a CU
+template <bool AX>
+constexpr int tile_items() { return AX ? 32 : 16; }
 constexpr int kRing = 3;         // item stages in flight
 constexpr int kTopkRegion = WaveTopk::kList + WaveTopk::kStage;
 
@@ -46,13 +50,14 @@ constexpr int kTopkRegion = WaveTopk::kList + WaveTopk::kStage;
 template <int PX, int D, int H, bool AX>
 struct FusedShape {
   static constexpr int P = 8 * PX;
+  static constexpr int TILE = tile_items<AX>();
   static constexpr int RUN = 2 * PX;     // s values per lane per query
   static constexpr int KD = D / 32;      // K blocks of GEMM1
   static constexpr int PT = P / 16;      // output tiles of GEMM3
   static constexpr int XROWCH = D / 8;   // 16-byte chunks per X row
   static constexpr int AROWCH = P / 4;   // 16-byte chunks per a_x row
-  static constexpr int XSTAGE = PX * kTile * D * 2;   // bytes of one X stage
-  static constexpr int ASTAGE = AX ? kTile * P * 4 : 0;   // bytes of one a_x stage
+  static constexpr int XSTAGE = PX * TILE * D * 2;   // bytes of one X stage
+  static constexpr int ASTAGE = AX ? TILE * P * 4 : 0;   // bytes of one a_x stage
   static constexpr int LDS_X = kRing * XSTAGE;
   static constexpr int LDS_AX = kRing * ASTAGE;
   static constexpr int LDS_CB = AX ? kQueriesPerWG * P * 4 : 0;   // [query][p] log2(e) (a_q + b2), f32
@@ -82,7 +87,7 @@ __device__ __forceinline__ void wg_coords(int g, int R, int G, int& r, int& qg) 
 }  // namespace
 
 template <int PX, int D, int H, int EPI>
-__global__ __launch_bounds__(64 * kWaves, 1) void k_mol_fused(
+__global__ __launch_bounds__(64 * kWaves, EPI == kEpiMaxDot ? 2 : 1) void k_mol_fused(
     DevProb pr, int k, int R, int range_len, int G, int n_begin, int n_end,
     const float* __restrict__ bound, uint64_t* __restrict__ partial, float* __restrict__ phi_out,
     long phi_stride) {
@@ -106,7 +111,7 @@ __global__ __launch_bounds__(64 * kWaves, 1) void k_mol_fused(
   const int qwv = qwg + 2 * wave;         // first of this wave's 2 queries
   const int nr0 = n_begin + r * range_len;
   const int nr1 = min(n_end, nr0 + range_len);
-  const int ntiles = nr1 > nr0 ? (nr1 - nr0 + kTile - 1) / kTile : 0;
+  const int ntiles = nr1 > nr0 ? (nr1 - nr0 + S::TILE - 1) / S::TILE : 0;
   const int N = pr.N;
   constexpr int P = S::P;
 
@@ -120,13 +125,13 @@ __global__ __launch_bounds__(64 * kWaves, 1) void k_mol_fused(
   // belongs there.  Items past the end are clamped to N-1 (valid memory,
   // masked later).
   auto stage = [&](int t, int buf) {
-    const int n0 = nr0 + kTile * t;
+    const int n0 = nr0 + S::TILE * t;
 #pragma unroll
     for (int cp = 0; cp < S::XBLOCKS / kWaves; ++cp) {
       const int blk = wave + kWaves * cp;
       const int pos = blk * 64 + lane;
-      const int px = pos / (kTile * S::XROWCH);
-      const int rem = pos % (kTile * S::XROWCH);
+      const int px = pos / (S::TILE * S::XROWCH);
+      const int rem = pos % (S::TILE * S::XROWCH);
       const int n = rem / S::XROWCH, phys = rem % S::XROWCH;
       const int cc = phys ^ (n % S::XROWCH);
       const int item = min(n0 + n, N - 1);
@@ -186,9 +191,9 @@ __global__ __launch_bounds__(64 * kWaves, 1) void k_mol_fused(
     const unsigned char* as = sAx + buf * S::ASTAGE;
 
 #pragma unroll
-    for (int st = 0; st < kTile / 16; ++st) {
+    for (int st = 0; st < S::TILE / 16; ++st) {
       const int n = 16 * st + c;            // item within the stage
-      const int item = nr0 + kTile * t + n;
+      const int item = nr0 + S::TILE * t + n;
       const bool item_ok = item < nr1;
 
       // LDS operands of the step, all issued before the first MFMA so that
@@ -197,7 +202,7 @@ __global__ __launch_bounds__(64 * kWaves, 1) void k_mol_fused(
       uint4 xb[PX][S::KD];
 #pragma unroll
       for (int px = 0; px < PX; ++px) {
-        const unsigned char* row = xs + (px * kTile + n) * (D * 2);
+        const unsigned char* row = xs + (px * S::TILE + n) * (D * 2);
 #pragma unroll
         for (int kk = 0; kk < S::KD; ++kk) {
           const int phys = (4 * kk + g) ^ (n % S::XROWCH);
@@ -225,13 +230,29 @@ __global__ __launch_bounds__(64 * kWaves, 1) void k_mol_fused(
       mfma_priority_end();
       // separate the two queries: s[q][mu] holds p = base(g) + mu
       float s2[2][S::RUN];
+      float mrow = 0.f;
+      if constexpr (EPI == kEpiMaxDot) {
+        // no split: lane group g holds query g / 2's rows pq = 4 (g % 2) ..
+        // + 3 for every px, so the maximum over its 4 PX values and the
+        // other group of the query (one permlane16 swap) is m, valid in the
+        // lanes of rows 2 q and 2 q + 1 as the offers expect
+        float mx = acc1[0][0];
 #pragma unroll
-      for (int mu = 0; mu < S::RUN; ++mu) {
-        const float a = acc1[mu % PX][mu / PX];
-        const float b = acc1[mu % PX][2 + mu / PX];
-        auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(a), __float_as_uint(b), false, false);
-        s2[0][mu] = __uint_as_float(sw[0]);
-        s2[1][mu] = __uint_as_float(sw[1]);
+        for (int px = 0; px < PX; ++px)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) mx = fmaxf(mx, acc1[px][e]);
+        const uint32_t u = __float_as_uint(mx);
+        auto sw = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+        mrow = fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1]));
+      } else {
+#pragma unroll
+        for (int mu = 0; mu < S::RUN; ++mu) {
+          const float a = acc1[mu % PX][mu / PX];
+          const float b = acc1[mu % PX][2 + mu / PX];
+          auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(a), __float_as_uint(b), false, false);
+          s2[0][mu] = __uint_as_float(sw[0]);
+          s2[1][mu] = __uint_as_float(sw[1]);
+        }
       }
       float phi[2];
       bool offer[2] = {item_ok, item_ok};
@@ -259,31 +280,30 @@ __global__ __launch_bounds__(64 * kWaves, 1) void k_mol_fused(
       }
 #pragma unroll
       for (int qb = 0; qb < 2 && (EPI == kEpiBounded || EPI == kEpiMaxDot); ++qb) {
-        if constexpr (EPI == kEpiBounded || EPI == kEpiMaxDot) {
+        if constexpr (EPI == kEpiMaxDot) {
+          phi[qb] = mrow;
+          continue;
+        }
+        if constexpr (EPI == kEpiBounded) {
           // m = max_p s_p of the lane's item
           float m = s2[qb][0];
 #pragma unroll
           for (int mu = 1; mu < S::RUN; ++mu) m = fmaxf(m, s2[qb][mu]);
           m = max_groups(m);
-          if constexpr (EPI == kEpiMaxDot) {
-            phi[qb] = m;
-            continue;
-          } else {
-            const float floor = fmaxf(qbound[qb], top[qb].theta_score);
-            // |m| <= max_p |s_p|: passing with the margin of |m| is passing
-            bool pass = m + bound_margin(fabsf(m)) >= floor;
-            if (!__all(pass || !item_ok)) {
-              // the margin of max_p |s_p| decides the rest
-              float mabs = fabsf(s2[qb][0]);
+          const float floor = fmaxf(qbound[qb], top[qb].theta_score);
+          // |m| <= max_p |s_p|: passing with the margin of |m| is passing
+          bool pass = m + bound_margin(fabsf(m)) >= floor;
+          if (!__all(pass || !item_ok)) {
+            // the margin of max_p |s_p| decides the rest
+            float mabs = fabsf(s2[qb][0]);
 #pragma unroll
-              for (int mu = 1; mu < S::RUN; ++mu) mabs = fmaxf(mabs, fabsf(s2[qb][mu]));
-              mabs = max_groups(mabs);
-              pass = m + bound_margin(mabs) >= floor;
-            }
-            offer[qb] = item_ok && pass;
-            phi[qb] = -__builtin_inff();
-            need[qb] = __any(offer[qb]);   // some item of the group can qualify
+            for (int mu = 1; mu < S::RUN; ++mu) mabs = fmaxf(mabs, fabsf(s2[qb][mu]));
+            mabs = max_groups(mabs);
+            pass = m + bound_margin(mabs) >= floor;
           }
+          offer[qb] = item_ok && pass;
+          phi[qb] = -__builtin_inff();
+          need[qb] = __any(offer[qb]);   // some item of the group can qualify
         }
       }
       if constexpr (EPI == kEpiBounded) {
@@ -358,14 +378,15 @@ bool fused_maxdot_supported(const DevProb& pr, int k) {
   return fused_shape(pr, false) && k <= WaveTopk::kList;
 }
 
-void fused_grid(const DevProb& pr, int n_count, int& R, int& range_len, int& G) {
+void fused_grid(const DevProb& pr, int n_count, int& R, int& range_len, int& G, bool maxdot) {
   G = (pr.B + kQueriesPerWG - 1) / kQueriesPerWG;
-  R = std::max(1, 256 / G);
+  // about one workgroup per CU (two in the max-dot form)
+  R = std::max(1, (maxdot ? 512 : 256) / G);
   // ranges of at least 128 items (4 tiles): small corpora still fill the chip
   const int max_r = std::max(1, n_count / 128);
   R = std::min(R, max_r);
   range_len = (n_count + R - 1) / R;
-  range_len = (range_len + kTile - 1) / kTile * kTile;
+  range_len = (range_len + 31) / 32 * 32;   // whole stages of either form
   R = (n_count + range_len - 1) / range_len;
 }
 
@@ -416,7 +437,7 @@ hipError_t launch_fused_maxdot(const DevProb& pr, int k, int R, int range_len, i
 hipError_t launch_fused_dense(const DevProb& pr, int n_begin, int n_count, float* phi,
                               hipStream_t st) {
   int R, range_len, G;
-  fused_grid(pr, n_count, R, range_len, G);
+  fused_grid(pr, n_count, R, range_len, G, false);
   return launch_fused_d<kEpiDense>(pr, 1, R, range_len, G, n_begin, n_begin + n_count, nullptr, nullptr,
                                    phi, n_count, st);
 }

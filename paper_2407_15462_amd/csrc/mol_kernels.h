@@ -98,7 +98,7 @@ namespace mol {
 bool fused_supported(const DevProb& pr, int k);
 // max-component-dot epilogue: the same shapes with H ignored
 bool fused_maxdot_supported(const DevProb& pr, int k);
-void fused_grid(const DevProb& pr, int n_count, int& R, int& range_len, int& G);
+void fused_grid(const DevProb& pr, int n_count, int& R, int& range_len, int& G, bool maxdot);
 // bound: NULL, or [B] floats: only items with max_p s_p (plus the rounding
 // margin) at or above bound[b] are ranked for query b
 hipError_t launch_fused_topk(const DevProb& pr, int k, int R, int range_len, int G,
