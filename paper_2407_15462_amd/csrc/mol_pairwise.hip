@@ -33,9 +33,8 @@ namespace {
 constexpr int kPairQB = 8;         // queries per workgroup
 // 16-item steps per wave: enough that a wave runs at least kPairMinIters
 // iterations (it builds its MLP operands once, from scattered weight
-// reads), more when the launch would exceed about kPairWaves waves
+// reads), more when the launch would exceed one round of resident waves
 constexpr int kPairMinIters = 16;
-constexpr long kPairWaves = 8192;
 }  // namespace
 
 // BOUNDED: Algorithm 1's second pass (kGenBounded); otherwise phi, negated
@@ -184,33 +183,72 @@ bool phi_mfma_supported(const DevProb& pr) {
   return pr.dtype == MOL_BF16 && pr.P <= 64 && pr.H <= 128;
 }
 
+// Waves of one k_phi_mfma instantiation that the device holds at once.
+template <int PXV, int HV, bool BOUNDED, bool GATHER>
+static long pair_resident_waves() {
+  static const long waves = [] {
+    int dev = 0, ncu = 0, nb = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || ncu <= 0)
+      ncu = 256;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, k_phi_mfma<PXV, HV, BOUNDED, GATHER>, 256, 0) !=
+            hipSuccess ||
+        nb <= 0)
+      nb = 1;
+    return static_cast<long>(nb) * 4 * ncu;
+  }();
+  return waves;
+}
+
+// Work split: per_query 16-item steps for each of `groups` query groups of
+// up to kPairQB (qb) queries.  Each wave takes `steps` steps: at least
+// kPairMinIters iterations, and about one round of resident waves for the
+// whole launch (a wave that lives longer amortises its operand set-up), but
+// no more than one workgroup of 4 waves needs for the whole range.
+template <int PXV, int HV, bool BOUNDED, bool GATHER>
+static void launch_phi_mfma_k(long per_query, long groups, long qb, const DevProb& pr, bool neg,
+                              const float* bound, int n_begin, int n_count, const int32_t* items,
+                              const int32_t* item_count, long item_stride, const float* sbuf, long s_pstride,
+                              long s_bstride, float* phi, long phi_stride, uint64_t* keys, long key_stride,
+                              hipStream_t st) {
+  const long waves = pair_resident_waves<PXV, HV, BOUNDED, GATHER>();
+  long steps = std::max<long>((kPairMinIters + qb - 1) / qb, (per_query * groups + waves - 1) / waves);
+  steps = std::max<long>(1, std::min<long>(steps, (per_query + 3) / 4));
+  const dim3 grid(static_cast<unsigned>((per_query + 4 * steps - 1) / (4 * steps)), static_cast<unsigned>(groups));
+  hipLaunchKernelGGL((k_phi_mfma<PXV, HV, BOUNDED, GATHER>), grid, dim3(256), 0, st, pr, neg, bound, n_begin,
+                     n_count, static_cast<int>(steps), items, item_count, item_stride, sbuf, s_pstride, s_bstride,
+                     phi, phi_stride, keys, key_stride);
+}
+
 template <int PXV, int HV, bool BOUNDED>
-static void launch_phi_mfma_m(dim3 grid, const DevProb& pr, bool neg, const float* bound, int n_begin,
-                              int n_count, int steps, const int32_t* items, const int32_t* item_count,
-                              long item_stride, const float* sbuf, long s_pstride, long s_bstride, float* phi,
-                              long phi_stride, uint64_t* keys, long key_stride, hipStream_t st) {
+static void launch_phi_mfma_m(long per_query, long groups, long qb, const DevProb& pr, bool neg,
+                              const float* bound, int n_begin, int n_count, const int32_t* items,
+                              const int32_t* item_count, long item_stride, const float* sbuf, long s_pstride,
+                              long s_bstride, float* phi, long phi_stride, uint64_t* keys, long key_stride,
+                              hipStream_t st) {
   if (items)
-    hipLaunchKernelGGL((k_phi_mfma<PXV, HV, BOUNDED, true>), grid, dim3(256), 0, st, pr, neg, bound, n_begin,
-                       n_count, steps, items, item_count, item_stride, sbuf, s_pstride, s_bstride, phi, phi_stride,
-                       keys, key_stride);
+    launch_phi_mfma_k<PXV, HV, BOUNDED, true>(per_query, groups, qb, pr, neg, bound, n_begin, n_count, items,
+                                              item_count, item_stride, sbuf, s_pstride, s_bstride, phi, phi_stride,
+                                              keys, key_stride, st);
   else
-    hipLaunchKernelGGL((k_phi_mfma<PXV, HV, BOUNDED, false>), grid, dim3(256), 0, st, pr, neg, bound, n_begin,
-                       n_count, steps, items, item_count, item_stride, sbuf, s_pstride, s_bstride, phi, phi_stride,
-                       keys, key_stride);
+    launch_phi_mfma_k<PXV, HV, BOUNDED, false>(per_query, groups, qb, pr, neg, bound, n_begin, n_count, items,
+                                               item_count, item_stride, sbuf, s_pstride, s_bstride, phi, phi_stride,
+                                               keys, key_stride, st);
 }
 
 template <int PXV, int HV>
-static void launch_phi_mfma_t(dim3 grid, const DevProb& pr, int mode, const float* bound, int n_begin,
-                              int n_count, int steps, const int32_t* items, const int32_t* item_count,
-                              long item_stride, const float* sbuf, long s_pstride, long s_bstride, float* phi,
-                              long phi_stride, uint64_t* keys, long key_stride, hipStream_t st) {
+static void launch_phi_mfma_t(long per_query, long groups, long qb, const DevProb& pr, int mode,
+                              const float* bound, int n_begin, int n_count, const int32_t* items,
+                              const int32_t* item_count, long item_stride, const float* sbuf, long s_pstride,
+                              long s_bstride, float* phi, long phi_stride, uint64_t* keys, long key_stride,
+                              hipStream_t st) {
   if (mode == kGenBounded)
-    launch_phi_mfma_m<PXV, HV, true>(grid, pr, false, bound, n_begin, n_count, steps, items, item_count,
+    launch_phi_mfma_m<PXV, HV, true>(per_query, groups, qb, pr, false, bound, n_begin, n_count, items, item_count,
                                      item_stride, sbuf, s_pstride, s_bstride, phi, phi_stride, keys, key_stride, st);
   else
-    launch_phi_mfma_m<PXV, HV, false>(grid, pr, mode == kGenNegPhi, nullptr, n_begin, n_count, steps, items,
-                                      item_count, item_stride, sbuf, s_pstride, s_bstride, phi, phi_stride, keys,
-                                      key_stride, st);
+    launch_phi_mfma_m<PXV, HV, false>(per_query, groups, qb, pr, mode == kGenNegPhi, nullptr, n_begin, n_count,
+                                      items, item_count, item_stride, sbuf, s_pstride, s_bstride, phi, phi_stride,
+                                      keys, key_stride, st);
 }
 
 hipError_t launch_phi_mfma(const DevProb& pr, int mode, const float* bound, int n_begin, int n_count,
@@ -227,15 +265,9 @@ hipError_t launch_phi_mfma(const DevProb& pr, int mode, const float* bound, int 
   const long per_query = (static_cast<long>(n_count) + 15) / 16;   // 16-item steps per query
   const long groups = (pr.B + kPairQB - 1) / kPairQB;
   const long qb = std::min<long>(kPairQB, pr.B);
-  // at least kPairMinIters iterations per wave, about kPairWaves waves, and
-  // at most what one workgroup of 4 waves needs for the whole range
-  long steps = std::max<long>((kPairMinIters + qb - 1) / qb, (per_query * groups + kPairWaves - 1) / kPairWaves);
-  steps = std::max<long>(1, std::min<long>(steps, (per_query + 3) / 4));
-  const dim3 grid(static_cast<unsigned>((per_query + 4 * steps - 1) / (4 * steps)), static_cast<unsigned>(groups));
 #define MOL_PHI_MFMA(PXV, HV)                                                                              \
-  launch_phi_mfma_t<PXV, HV>(grid, pr, mode, bound, n_begin, n_count, static_cast<int>(steps), items,     \
-                             item_count, item_stride, sbuf,                                                \
-                             s_pstride, s_bstride, phi, phi_stride, keys, key_stride, st)
+  launch_phi_mfma_t<PXV, HV>(per_query, groups, qb, pr, mode, bound, n_begin, n_count, items, item_count, \
+                             item_stride, sbuf, s_pstride, s_bstride, phi, phi_stride, keys, key_stride, st)
   if (pr.P <= 16) {
     if (pr.H <= 32) MOL_PHI_MFMA(2, 32);
     else if (pr.H <= 64) MOL_PHI_MFMA(2, 64);
