@@ -277,7 +277,7 @@ RerankPlan plan_rerank(const DevProb& pr, int C, int k) {
   // generic path: keys of every candidate; fused path: per-chunk top-k lists
   long L0 = C;
   if (rerank_supported(pr, k)) {
-    const int chunk = rerank_chunk(C);
+    const int chunk = rerank_chunk(B, C);
     L0 = static_cast<long>((C + chunk - 1) / chunk) * k;
   }
   const int S0 = segment_size_for(static_cast<int>(L0), k);
@@ -566,7 +566,7 @@ int run_rerank(const DevProb& pr, const int32_t* cand, int C, const int32_t* can
   uint64_t* fin = reinterpret_cast<uint64_t*>(w + r.offFinal);
   MOL_TRY_HIP(launch_dedup(cand, C, cand2, C2, pr.B, pr.N, uniq, nu, st), "dedup");
   if (rerank_supported(pr, k)) {
-    const int chunk = rerank_chunk(CT);
+    const int chunk = rerank_chunk(pr.B, CT);
     const long L0 = static_cast<long>((CT + chunk - 1) / chunk) * k;
     MOL_TIMED_LAUNCH(timed_op, st, launch_rerank(pr, uniq, nu, CT, k, negate, A, st), "fused rerank");
     if ((rc = reduce_rows(r.s, w, L0, fin, k, st))) return rc;

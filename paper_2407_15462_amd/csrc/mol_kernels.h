@@ -137,7 +137,7 @@ namespace mol {
 
 // Fused MFMA rerank of deduplicated candidates (same shapes as the fused scorer).
 bool rerank_supported(const DevProb& pr, int k);
-int rerank_chunk(int C);
+int rerank_chunk(int B, int C);
 // negate: rank by -phi (the smallest scores first)
 hipError_t launch_rerank(const DevProb& pr, const int32_t* uniq, const int32_t* n_unique, int C, int k,
                          bool negate, uint64_t* partial, hipStream_t st);

@@ -106,7 +106,16 @@ __global__ __launch_bounds__(64 * kWaves, 2) void k_mol_rerank(
 // ---------------------------------------------------------------------------
 bool rerank_supported(const DevProb& pr, int k) { return fused_supported(pr, k); }
 
-int rerank_chunk(int C) { return C <= 1024 ? 256 : 1024; }
+// Candidates per wave: the largest of 2048, 1024, 512 and 256 that still
+// gives at least one round of resident waves (two 4-wave workgroups per CU
+// on 256 CUs), so that long lists amortise each wave's operand set-up and
+// small batches still fill the chip.
+int rerank_chunk(int B, int C) {
+  constexpr long kResidentWaves = 2l * kWaves * 256;
+  for (int chunk = 2048; chunk > 256; chunk /= 2)
+    if (static_cast<long>(B) * ((C + chunk - 1) / chunk) >= kResidentWaves) return chunk;
+  return 256;
+}
 
 template <bool NEG>
 static void launch_rerank_t(const DevProb& pr, dim3 grid, const int32_t* uniq, const int32_t* n_unique,
@@ -127,7 +136,7 @@ static void launch_rerank_t(const DevProb& pr, dim3 grid, const int32_t* uniq, c
 
 hipError_t launch_rerank(const DevProb& pr, const int32_t* uniq, const int32_t* n_unique, int C, int k,
                          bool negate, uint64_t* partial, hipStream_t st) {
-  const int chunk = rerank_chunk(C);
+  const int chunk = rerank_chunk(pr.B, C);
   const int nchunks = (C + chunk - 1) / chunk;
   const long waves = static_cast<long>(pr.B) * nchunks;
   const dim3 grid(static_cast<unsigned>((waves + kWaves - 1) / kWaves));
