@@ -25,7 +25,9 @@
 //
 // Workgroup: 8 waves (2 per SIMD) = 16 queries sharing an LDS-staged
 // stream of 32-item tiles (a three-deep ring) loaded with direct
-// global->LDS copies.
+// global->LDS copies.  The max-dot form stages 16-item tiles, so that two
+// workgroups share a CU (4 waves per SIMD), and takes m straight from
+// GEMM1's tile without splitting the two queries.
 #include "mol_tile.h"
 
 namespace mol {
