@@ -165,9 +165,14 @@ __global__ __launch_bounds__(256) void k_dots_generic(DevProb pr, int n_begin, i
 }
 
 // ---------------------------------------------------------------------------
-// Segmented top-k: block (seg, row) sorts keys in[row][seg*S .. seg*S+S) in
-// LDS (bitonic, descending; missing slots are empty keys) and writes the
-// first k to out[row][seg*k ..].
+// Segmented top-k: block (seg, row) takes keys in[row][seg*S .. seg*S+S)
+// into LDS (missing slots are empty keys) and writes the k largest, sorted
+// descending, to out[row][seg*k ..].  With C the power of two >= k (at
+// least 64): runs of C keys are bitonic-sorted in alternating directions,
+// then rounds halve the keys, each keeping, of two adjacent runs (one
+// descending, one ascending), the elementwise maximum (a bitonic sequence
+// holding the C largest of the pair) and bitonic-merging it, until one
+// descending run of C remains.  Where C >= S this is a full bitonic sort.
 // ---------------------------------------------------------------------------
 template <int S, int NT>
 __global__ __launch_bounds__(NT) void k_segment_topk(const uint64_t* __restrict__ in, long in_stride,
@@ -180,20 +185,42 @@ __global__ __launch_bounds__(NT) void k_segment_topk(const uint64_t* __restrict_
   const int len = static_cast<int>(min(static_cast<long>(S), static_cast<long>(L) - base));
   for (int t = threadIdx.x; t < S; t += NT) sk[t] = t < len ? src[t] : 0ull;
   __syncthreads();
-  for (int size = 2; size <= S; size <<= 1) {
-    for (int stride = size >> 1; stride > 0; stride >>= 1) {
-      for (int i = threadIdx.x; i < S / 2; i += NT) {
-        const int lo = 2 * i - (i & (stride - 1));
-        const int hi = lo + stride;
-        const bool desc = (lo & size) == 0;
-        const uint64_t a = sk[lo], c = sk[hi];
-        if ((a < c) == desc) {
-          sk[lo] = c;
-          sk[hi] = a;
-        }
+  int C = 64;
+  while (C < k && C < S) C <<= 1;
+  // one compare-exchange stage over the first n keys: pairs at distance
+  // stride, direction alternating every dirspan keys
+  auto stage = [&](int n, int stride, int dirspan) {
+    for (int i = threadIdx.x; i < n / 2; i += NT) {
+      const int lo = 2 * i - (i & (stride - 1));
+      const int hi = lo + stride;
+      const bool desc = (lo & dirspan) == 0;
+      const uint64_t a = sk[lo], c = sk[hi];
+      if ((a < c) == desc) {
+        sk[lo] = c;
+        sk[hi] = a;
       }
-      __syncthreads();
     }
+    __syncthreads();
+  };
+  // runs of C keys, sorted descending / ascending in turn
+  for (int size = 2; size <= C; size <<= 1)
+    for (int stride = size >> 1; stride > 0; stride >>= 1) stage(S, stride, size);
+  for (int n = S; n > C; n >>= 1) {
+    // run pair (2m, 2m+1) -> run m: the elementwise maximum, kept in
+    // registers until every thread has read its pair
+    uint64_t keep[S / (2 * NT) > 0 ? S / (2 * NT) : 1];
+    int cnt = 0;
+    for (int t = threadIdx.x; t < n / 2; t += NT, ++cnt) {
+      const int m = t / C, i = t - m * C;
+      const uint64_t a = sk[2 * m * C + i], c = sk[(2 * m + 1) * C + i];
+      keep[cnt] = a > c ? a : c;
+    }
+    __syncthreads();
+    cnt = 0;
+    for (int t = threadIdx.x; t < n / 2; t += NT, ++cnt) sk[t] = keep[cnt];
+    __syncthreads();
+    // merge each bitonic run; the last one (n / 2 == C) descending
+    for (int stride = C >> 1; stride > 0; stride >>= 1) stage(n / 2, stride, C);
   }
   uint64_t* dst = out + row * out_stride + static_cast<long>(blockIdx.x) * k;
   for (int t = threadIdx.x; t < k; t += NT) dst[t] = sk[t];
