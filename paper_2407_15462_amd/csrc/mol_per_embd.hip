@@ -454,11 +454,16 @@ static void scan_grid(const DevProb& pr, int kp, bool scan2, PerEmbdGrid::Scan& 
 void per_embd_grid(const DevProb& pr, int kp, PerEmbdGrid& g) {
   scan_grid(pr, kp, false, g.s1);
   scan_grid(pr, kp, true, g.s2);
-  // buckets: as many as fit kMaxBuckets per list over all ranges and halves
+  // buckets: as many as fit `cap` per list over all ranges and halves.  For
+  // k' <= 128, 1024 buckets leave about k'^2 / 2048 <= 8 collisions among
+  // the k' largest items, so the bound admits few more keys than 2048 do,
+  // while the bucket scan stores and the threshold kernel reads half as
+  // many maxima
+  const int cap = kp <= 128 ? kMaxBuckets / 2 : kMaxBuckets;
   const int ntiles = g.s1.range_len / 32;
-  g.bucket_tiles = std::max(1, (2 * g.s1.R * ntiles + kMaxBuckets - 1) / kMaxBuckets);
+  g.bucket_tiles = std::max(1, (2 * g.s1.R * ntiles + cap - 1) / cap);
   g.nbk = (ntiles + g.bucket_tiles - 1) / g.bucket_tiles;
-  while (2 * g.s1.R * g.nbk > kMaxBuckets) {
+  while (2 * g.s1.R * g.nbk > cap) {
     ++g.bucket_tiles;
     g.nbk = (ntiles + g.bucket_tiles - 1) / g.bucket_tiles;
   }
