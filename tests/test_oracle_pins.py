@@ -382,6 +382,70 @@ def test_theorem3_combined_gap_bound():
         assert phi[rest].max() <= bnd["S"] + 1e-15
 
 
+THEOREM3 = os.path.join(os.path.dirname(__file__), "golden", "theorem3_example.txt")
+THEOREM3_KEYS = ("per-component lists (K'=1)", "TopKAvg (K_avg=1)", "candidates", "Theorem 3 S' ",
+                 "Theorem 3 S_K", "Theorem 3 bound S' - S_K", "Definition 2 gap")
+
+
+def theorem3_problem():
+    """The hand-built Theorem 3 instance, realised like the Appendix B
+    example: f = e1, g_p(x) = dot_p(x) e1, per-item gating logits only."""
+    rows, expect = {}, {}
+    with open(THEOREM3) as f:
+        for line in f:
+            line = line.strip()
+            if not line:
+                continue
+            if line.startswith("#"):
+                body = line[1:].strip()
+                for key in THEOREM3_KEYS:
+                    if body.startswith(key):
+                        expect[key.strip()] = body[len(key):].split()
+                continue
+            name, *vals = line.split()
+            rows[name] = [float(v) for v in vals]
+    names = sorted(rows)
+    N, d = len(names), 2
+    Q = np.zeros((1, 1, d), np.float32)
+    Q[0, 0, 0] = 1.0
+    X = np.zeros((2, N, d), np.float32)
+    a_x = np.zeros((N, 2), np.float32)
+    for n, name in enumerate(names):
+        dot1, dot2, pi1, pi2, _ = rows[name]
+        X[0, n, 0], X[1, n, 0] = dot1, dot2
+        if pi1 != pi2:
+            a_x[n] = (20.0, -20.0) if pi1 > pi2 else (-20.0, 20.0)
+    z = lambda *s: np.zeros(s, np.float32)
+    prob = mo.Problem(Q, X, z(1, 2), a_x, z(1, 2), z(1), z(2, 1), z(2), "f32")
+    return prob, names, rows, expect
+
+
+def test_theorem3_value_pin_on_hand_built_instance():
+    """S', S_K and the bound of Theorem 3 equal the hand-derived values.  The
+    instance has an item in one component's list that carries the largest
+    dot of the other component outside that component's own list and the
+    TopKAvg set, so excluding the whole candidate union from every
+    component (a plausible mistake) gives a different S'."""
+    prob, names, rows, expect = theorem3_problem()
+    s, pi, phi = mo.mol_terms(prob, 0, slice(None))
+    for n, name in enumerate(names):
+        assert abs(phi[n] - rows[name][4]) < 1e-12
+    avg = mo.averaged_problem(prob)
+    lists = [mo.topk_desc(s[:, p], 1)[1] for p in range(2)]
+    assert [names[int(l[0])] for l in lists] == expect["per-component lists (K'=1)"]
+    _, avg_ids = mo.topk_avg(prob, 0, 1, avg)
+    assert [names[int(i)] for i in avg_ids] == expect["TopKAvg (K_avg=1)"]
+    res = mo.approx_topk(prob, 0, k=3, kprime=1, k_avg=1, avg=avg)
+    assert [names[int(i)] for i in mo.union_dedup([res["cand"]])] == expect["candidates"]
+    bnd = mo.gap_bound_combined(prob, 0, 3, 1, 1, avg)
+    assert bnd["S"] == float(expect["Theorem 3 S'"][0])
+    assert abs(bnd["S_K"] - float(expect["Theorem 3 S_K"][0])) < 1e-12
+    assert abs(bnd["bound"] - float(expect["Theorem 3 bound S' - S_K"][0])) < 1e-12
+    g = mo.gap(phi, res["ids"], 3)
+    assert abs(g - float(expect["Definition 2 gap"][0])) < 1e-12
+    assert g <= bnd["bound"]
+
+
 def test_union_dedup_is_set_union_and_rerank_pads():
     rng = np.random.default_rng(13)
     lists = [rng.integers(-1, 50, size=30) for _ in range(4)]
