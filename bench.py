@@ -54,6 +54,10 @@ def parse():
     ap.add_argument("--cpu-baseline-queries", type=int, default=None,
                     help="oracle queries timed for cpu_baseline (default: about 10-20 s of work)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--extras", default="hybrid_8m,exact_1m_skewed",
+                    help="other workloads summarised as extra keys of the exact_1m line "
+                         "(comma list; empty for none)")
+    ap.add_argument("--extra-steps", type=int, default=3)
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy three times (the "
@@ -128,9 +132,64 @@ def main():
         paper_table(spec, args)
         return
     paths = [p for p in args.paths.split(",") if p]
+    out, inp = run_workload(spec, args.steps, args.warmup, paths, args.seed)
+    ms_step = out.pop("_ms_step")
+    line = {
+        "metric": METRIC,
+        "value": spec.B / (ms_step / 1e3),
+        "unit": "queries/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": spec.dtype, "data": "synthetic",
+        "config": {"workload": spec.name, "B": spec.B, "N": spec.N, "Pq": spec.Pq, "Px": spec.Px,
+                   "d": spec.d, "H": spec.H, "k": spec.k,
+                   "kprime": (spec.kprime or 128) if "approx" in paths else None, "paths": paths},
+    }
+    line.update(out)
+    if not args.no_cpu_baseline:
+        nq = args.cpu_baseline_queries or max(1, (8 << 20) // spec.N)
+        line["cpu_baseline"] = cpu_baseline(inp, spec, nq)
+    del inp
+    extras = [e for e in args.extras.split(",") if e and e != spec.name] if spec.name == "exact_1m" else []
+    for name in extras:
+        import torch
+        torch.cuda.empty_cache()
+        x_spec = synth.WORKLOADS[name]
+        x_out, x_inp = run_workload(x_spec, args.extra_steps, 1, ["exact", "approx"], args.seed)
+        x_ms = x_out.pop("_ms_step")
+        summary = {"config": {"B": x_spec.B, "N": x_spec.N, "Pq": x_spec.Pq, "Px": x_spec.Px, "d": x_spec.d,
+                              "H": x_spec.H, "k": x_spec.k, "kprime": x_spec.kprime, "k_avg": x_spec.k_avg or None,
+                              "gating_std": x_spec.gating_std},
+                   "steps": args.extra_steps, "ms_per_step": x_ms, "queries_per_s": x_spec.B / (x_ms / 1e3)}
+        ex, ap_, rf = x_out.get("exact", {}), x_out.get("approx", {}), x_out.get("roofline", {})
+        summary.update({
+            "exact_ms": ex.get("ms"), "exact_kernel_ms": ex.get("kernel_ms"),
+            "fused_frac": rf.get("frac"), "fused_traffic": rf.get("traffic"),
+            "approx_ms": ap_.get("ms"), "per_embd_ms": ap_.get("ms_per_embd"),
+            "topk_avg_ms": ap_.get("ms_topk_avg"), "rerank_ms": ap_.get("ms_rerank"),
+            "recall_at_100_vs_exact": ap_.get("recall_at_100_vs_exact"),
+            "candidates_per_query_mean": ap_.get("candidates_per_query_mean")})
+        line[name] = summary
+        print(f"# extra {name}: {x_ms:.1f} ms/step, recall {summary['recall_at_100_vs_exact']}",
+              file=sys.stderr, flush=True)
+        del x_inp
+    print(json.dumps(line), flush=True)
+
+
+def run_workload(spec, steps, warmup, paths, seed):
+    """Time `steps` steps (after `warmup`) of the exact and / or approximate
+    path on one workload.  Returns (result keys, the inputs)."""
+    import statistics
+
+    import torch
+
+    import synth
+    from paper_2407_15462_amd import mol
+
     dev = "cuda"
     t0 = time.time()
-    inp = synth.generate(spec, seed=args.seed, device=dev)
+    inp = synth.generate(spec, seed=seed, device=dev)
     torch.cuda.synchronize()
     print(f"# generated {spec.name} in {time.time() - t0:.1f}s", file=sys.stderr, flush=True)
     prob = mol.Problem.from_inputs(inp)
@@ -190,7 +249,7 @@ def main():
                 seg["topk_avg"].append((e1, e2))
                 seg["rerank"].append((e2, e3))
 
-    for _ in range(args.warmup):
+    for _ in range(warmup):
         step(False)
     torch.cuda.synchronize()
     timed_ops = (mol.MOL_OP_TOPK_EXACT, mol.MOL_OP_TOPK_PER_EMBD, mol.MOL_OP_RERANK)
@@ -198,13 +257,12 @@ def main():
         mol.mol_timing_read(op)             # drop anything recorded before
     mol.mol_timing_enable(True)
     t_start = time.perf_counter()
-    for _ in range(args.steps):
+    for _ in range(steps):
         step(True)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t_start
     mol.mol_timing_enable(False)
-    ms_step = 1e3 * wall / args.steps
-    import statistics
+    ms_step = 1e3 * wall / steps
     seg_ms = {p: [a.elapsed_time(b) for a, b in v] for p, v in seg.items()}
     ms = {p: (statistics.fmean(v) if v else None) for p, v in seg_ms.items()}
 
@@ -215,21 +273,10 @@ def main():
     for op in timed_ops:
         tot, n = mol.mol_timing_read(op)
         kern[op] = tot / n if n else None
-        kern_step[op] = tot / args.steps if n else None
+        kern_step[op] = tot / steps if n else None
 
     flops_pair = 2 * P * d + 4 * P * H
-    out = {
-        "metric": METRIC,
-        "value": B / (ms_step / 1e3),
-        "unit": "queries/s",
-        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
-        "ms_per_step": ms_step,
-        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
-        "dtype": spec.dtype, "data": "synthetic",
-        "config": {"workload": spec.name, "B": B, "N": N, "Pq": spec.Pq, "Px": spec.Px, "d": d,
-                   "H": H, "k": k, "kprime": kprime if "approx" in paths else None,
-                   "paths": paths},
-    }
+    out = {"_ms_step": ms_step}
     if ms["exact"]:
         t = ms["exact"] / 1e3
         tk = kern[mol.MOL_OP_TOPK_EXACT] / 1e3
@@ -275,10 +322,7 @@ def main():
                          "recall_at_100_vs_exact": recall,
                          "candidates_per_query_mean": uniq_total / B}
 
-    if not args.no_cpu_baseline:
-        nq = args.cpu_baseline_queries or max(1, (8 << 20) // spec.N)
-        out["cpu_baseline"] = cpu_baseline(inp, spec, nq)
-    print(json.dumps(out), flush=True)
+    return out, inp
 
 
 def paper_table(spec, args):
@@ -442,36 +486,62 @@ def paper_table(spec, args):
         "methods": results}), flush=True)
 
 
-def cpu_baseline(inp, spec, nq):
+def cpu_model_name():
+    """The host CPU's full model name (lscpu, else /proc/cpuinfo)."""
+    import subprocess
+    try:
+        r = subprocess.run(["lscpu"], capture_output=True, text=True, timeout=10)
+        for line in r.stdout.splitlines():
+            if line.strip().lower().startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except (OSError, subprocess.SubprocessError):
+        pass
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
+
+
+# host threads given to the oracle: the CPU share of one GPU on the benchmark
+# hosts (16), or fewer where the machine has fewer
+CPU_THREAD_CAP = 16
+
+
+def cpu_baseline(inp, spec, nq, nq_single=1):
     """The FP64 oracle, as it stands, on a bounded sample of the same
-    workload: exact MoL top-k for the first ``nq`` queries over all N items."""
-    import numpy as np
+    workload: exact MoL top-k for the first ``nq`` queries over all N items
+    with the BLAS pool at the host's thread share, and for the first
+    ``nq_single`` queries with one thread."""
     from threadpoolctl import threadpool_info, threadpool_limits
 
     import synth
     from oracle import mol_oracle as mo
 
-    cores = min(16, os.cpu_count() or 1)
-    queries = list(range(nq))
-    arrays = synth.to_numpy(inp, queries=queries)
+    threads = min(CPU_THREAD_CAP, os.cpu_count() or 1)
+    arrays = synth.to_numpy(inp, queries=list(range(max(nq, nq_single))))
     op = mo.Problem.from_arrays(arrays)
-    with threadpool_limits(limits=cores):
-        t0 = time.perf_counter()
-        mo.exact_topk(op, list(range(nq)), spec.k)
-        dt = time.perf_counter() - t0
-    model = None
-    try:
-        with open("/proc/cpuinfo") as f:
-            for line in f:
-                if line.startswith("model name"):
-                    model = line.split(":", 1)[1].strip()
-                    break
-    except OSError:
-        pass
-    return {"value": nq / dt, "unit": "queries/s", "cores": cores, "kind": "oracle",
+
+    def timed(n, limit):
+        with threadpool_limits(limits=limit):
+            used = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+            t0 = time.perf_counter()
+            mo.exact_topk(op, list(range(n)), spec.k)
+            return time.perf_counter() - t0, used
+
+    dt, used = timed(nq, threads)
+    dt1, _ = timed(nq_single, 1)
+    return {"value": nq / dt, "unit": "queries/s", "cores": used, "kind": "oracle",
             "sample": f"exact top-{spec.k} for {nq} of {spec.B} queries over all "
-                      f"{spec.N} items (FP64 NumPy, BLAS threads={cores})",
-            "seconds": dt, "host_cpus": os.cpu_count(), "cpu_model": model}
+                      f"{spec.N} items (FP64 NumPy, BLAS threads={used}); single-thread leg: "
+                      f"{nq_single} query",
+            "seconds": dt, "threads": used,
+            "thread_cap": f"{CPU_THREAD_CAP} (the host CPU share of one GPU)",
+            "single_thread_queries_per_s": nq_single / dt1, "single_thread_seconds": dt1,
+            "host_cpus": os.cpu_count(), "cpu_model": cpu_model_name()}
 
 
 if __name__ == "__main__":

@@ -126,7 +126,7 @@ bool per_embd_supported(const DevProb& pr, int kp);
 int per_embd_list_cap(int kp);
 int per_embd_stage_cap(int kp);
 void per_embd_grid(const DevProb& pr, int kp, PerEmbdGrid& g);
-// bmax: [B*Pq*Px][s1.R][2][nbk] floats; thr: [B*Pq*Px] floats;
+// bmax: [Px][s1.R][nbk][B*Pq][2] floats; thr: [B*Pq*Px] floats;
 // lists: [B*Pq*Px][s2.R][KL] keys; stg: [B*Pq*Px][s2.R][stage_cap] keys.
 hipError_t launch_per_embd(const DevProb& pr, int kp, const PerEmbdGrid& g, float* bmax, float* thr,
                            uint64_t* lists, uint64_t* stg, hipStream_t st);

@@ -86,7 +86,9 @@ struct EmbdShape {
 // Grid: WG -> (vector group, px, range).  WGs sharing (px, range) are placed
 // on the same XCD (WG id mod 8) when the grid allows it.
 // R, range_len, G: this scan's item ranges and query-vector groups.
-// bmax: [nvec * Px][R][2][nbk] bucket maxima (scan 1 writes, scan 2 unused);
+// bmax: [Px][R][nbk][nvec][2] bucket maxima (scan 1 writes, scan 2 unused):
+//   for one (component, range, bucket) the two lanes of every list are
+//   adjacent and the lists contiguous, so a wave's store covers one line;
 // thr: [nvec * Px] starting thresholds (scan 2 reads);
 // lists: [nvec * Px][R][KL] keys; stg: [nvec * Px][R][2][SG] keys (scan 2).
 template <int D, int KL, bool SCAN2, bool SMALL>
@@ -165,9 +167,10 @@ __global__ __launch_bounds__(64 * waves_for(KL), 1) void k_topk_per_embd(
       }
     }
   }
+  // bucket bk of the lane's list in block nb: bucket_ptr(nb)[bk * nv2]
+  const long nv2 = 2l * nvec;
   auto bucket_ptr = [&](int nb) {
-    return bmax + ((static_cast<long>(vwave + 32 * nb + col) * Px + px) * R + r) * 2 * nbk +
-           static_cast<long>(half) * nbk;
+    return bmax + (static_cast<long>(px) * R + r) * nbk * nv2 + 2l * (vwave + 32 * nb + col) + half;
   };
   // merge the staged keys of list (nb, c) into it; nb and c are wave-uniform
   auto merge = [&](int nb, int c) {
@@ -270,7 +273,7 @@ __global__ __launch_bounds__(64 * waves_for(KL), 1) void k_topk_per_embd(
       if (++bcount == bucket_tiles) {
 #pragma unroll
         for (int nb = 0; nb < S::NB; ++nb) {
-          if (vok[nb]) bucket_ptr(nb)[bk] = bm[nb];
+          if (vok[nb] && bk < nbk) bucket_ptr(nb)[bk * nv2] = bm[nb];
           bm[nb] = -__builtin_inff();
         }
         bcount = 0;
@@ -359,8 +362,8 @@ __global__ __launch_bounds__(64 * waves_for(KL), 1) void k_topk_per_embd(
       if (!vok[nb]) continue;
       float* bp = bucket_ptr(nb);
       int b = bk;
-      if (bcount != 0) bp[b++] = bm[nb];
-      for (; b < nbk; ++b) bp[b] = -__builtin_inff();
+      if (bcount != 0 && b < nbk) bp[b++ * nv2] = bm[nb];
+      for (; b < nbk; ++b) bp[b * nv2] = -__builtin_inff();
     }
     return;
   }
@@ -390,33 +393,57 @@ __global__ __launch_bounds__(64 * waves_for(KL), 1) void k_topk_per_embd(
   }
 }
 
-// k'-th largest bucket maximum of every list (one wave per list): the
-// starting threshold of the second scan.  Bitwise search over the
-// order-preserving 32-bit image of the scores; fewer than k' finite
-// maxima give -inf (no filtering).
-__global__ __launch_bounds__(256) void k_bucket_threshold(const float* __restrict__ bmax, int nlists,
-                                                         int per_list, int kp, float* __restrict__ thr) {
-  const int lane = threadIdx.x & 63;
-  const long list = static_cast<long>(blockIdx.x) * 4 + (threadIdx.x >> 6);
-  if (list >= nlists) return;                    // whole wave exits
-  const float* row = bmax + list * per_list;
-  uint32_t v[kMaxBuckets / 64];
+// k'-th largest bucket maximum of every list: the starting threshold of the
+// second scan.  A workgroup of kThrLists waves takes kThrLists consecutive
+// query vectors of one component: their bucket maxima ([Px][R][nbk][nvec][2],
+// so one (range, bucket) row of the block is 2 kThrLists contiguous floats)
+// are read coalesced and transposed through LDS to one row of per_list + 1
+// floats per list (an odd stride: a row's transposing stores hit distinct
+// banks); then each wave runs a bitwise search over the order-preserving
+// 32-bit images of its list's VPL * 64 maxima.  Fewer than k' finite maxima
+// give -inf (no filtering).
+constexpr int kThrLists = 16;
+template <int VPL>
+__global__ __launch_bounds__(64 * kThrLists) void k_bucket_threshold(const float* __restrict__ bmax, int nvec,
+                                                                    int Px, int rows, int kp,
+                                                                    float* __restrict__ thr) {
+  extern __shared__ float sm[];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int nblk = (nvec + kThrLists - 1) / kThrLists;
+  const int px = blockIdx.x / nblk, v0 = (blockIdx.x % nblk) * kThrLists;
+  const int per_list = 2 * rows;               // maxima per list: rows x 2 lanes
+  const int row_stride = per_list + 1;
+  const long nv2 = 2l * nvec;
+  const float* base = bmax + static_cast<long>(px) * rows * nv2 + 2l * v0;
+  // element e of a block row: list v0 + e / 2, lane half e % 2
+  constexpr int kRowElems = 2 * kThrLists;
+  const int nvalid = 2 * min(kThrLists, nvec - v0);
+  for (int i = tid; i < rows * kRowElems; i += 64 * kThrLists) {
+    const int row = i / kRowElems, e = i % kRowElems;
+    const float v = e < nvalid ? base[row * nv2 + e] : -__builtin_inff();
+    sm[(e >> 1) * row_stride + 2 * row + (e & 1)] = v;
+  }
+  __syncthreads();
+  const int v = v0 + wave;
+  if (v >= nvec) return;                       // wave-uniform
+  const float* row = sm + wave * row_stride;
+  uint32_t val[VPL];
 #pragma unroll
-  for (int j = 0; j < kMaxBuckets / 64; ++j) {
+  for (int j = 0; j < VPL; ++j) {
     const int i = lane + 64 * j;
-    v[j] = i < per_list ? float_to_ordered(row[i]) : 0u;
+    val[j] = i < per_list ? float_to_ordered(row[i]) : 0u;
   }
   uint32_t t = 0u;
   for (int bit = 31; bit >= 0; --bit) {
     const uint32_t c = t | (1u << bit);
     int n = 0;
 #pragma unroll
-    for (int j = 0; j < kMaxBuckets / 64; ++j) n += __popcll(__ballot(v[j] >= c));
+    for (int j = 0; j < VPL; ++j) n += __popcll(__ballot(val[j] >= c));
     if (n >= kp) t = c;
   }
   // t is the k'-th largest image; images below that of -inf mean "none"
   const float f = t >= float_to_ordered(-__builtin_inff()) ? ordered_to_float(t) : -__builtin_inff();
-  if (lane == 0) thr[list] = f;
+  if (lane == 0) thr[static_cast<long>(v) * Px + px] = f;
 }
 
 // ---------------------------------------------------------------------------
@@ -438,6 +465,9 @@ int per_embd_stage_cap(int kp) {
   return (kl <= 256 ? 512 : 2 * kl) - kl;
 }
 
+// items of one LDS stage (EmbdShape::ST) for width d and list capacity kl
+static int stage_items(int d, int kl) { return (waves_for(kl) == 8 ? 32768 : 16384) / (2 * d); }
+
 static void scan_grid(const DevProb& pr, int kp, bool scan2, PerEmbdGrid::Scan& sc) {
   const int nvec = pr.B * pr.Pq;
   const int vec_wg = waves_for(per_embd_list_cap(kp)) * 32 * nb_pick(pr.d, scan2, per_embd_small(pr, kp));
@@ -446,8 +476,11 @@ static void scan_grid(const DevProb& pr, int kp, bool scan2, PerEmbdGrid::Scan& 
   // about one workgroup per CU, with ranges of at least 512 items
   int R = std::max(1, (256 + units - 1) / units);
   R = std::min(R, std::max(1, pr.N / 512));
+  // whole stages per range: a range's tile walk then covers exactly
+  // range_len / 32 tiles, the count the bucket layout is sized for
+  const int unit = std::max(128, stage_items(pr.d, per_embd_list_cap(kp)));
   sc.range_len = (pr.N + R - 1) / R;
-  sc.range_len = (sc.range_len + 127) / 128 * 128;
+  sc.range_len = (sc.range_len + unit - 1) / unit * unit;
   sc.R = (pr.N + sc.range_len - 1) / sc.range_len;
 }
 
@@ -488,9 +521,16 @@ static hipError_t launch_pe_s(const DevProb& pr, int kp, const PerEmbdGrid& g, f
                               uint64_t* lists, uint64_t* stg, hipStream_t st) {
   hipError_t e = launch_pe_t<D, KL, false, SMALL>(pr, kp, g, bmax, thr, lists, stg, st);
   if (e != hipSuccess) return e;
-  const int nlists = pr.B * pr.Pq * pr.Px;
-  hipLaunchKernelGGL(k_bucket_threshold, dim3((nlists + 3) / 4), dim3(256), 0, st, bmax, nlists,
-                     2 * g.s1.R * g.nbk, kp, thr);
+  const int nvec = pr.B * pr.Pq;
+  const int nblk = (nvec + kThrLists - 1) / kThrLists;
+  const int per_list = 2 * g.s1.R * g.nbk;
+  const int lds = kThrLists * (per_list + 1) * 4;
+  auto thr_kern = per_list <= kMaxBuckets / 2 ? &k_bucket_threshold<kMaxBuckets / 128>
+                                              : &k_bucket_threshold<kMaxBuckets / 64>;
+  e = hipFuncSetAttribute(reinterpret_cast<const void*>(thr_kern), hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(thr_kern, dim3(nblk * pr.Px), dim3(64 * kThrLists), lds, st, bmax, nvec, pr.Px,
+                     g.s1.R * g.nbk, kp, thr);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   return launch_pe_t<D, KL, true, SMALL>(pr, kp, g, bmax, thr, lists, stg, st);

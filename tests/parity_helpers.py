@@ -45,6 +45,18 @@ def check_topk_row(scores_all: np.ndarray, got_ids: np.ndarray, got_scores: np.n
             f"{what}: order broken at rank {j}"
 
 
+def assert_dedup_set(ids_row, n_unique, want, what):
+    """The deduplicated union G as an exact integer set: the first n_unique
+    slots hold distinct ids equal to the oracle's union, the rest is padding."""
+    got = np.asarray(ids_row[:n_unique], dtype=np.int64)
+    assert n_unique == len(want), f"{what}: {n_unique} unique ids, {len(want)} in the union"
+    assert len(np.unique(got)) == n_unique, f"{what}: duplicate ids in the deduplicated set"
+    assert np.array_equal(np.sort(got), want), \
+        f"{what}: id set differs from the union ({np.setdiff1d(want, got)[:5]} missing, " \
+        f"{np.setdiff1d(got, want)[:5]} extra)"
+    assert np.all(ids_row[n_unique:] == -1), f"{what}: padding past the unique ids"
+
+
 def recall(got_ids: np.ndarray, exact_ids: np.ndarray) -> float:
     hits = sum(len(set(g.tolist()) & set(e.tolist())) for g, e in zip(got_ids, exact_ids))
     return hits / exact_ids.size

@@ -14,7 +14,7 @@ import torch
 import synth
 from oracle import mol_oracle as mo
 from paper_2407_15462_amd import mol
-from parity_helpers import check_topk_row, log, recall
+from parity_helpers import assert_dedup_set, check_topk_row, log, recall
 
 pytestmark = pytest.mark.gpu
 
@@ -88,6 +88,16 @@ def test_per_embd_and_rerank_full_scale(full):
     log(f"[full] approx recall@100 vs exact (all {spec.B} queries): {rec:.4f}; "
         f"candidates/query mean {nu.mean():.0f}")
     assert 0.0 < rec <= 1.0
+    # the deduplicated union of the sampled queries' full-size candidate rows
+    # as an exact set: a rerank with k = C returns all of it
+    sub = mol.Problem(inp.Q[SAMPLE].contiguous(), inp.X, inp.a_q[SAMPLE].contiguous(), inp.a_x,
+                      inp.W1, inp.b1, inp.W2, inp.b2)
+    _, si, snu = mol.rerank(sub, cand[SAMPLE].contiguous(), C)
+    torch.cuda.synchronize()
+    si, snu = si.cpu().numpy(), snu.cpu().numpy()
+    for r, b in enumerate(SAMPLE):
+        log(f"[full] deduplicated union of query {b} as a set")
+        assert_dedup_set(si[r], int(snu[r]), mo.union_dedup([cand_np[b]]), f"dedup_1m query {b}")
 
 
 # ---------------------------------------------------------------- 8M items

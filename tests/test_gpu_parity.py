@@ -9,8 +9,8 @@ import torch
 import synth
 from oracle import mol_oracle as mo
 from paper_2407_15462_amd import mol
-from parity_helpers import (TAU, check_scores, check_topk_row, cuda_inputs, log, oracle_problem,
-                            recall)
+from parity_helpers import (TAU, assert_dedup_set, check_scores, check_topk_row, cuda_inputs, log,
+                            oracle_problem, recall)
 
 pytestmark = pytest.mark.gpu
 
@@ -366,6 +366,44 @@ def test_rerank_matches_oracle(C, k):
         full[uniq] = phi
         check_topk_row(full, i[b, :kk], s[b, :kk], kk, f"rerank query {b}")
         assert np.all(i[b, kk:] == -1) and np.all(np.isneginf(s[b, kk:]))
+
+
+@pytest.mark.parametrize("C,C2", [(700, 0), (4096, 0), (1000, 300)])
+def test_dedup_union_is_exact_set(C, C2):
+    """Algorithm 2's deduplicated set G, checked as a set: mol_rerank with
+    k = C + C2 returns every distinct candidate of a query (the rest padded),
+    so the id set must equal the union computed by the oracle, integer for
+    integer -- a dedup that dropped one id and kept another twice, or emitted
+    a wrong id, fails here even where counts and the top-k agree."""
+    spec = W["exact_1m"].scaled(B=7, N=3000, clusters=32)
+    k = C + C2
+    log(f"[dedup set] C={C} C2={C2} k={k}")
+    inp = cuda_inputs(spec, seed=27)
+    prob = mol.Problem.from_inputs(inp)
+    g = torch.Generator(device="cuda").manual_seed(9)
+    cand = torch.randint(-1, spec.N, (spec.B, C), device="cuda", generator=g, dtype=torch.int32)
+    cand[1] = 42                      # every slot the same id
+    cand[2, : C // 2] = -1            # half empty
+    cand[3, 0] = spec.N + 5           # out of range: treated as empty
+    cand[4, C // 3:] = cand[4, : C - C // 3].clone()   # long runs of repeats
+    cand2 = None
+    if C2:
+        cand2 = torch.randint(-1, spec.N, (spec.B, C2), device="cuda", generator=g, dtype=torch.int32)
+        cand2[5] = cand[5, :C2]       # the second set repeats the first
+        cand2[6] = -1                 # the second set empty
+    s, i, nu = mol.rerank(prob, cand, k, cand2=cand2)
+    torch.cuda.synchronize()
+    cand_np = cand.cpu().numpy().astype(np.int64)
+    cand_np[cand_np >= spec.N] = -1
+    sets = [cand_np]
+    if C2:
+        c2 = cand2.cpu().numpy().astype(np.int64)
+        c2[c2 >= spec.N] = -1
+        sets.append(c2)
+    i, nu = i.cpu().numpy(), nu.cpu().numpy()
+    for b in range(spec.B):
+        want = mo.union_dedup([c[b] for c in sets])
+        assert_dedup_set(i[b], int(nu[b]), want, f"dedup C={C} C2={C2} query {b}")
 
 
 @pytest.mark.parametrize("name,spec,C", [
