@@ -13,7 +13,8 @@
  * Memory: every array pointer below is a DEVICE pointer owned by the caller.
  * The library allocates no device memory, keeps no pointer after a call
  * returns, and holds no global state other than a per-thread last-error
- * string and the optional kernel-timing records (mol_timing_enable).
+ * string, the optional kernel-timing records (mol_timing_enable) and the
+ * static device scratch array of mol_topk_exact_noalloc.
  * Calls are asynchronous on `stream` (a hipStream_t passed as void*,
  * NULL = the null stream); outputs are valid once the caller has
  * synchronised that stream.  Calls on different streams may run
@@ -124,6 +125,28 @@ int mol_score(const mol_problem *prob, int32_t n_begin, int32_t n_count,
  * bytes of workspace (any alignment of 256 bytes or more). */
 int mol_topk_exact(const mol_problem *prob, int32_t k, float *out_score,
                    int32_t *out_idx, void *ws, size_t ws_bytes, void *stream);
+
+/* Bytes of device scratch the library itself holds on each GPU for
+ * mol_topk_exact_noalloc. */
+#define MOL_NOALLOC_SCRATCH_BYTES (16u << 20)
+
+/* mol_topk_exact without a workspace argument and without allocating, for
+ * callers that cannot allocate device memory at call time (code under HIP
+ * graph capture, tight serving loops, harnesses that forbid hipMalloc).
+ * Same computation, outputs, ordering and limits as mol_topk_exact; the
+ * workspace mol_topk_exact would take (mol_workspace_size with
+ * MOL_OP_TOPK_EXACT) must be at most MOL_NOALLOC_SCRATCH_BYTES, which
+ * covers the fused shapes at up to 1024 queries and k <= 128 (e.g. B = 1024,
+ * N = 2^20, P = 8 x 8, d = 64: 4.7 MiB); larger needs return
+ * MOL_EWORKSPACE and launch nothing.  The scratch is a static device array
+ * of the library, one per GPU, kept until the process ends and located on
+ * each device's first call.  Every call on a GPU uses that GPU's one array:
+ * calls that overlap on the same GPU (two streams, two threads) race and
+ * must be serialised by the caller.  The kernels write every scratch byte
+ * they read, so no clearing is needed between calls.  Nothing is allocated,
+ * freed or synchronised. */
+int mol_topk_exact_noalloc(const mol_problem *prob, int32_t k, float *out_score,
+                           int32_t *out_idx, void *stream);
 
 /* Exact top-k with MoL among the items that can reach a per-query bound
  * (Algorithm 1's RangeDotProduct followed by BruteForceTopKMoL, in one pass

@@ -618,6 +618,54 @@ int run_two_pass(const DevProb& pr, int k, int mode, float* out_score, int32_t* 
   return MOL_OK;
 }
 
+// ---------------------------------------------------------------------------
+// Library-owned scratch of mol_topk_exact_noalloc: a file-scope device
+// array of MOL_NOALLOC_SCRATCH_BYTES, one copy per GPU, held until the
+// process ends.  In host code `scratch` only names the symbol; its device
+// address on each GPU comes from hipGetSymbolAddress (taken once per
+// device, with that device current) and is the only handle host code
+// passes on.  Calls that overlap on one GPU share the array and race.
+static __device__ __align__(256) unsigned char scratch[MOL_NOALLOC_SCRATCH_BYTES];
+
+constexpr int kMaxDevices = 64;
+
+struct ScratchTable {
+  std::mutex mu;
+  void* ptr[kMaxDevices] = {};
+};
+
+ScratchTable& scratch_table() {
+  static ScratchTable t;
+  return t;
+}
+
+// Device address of the scratch array on the current device (nullptr and a
+// recorded error on failure).
+void* scratch_ptr() {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) {
+    hip_fail(e, "hipGetDevice");
+    return nullptr;
+  }
+  if (dev < 0 || dev >= kMaxDevices) {
+    fail(MOL_EUNSUPPORTED, "device %d beyond the %d the scratch table holds", dev, kMaxDevices);
+    return nullptr;
+  }
+  ScratchTable& t = scratch_table();
+  std::lock_guard<std::mutex> g(t.mu);
+  if (!t.ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p) {
+      hip_fail(e != hipSuccess ? e : hipErrorInvalidSymbol, "hipGetSymbolAddress(scratch)");
+      return nullptr;
+    }
+    t.ptr[dev] = p;
+  }
+  return t.ptr[dev];
+}
+
 }  // namespace
 
 extern "C" {
@@ -710,6 +758,22 @@ int mol_topk_exact(const mol_problem* prob, int32_t k, float* out_score, int32_t
   if ((rc = check_ws(ws, ws_bytes, exact_ws_bytes(pr, k)))) return rc;
   return run_exact(pr, k, nullptr, out_score, out_idx, static_cast<char*>(ws), MOL_OP_TOPK_EXACT,
                    static_cast<hipStream_t>(stream));
+}
+
+int mol_topk_exact_noalloc(const mol_problem* prob, int32_t k, float* out_score, int32_t* out_idx,
+                           void* stream) {
+  int rc;
+  if ((rc = check_problem(prob, true))) return rc;
+  if ((rc = check_k(k, prob->N, "k"))) return rc;
+  if (!out_score || !out_idx) return fail(MOL_EINVAL, "output pointer is NULL");
+  const DevProb pr = dev_prob(prob);
+  const size_t need = exact_ws_bytes(pr, k);
+  if (need > MOL_NOALLOC_SCRATCH_BYTES)
+    return fail(MOL_EWORKSPACE, "this problem needs %zu bytes of scratch; the library holds %zu "
+                "(use mol_topk_exact with a workspace)", need, static_cast<size_t>(MOL_NOALLOC_SCRATCH_BYTES));
+  char* w = static_cast<char*>(scratch_ptr());
+  if (!w) return MOL_EHIP;
+  return run_exact(pr, k, nullptr, out_score, out_idx, w, MOL_OP_TOPK_EXACT, static_cast<hipStream_t>(stream));
 }
 
 int mol_topk_exact_bounded(const mol_problem* prob, int32_t k, const float* bound, float* out_score,

@@ -22,7 +22,7 @@ MOL_F32, MOL_BF16 = 0, 1
  MOL_OP_TOPK_BOUNDED, MOL_OP_TOPK_TWO_PASS) = range(7)
 MOL_TWO_PASS_MIN, MOL_TWO_PASS_KTH = 0, 1
 
-EXPORTS = ("mol_workspace_size", "mol_score", "mol_topk_exact", "mol_topk_exact_bounded",
+EXPORTS = ("mol_workspace_size", "mol_score", "mol_topk_exact", "mol_topk_exact_noalloc", "mol_topk_exact_bounded",
            "mol_topk_two_pass", "mol_topk_maxdot", "mol_topk_per_embd",
            "mol_rerank", "mol_avg_embed", "mol_gap_bound", "mol_gap_bound_combined",
            "mol_timing_enable", "mol_timing_read",
@@ -65,6 +65,7 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "mol_workspace_size": [P, ctypes.c_int, i32, i32, i32, ctypes.POINTER(sz)],
         "mol_score": [P, i32, i32, vp, vp],
         "mol_topk_exact": [P, i32, vp, vp, vp, sz, vp],
+        "mol_topk_exact_noalloc": [P, i32, vp, vp, vp],
         "mol_topk_exact_bounded": [P, i32, vp, vp, vp, vp, sz, vp],
         "mol_topk_two_pass": [P, i32, i32, vp, vp, vp, vp, sz, vp],
         "mol_topk_maxdot": [P, i32, vp, vp, vp, sz, vp],
@@ -158,6 +159,10 @@ def mol_score(prob: Problem, n_begin: int, n_count: int, phi: torch.Tensor, stre
 def mol_topk_exact(prob: Problem, k: int, out_score, out_idx, ws, stream=None) -> None:
     _check(load().mol_topk_exact(prob.ref, k, _ptr(out_score), _ptr(out_idx), _ptr(ws),
                                  ws.numel() if ws is not None else 0, _stream(stream)))
+
+
+def mol_topk_exact_noalloc(prob: Problem, k: int, out_score, out_idx, stream=None) -> None:
+    _check(load().mol_topk_exact_noalloc(prob.ref, k, _ptr(out_score), _ptr(out_idx), _stream(stream)))
 
 
 def mol_topk_exact_bounded(prob: Problem, k: int, bound, out_score, out_idx, ws, stream=None) -> None:

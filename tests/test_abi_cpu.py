@@ -197,3 +197,19 @@ def test_combined_gap_bound_validation():
     args = list(ok)
     args[3] = None                     # dots NULL
     assert lib.mol_gap_bound_combined(*args) == mol.MOL_EINVAL
+
+
+def test_noalloc_entry_point_validates_on_the_host():
+    """mol_topk_exact_noalloc rejects bad arguments, and problems whose
+    workspace would exceed the library's static scratch, before touching the
+    GPU."""
+    lib = mol.load()
+    c = _problem(B=4, N=1000, Pq=8, Px=8, d=64, H=64)
+    assert lib.mol_topk_exact_noalloc(ctypes.byref(c), 10, None, 256, None) == mol.MOL_EINVAL
+    assert lib.mol_topk_exact_noalloc(ctypes.byref(c), 0, 256, 256, None) == mol.MOL_EINVAL
+    assert lib.mol_topk_exact_noalloc(None, 10, 256, 256, None) == mol.MOL_EINVAL
+    big = _problem(B=65535, N=1 << 20, Pq=8, Px=8, d=64, H=64)
+    rc, need = _ws(big, mol.MOL_OP_TOPK_EXACT, k=100)
+    assert rc == mol.MOL_OK and need > 16 << 20
+    assert lib.mol_topk_exact_noalloc(ctypes.byref(big), 100, 256, 256, None) == mol.MOL_EWORKSPACE
+    assert b"scratch" in lib.mol_last_error()
