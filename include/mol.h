@@ -76,6 +76,9 @@ typedef enum {
   MOL_TWO_PASS_KTH = 1   /* k-th largest MoL score over G (tighter)          */
 } mol_two_pass_mode;
 
+/* Problem flags (mol_problem.flags). */
+#define MOL_FLAG_F32_GATING 1u  /* gating MLP in float32 (see mol_problem) */
+
 /* Limits of the kernel set. */
 #define MOL_MAX_B 65535   /* queries per call                                */
 #define MOL_MAX_P 64      /* Pq * Px                                        */
@@ -86,7 +89,20 @@ typedef enum {
 
 /* One retrieval problem: shapes, storage type and device pointers (the
  * notation table of Section 2; gating parameters per Appendix A.3).
- * Pointers not used by an entry point may be NULL (see each function). */
+ * Pointers not used by an entry point may be NULL (see each function).
+ *
+ * Precision of the gating MLP.  By default the bf16 fused kernels evaluate
+ * it on matrix cores with float16 operands: s, -log2(e) W1 and the hidden
+ * activations are rounded to float16 (W2 is exact), accumulation is
+ * float32.  The resulting error in phi grows with the scale of W1 and W2:
+ * measured against float64 on the exact_1m data recipe, its largest value
+ * over 16 x 4096 pairs is 2.2e-6 for entries of standard deviation 0.1,
+ * 7.8e-6 for 0.2, 2.0e-5 for 0.3 and 1.5e-4 for 0.5.  The fused path is
+ * meant for gating weights with entries of RMS up to 0.3.  Beyond that,
+ * set MOL_FLAG_F32_GATING: the gating MLP, softmax and phi then run in
+ * float32 in the pair-wise kernel (component dots still on matrix cores,
+ * exact products, float32 sums), several times slower.  float32 problems
+ * always take that path. */
 typedef struct mol_problem {
   int32_t B;      /* number of queries                                      */
   int32_t N;      /* number of items                                        */
@@ -103,6 +119,7 @@ typedef struct mol_problem {
   const float *b1;
   const void *W2;
   const float *b2;
+  uint32_t flags; /* MOL_FLAG_* bits; 0 for the defaults                    */
 } mol_problem;
 
 /* Bytes of workspace an entry point needs for this problem (k, kprime and C

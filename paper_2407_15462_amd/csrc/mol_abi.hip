@@ -111,6 +111,7 @@ int check_problem(const mol_problem* p, bool gating) {
   if (p->B > MOL_MAX_B) return fail(MOL_EUNSUPPORTED, "B = %d exceeds %d", p->B, MOL_MAX_B);
   if (p->dtype != MOL_F32 && p->dtype != MOL_BF16)
     return fail(MOL_EUNSUPPORTED, "dtype %d is not MOL_F32 or MOL_BF16", p->dtype);
+  if (p->flags & ~MOL_FLAG_F32_GATING) return fail(MOL_EINVAL, "unknown flag bits 0x%x", p->flags);
   if (p->Pq > MOL_MAX_P || p->Px > MOL_MAX_P || p->Pq * p->Px > MOL_MAX_P)
     return fail(MOL_EUNSUPPORTED, "P = Pq*Px = %d*%d exceeds %d", p->Pq, p->Px, MOL_MAX_P);
   if (p->d > MOL_MAX_D) return fail(MOL_EUNSUPPORTED, "d = %d exceeds %d", p->d, MOL_MAX_D);
@@ -124,7 +125,7 @@ int check_problem(const mol_problem* p, bool gating) {
 DevProb dev_prob(const mol_problem* p) {
   DevProb d;
   d.B = p->B; d.N = p->N; d.Pq = p->Pq; d.Px = p->Px; d.P = p->Pq * p->Px;
-  d.d = p->d; d.H = p->H; d.dtype = p->dtype;
+  d.d = p->d; d.H = p->H; d.dtype = p->dtype; d.flags = p->flags;
   d.Q = p->Q; d.X = p->X; d.a_q = p->a_q; d.a_x = p->a_x;
   d.W1 = p->W1; d.b1 = p->b1; d.W2 = p->W2; d.b2 = p->b2;
   return d;
@@ -200,8 +201,9 @@ hipError_t pairwise_tile(const DevProb& pr, const StreamPlan& s, char* w, int mo
 
 // Reduce rows of `len` keys held in buffer A (stride strideA) to the top k,
 // written to `out` (stride out_stride).  Uses A and B as ping-pong buffers.
+// gate: NULL, or a device flag; every launch does nothing while it is zero.
 int reduce_rows(const StreamPlan& s, char* ws, long len, uint64_t* out, long out_stride,
-                hipStream_t st) {
+                hipStream_t st, const uint32_t* gate = nullptr) {
   uint64_t* bufs[2] = {reinterpret_cast<uint64_t*>(ws + s.offA), reinterpret_cast<uint64_t*>(ws + s.offB)};
   long strides[2] = {s.strideA, s.strideB};
   int cur = 0;
@@ -211,7 +213,8 @@ int reduce_rows(const StreamPlan& s, char* ws, long len, uint64_t* out, long out
   if (len > 2 * kRadixChunk && s.rows < kRadixFewRows && s.k <= 1024) {
     const int chunks = static_cast<int>((len + kRadixChunk - 1) / kRadixChunk);
     if (static_cast<long>(chunks) * s.k > strides[1]) return fail(MOL_EHIP, "internal: chunk lists too long");
-    MOL_TRY_HIP(launch_radix_topk_chunks(bufs[0], strides[0], s.rows, len, s.k, chunks, kRadixChunk, bufs[1], st),
+    MOL_TRY_HIP(launch_radix_topk_chunks(bufs[0], strides[0], s.rows, len, s.k, chunks, kRadixChunk, bufs[1], st,
+                                         gate),
                 "radix top-k per chunk");
     // (rows of chunks * k keys at stride chunks * k)
     strides[1] = static_cast<long>(chunks) * s.k;
@@ -220,7 +223,8 @@ int reduce_rows(const StreamPlan& s, char* ws, long len, uint64_t* out, long out
   }
   // long rows or large k: one radix selection per row
   if (s.k > 1024 || len > kRadixRowMin) {
-    MOL_TRY_HIP(launch_radix_topk(bufs[cur], strides[cur], s.rows, len, s.k, out, out_stride, st), "radix top-k");
+    MOL_TRY_HIP(launch_radix_topk(bufs[cur], strides[cur], s.rows, len, s.k, out, out_stride, st, nullptr, gate),
+                "radix top-k");
     return MOL_OK;
   }
   for (;;) {
@@ -228,13 +232,13 @@ int reduce_rows(const StreamPlan& s, char* ws, long len, uint64_t* out, long out
     const long nseg = (len + S - 1) / S;
     if (nseg == 1) {
       MOL_TRY_HIP(launch_segment_topk(bufs[cur], strides[cur], s.rows, static_cast<int>(len), s.k,
-                                      out, out_stride, st), "segment top-k");
+                                      out, out_stride, st, gate), "segment top-k");
       return MOL_OK;
     }
     const int nxt = 1 - cur;
     if (nseg * s.k > strides[nxt]) return fail(MOL_EHIP, "internal: top-k buffer too small");
     MOL_TRY_HIP(launch_segment_topk(bufs[cur], strides[cur], s.rows, static_cast<int>(len), s.k,
-                                    bufs[nxt], strides[nxt], st), "segment top-k");
+                                    bufs[nxt], strides[nxt], st, gate), "segment top-k");
     len = nseg * s.k;
     cur = nxt;
   }
@@ -329,7 +333,8 @@ struct PerEmbdPlan {
   StreamPlan s;
   PerEmbdGrid g;
   int KL = 0;
-  size_t offFinal = 0, offStg = 0, offBmax = 0, offThr = 0, bytes = 0;
+  size_t offFinal = 0, offStg = 0, offBmax = 0, offThr = 0, offThrT = 0;
+  size_t offCtl = 0, offKeys = 0, offHotV = 0, offHotN = 0, offWork = 0, bytes = 0;
 };
 
 PerEmbdPlan plan_per_embd(const DevProb& pr, int kp) {
@@ -348,10 +353,36 @@ PerEmbdPlan plan_per_embd(const DevProb& pr, int kp) {
   s.offB = off;     off = align_up(off + 8ul * s.rows * s.strideB);
   f.offFinal = off; off = align_up(off + 8ul * s.rows * kp);
   f.offStg = off;   off = align_up(off + 8ul * s.rows * f.g.s2.R * per_embd_stage_cap(kp));
-  f.offBmax = off;  off = align_up(off + 4ul * s.rows * f.g.s1.R * 2 * f.g.nbk);
+  f.offBmax = off;  off = align_up(off + 4ul * s.rows * f.g.s1.R * f.g.nbk);
   f.offThr = off;   off = align_up(off + 4ul * s.rows);
+  f.offThrT = off;  off = align_up(off + 4ul * s.rows);
+  if (f.g.pruned) {
+    const size_t nvec = static_cast<size_t>(pr.B) * pr.Pq;
+    f.offCtl = off;   off = align_up(off + 4ul * (s.rows + 2) + 4);       // counts, flag, work-list length
+    f.offKeys = off;  off = align_up(off + 8ul * s.rows * f.g.key_cap);
+    f.offHotV = off;  off = align_up(off + 4ul * f.g.groups * nvec);
+    f.offHotN = off;  off = align_up(off + 4ul * f.g.groups);
+    f.offWork = off;  off = align_up(off + 4ul * f.g.groups * f.g.CH);
+  }
   f.bytes = off;
   return f;
+}
+
+PerEmbdBufs per_embd_bufs(const PerEmbdPlan& f, char* w) {
+  PerEmbdBufs b;
+  b.lists = reinterpret_cast<uint64_t*>(w + f.s.offA);
+  b.stg = reinterpret_cast<uint64_t*>(w + f.offStg);
+  b.bmax = reinterpret_cast<float*>(w + f.offBmax);
+  b.thr = reinterpret_cast<float*>(w + f.offThr);
+  b.thr_t = reinterpret_cast<float*>(w + f.offThrT);
+  if (f.g.pruned) {
+    b.ctl = reinterpret_cast<uint32_t*>(w + f.offCtl);
+    b.keys = reinterpret_cast<uint64_t*>(w + f.offKeys);
+    b.hot_v = reinterpret_cast<int*>(w + f.offHotV);
+    b.hot_n = reinterpret_cast<int*>(w + f.offHotN);
+    b.work = reinterpret_cast<int*>(w + f.offWork);
+  }
+  return b;
 }
 
 // Per-component top-k' for the shapes without the fused per-component
@@ -515,15 +546,18 @@ int run_per_embd(const DevProb& pr, int kprime, float* out_dot, int32_t* out_idx
   const int rows = pr.B * pr.P;
   if (per_embd_supported(pr, kprime)) {
     const PerEmbdPlan f = plan_per_embd(pr, kprime);
-    uint64_t* lists = reinterpret_cast<uint64_t*>(w + f.s.offA);
+    const PerEmbdBufs b = per_embd_bufs(f, w);
     uint64_t* fin = reinterpret_cast<uint64_t*>(w + f.offFinal);
-    uint64_t* stg = reinterpret_cast<uint64_t*>(w + f.offStg);
-    float* bmax = reinterpret_cast<float*>(w + f.offBmax);
-    float* thr = reinterpret_cast<float*>(w + f.offThr);
-    MOL_TIMED_LAUNCH(timed_op, st, launch_per_embd(pr, kprime, f.g, bmax, thr, lists, stg, st),
-                     "per-component top-k'");
-    if ((rc = reduce_rows(f.s, w, static_cast<long>(f.g.s2.R) * f.KL, fin, kprime, st))) return rc;
-    MOL_TRY_HIP(launch_decode(fin, kprime, rows, kprime, out_dot, out_idx, st), "decode");
+    MOL_TIMED_LAUNCH(timed_op, st, launch_per_embd(pr, kprime, f.g, b, st), "per-component top-k'");
+    // pruned form: a sort per list, then the threshold scan's lists are
+    // reduced only if some list overflowed its key buffer (flag ctl[rows])
+    const uint32_t* gate = nullptr;
+    if (f.g.pruned) {
+      MOL_TRY_HIP(launch_per_embd_select(pr, kprime, f.g, b, out_dot, out_idx, st), "per-component select");
+      gate = b.ctl + rows;
+    }
+    if ((rc = reduce_rows(f.s, w, static_cast<long>(f.g.s2.R) * f.KL, fin, kprime, st, gate))) return rc;
+    MOL_TRY_HIP(launch_decode(fin, kprime, rows, kprime, out_dot, out_idx, st, gate), "decode");
     return MOL_OK;
   }
   if (use_thresh_per_embd(pr, kprime)) {

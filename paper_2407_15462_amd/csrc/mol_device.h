@@ -11,6 +11,7 @@ namespace mol {
 // Kernel-side view of a mol_problem (plain pointers, P precomputed).
 struct DevProb {
   int B, N, Pq, Px, P, d, H, dtype;
+  unsigned flags;   // MOL_FLAG_* bits
   const void* Q;
   const void* X;
   const float* a_q;

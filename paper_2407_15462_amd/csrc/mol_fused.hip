@@ -375,7 +375,9 @@ static bool fused_shape(const DevProb& pr, bool mlp) {
   return false;
 }
 
-bool fused_supported(const DevProb& pr, int k) { return fused_shape(pr, true) && k <= WaveTopk::kList; }
+bool fused_supported(const DevProb& pr, int k) {
+  return !(pr.flags & MOL_FLAG_F32_GATING) && fused_shape(pr, true) && k <= WaveTopk::kList;
+}
 bool fused_maxdot_supported(const DevProb& pr, int k) {
   return fused_shape(pr, false) && k <= WaveTopk::kList;
 }

@@ -177,8 +177,9 @@ __global__ __launch_bounds__(256) void k_dots_generic(DevProb pr, int n_begin, i
 template <int S, int NT>
 __global__ __launch_bounds__(NT) void k_segment_topk(const uint64_t* __restrict__ in, long in_stride,
                                                      int L, int k, uint64_t* __restrict__ out,
-                                                     long out_stride) {
+                                                     long out_stride, const uint32_t* __restrict__ gate) {
   __shared__ uint64_t sk[S];
+  if (gate && *gate == 0u) return;             // whole workgroup: a path that is not taken
   const long row = blockIdx.y;
   const long base = static_cast<long>(blockIdx.x) * S;
   const uint64_t* src = in + row * in_stride + base;
@@ -227,7 +228,9 @@ __global__ __launch_bounds__(NT) void k_segment_topk(const uint64_t* __restrict_
 }
 
 __global__ void k_decode_keys(const uint64_t* __restrict__ keys, long key_stride, int rows, int k,
-                              float* __restrict__ score, int32_t* __restrict__ idx) {
+                              float* __restrict__ score, int32_t* __restrict__ idx,
+                              const uint32_t* __restrict__ gate) {
+  if (gate && *gate == 0u) return;
   const long i = static_cast<long>(blockIdx.x) * blockDim.x + threadIdx.x;
   if (i >= static_cast<long>(rows) * k) return;
   const long r = i / k, j = i - (i / k) * k;
@@ -516,24 +519,29 @@ int segment_size_for(int L, int k) {
 }
 
 hipError_t launch_segment_topk(const uint64_t* in, long in_stride, int rows, int L, int k,
-                               uint64_t* out, long out_stride, hipStream_t st) {
+                               uint64_t* out, long out_stride, hipStream_t st, const uint32_t* gate) {
   const int S = segment_size_for(L, k);
   dim3 grid((L + S - 1) / S, rows);
   if (S == 256)
-    hipLaunchKernelGGL((k_segment_topk<256, 128>), grid, dim3(128), 0, st, in, in_stride, L, k, out, out_stride);
+    hipLaunchKernelGGL((k_segment_topk<256, 128>), grid, dim3(128), 0, st, in, in_stride, L, k, out, out_stride,
+                       gate);
   else if (S == 512)
-    hipLaunchKernelGGL((k_segment_topk<512, 256>), grid, dim3(256), 0, st, in, in_stride, L, k, out, out_stride);
+    hipLaunchKernelGGL((k_segment_topk<512, 256>), grid, dim3(256), 0, st, in, in_stride, L, k, out, out_stride,
+                       gate);
   else if (S == 1024)
-    hipLaunchKernelGGL((k_segment_topk<1024, 512>), grid, dim3(512), 0, st, in, in_stride, L, k, out, out_stride);
+    hipLaunchKernelGGL((k_segment_topk<1024, 512>), grid, dim3(512), 0, st, in, in_stride, L, k, out, out_stride,
+                       gate);
   else
-    hipLaunchKernelGGL((k_segment_topk<4096, 1024>), grid, dim3(1024), 0, st, in, in_stride, L, k, out, out_stride);
+    hipLaunchKernelGGL((k_segment_topk<4096, 1024>), grid, dim3(1024), 0, st, in, in_stride, L, k, out,
+                       out_stride, gate);
   return hipGetLastError();
 }
 
 hipError_t launch_decode(const uint64_t* keys, long key_stride, int rows, int k, float* score,
-                         int32_t* idx, hipStream_t st) {
+                         int32_t* idx, hipStream_t st, const uint32_t* gate) {
   const long n = static_cast<long>(rows) * k;
-  hipLaunchKernelGGL(k_decode_keys, dim3((n + 255) / 256), dim3(256), 0, st, keys, key_stride, rows, k, score, idx);
+  hipLaunchKernelGGL(k_decode_keys, dim3((n + 255) / 256), dim3(256), 0, st, keys, key_stride, rows, k, score, idx,
+                     gate);
   return hipGetLastError();
 }
 

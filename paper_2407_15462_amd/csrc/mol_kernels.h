@@ -55,22 +55,25 @@ hipError_t launch_phi_mfma(const DevProb& pr, int mode, const float* bound, int 
                            const float* sbuf, long s_pstride, long s_bstride, float* phi, long phi_stride,
                            uint64_t* keys, long key_stride, hipStream_t st);
 
-// Selection machinery over 64-bit sort keys.
+// Selection machinery over 64-bit sort keys.  gate: NULL, or a device flag
+// read at the start of every workgroup; the launch does nothing while it is
+// zero (the second of two alternative paths, chosen on the device).
 int segment_size_for(int L, int k);
 // Rows of L keys -> their top k (k <= 8192) by radix selection, one
 // workgroup per row (keys of a row distinct apart from empty ones).
 // row_len: NULL, or per-row key counts (row r reads min(row_len[r], L) keys).
 hipError_t launch_radix_topk(const uint64_t* in, long in_stride, int rows, long L, int k, uint64_t* out,
-                             long out_stride, hipStream_t st, const uint32_t* row_len = nullptr);
+                             long out_stride, hipStream_t st, const uint32_t* row_len = nullptr,
+                             const uint32_t* gate = nullptr);
 // The same per chunk of chunk_len keys (chunks * chunk_len >= L): row r's
 // chunk j's top k at out[(r * chunks + j) * k], so a row's chunk lists are
 // one contiguous run of chunks * k keys.
 hipError_t launch_radix_topk_chunks(const uint64_t* in, long in_stride, int rows, long L, int k, int chunks,
-                                    long chunk_len, uint64_t* out, hipStream_t st);
+                                    long chunk_len, uint64_t* out, hipStream_t st, const uint32_t* gate = nullptr);
 hipError_t launch_segment_topk(const uint64_t* in, long in_stride, int rows, int L, int k,
-                               uint64_t* out, long out_stride, hipStream_t st);
+                               uint64_t* out, long out_stride, hipStream_t st, const uint32_t* gate = nullptr);
 hipError_t launch_decode(const uint64_t* keys, long key_stride, int rows, int k, float* score,
-                         int32_t* idx, hipStream_t st);
+                         int32_t* idx, hipStream_t st, const uint32_t* gate = nullptr);
 hipError_t launch_fill(uint64_t* p, long n, uint64_t v, hipStream_t st);
 hipError_t launch_copy_rows(const uint64_t* src, long src_stride, int rows, int k, uint64_t* dst,
                             long dst_stride, hipStream_t st);
@@ -120,16 +123,36 @@ struct PerEmbdGrid {
     int R = 0, range_len = 0, G = 0;   // item ranges, items per range, vector groups
   };
   Scan s1, s2;                         // bucket scan, threshold scan
-  int bucket_tiles = 0, nbk = 0;       // 32-item tiles per bucket, buckets per (range, half)
+  int bucket_tiles = 0, nbk = 0;       // 32-item tiles per bucket, buckets per range
+  bool pruned = false;                 // the pruned second pass (else the threshold scan)
+  int key_cap = 0;                     // pruned pass: keys per list buffer
+  int vec_wg_pruned = 0, CH = 0;       // pruned pass: vectors per workgroup, chunks per bucket group
+  int groups = 0;                      // bucket groups Px * s1.R * nbk
+};
+// Device buffers of the per-component path (rows = B * Pq * Px lists).
+struct PerEmbdBufs {
+  float* bmax = nullptr;      // [Px][s1.R][nbk][B*Pq] bucket maxima
+  float* thr = nullptr;       // [rows] starting thresholds
+  float* thr_t = nullptr;     // [Px][B*Pq]: the same, component-major
+  uint64_t* lists = nullptr;  // [rows][s2.R][KL] keys (threshold scan)
+  uint64_t* stg = nullptr;    // [rows][s2.R][stage_cap] keys (threshold scan)
+  int* hot_v = nullptr;       // [groups][B*Pq] (pruned pass)
+  int* hot_n = nullptr;       // [groups]
+  int* work = nullptr;        // [groups * CH]
+  uint32_t* ctl = nullptr;    // [rows] key counts, then the overflow flag, then the work-list length
+  uint64_t* keys = nullptr;   // [rows][key_cap]
 };
 bool per_embd_supported(const DevProb& pr, int kp);
 int per_embd_list_cap(int kp);
 int per_embd_stage_cap(int kp);
 void per_embd_grid(const DevProb& pr, int kp, PerEmbdGrid& g);
-// bmax: [Px][s1.R][nbk][B*Pq][2] floats; thr: [B*Pq*Px] floats;
-// lists: [B*Pq*Px][s2.R][KL] keys; stg: [B*Pq*Px][s2.R][stage_cap] keys.
-hipError_t launch_per_embd(const DevProb& pr, int kp, const PerEmbdGrid& g, float* bmax, float* thr,
-                           uint64_t* lists, uint64_t* stg, hipStream_t st);
+// the scans (and, for the pruned form, its work list and pass); the lists
+// are then finished by launch_per_embd_select (pruned form) and, gated on
+// ctl[rows] (every list when it is set; always without the pruned form),
+// by the segmented reduction of `lists`
+hipError_t launch_per_embd(const DevProb& pr, int kp, const PerEmbdGrid& g, const PerEmbdBufs& b, hipStream_t st);
+hipError_t launch_per_embd_select(const DevProb& pr, int kp, const PerEmbdGrid& g, const PerEmbdBufs& b,
+                                  float* out_dot, int32_t* out_idx, hipStream_t st);
 
 }  // namespace mol
 

@@ -33,10 +33,12 @@ __device__ __forceinline__ bool has_prefix(uint64_t key, uint64_t prefix, int sh
 __global__ __launch_bounds__(kSelThreads) void k_radix_topk(const uint64_t* __restrict__ in, long in_stride,
                                                             long L_all, int k, uint64_t* __restrict__ out,
                                                             long out_stride, const uint32_t* __restrict__ row_len,
-                                                            int chunks, long chunk_len) {
+                                                            int chunks, long chunk_len,
+                                                            const uint32_t* __restrict__ gate) {
   __shared__ uint64_t buf[kSelCap];
   __shared__ uint32_t hist[256];
   __shared__ uint32_t s_bin, s_above, s_nz, s_count;
+  if (gate && *gate == 0u) return;             // whole workgroup: a path that is not taken
   const int tid = threadIdx.x, lane = tid & 63;
   // workgroup = (row, chunk j): keys [j chunk_len, (j + 1) chunk_len) of the row
   const long row = blockIdx.x / chunks, j = blockIdx.x - (blockIdx.x / chunks) * chunks;
@@ -164,18 +166,18 @@ __global__ __launch_bounds__(kSelThreads) void k_radix_topk(const uint64_t* __re
 }
 
 hipError_t launch_radix_topk(const uint64_t* in, long in_stride, int rows, long L, int k, uint64_t* out,
-                             long out_stride, hipStream_t st, const uint32_t* row_len) {
+                             long out_stride, hipStream_t st, const uint32_t* row_len, const uint32_t* gate) {
   if (k > kSelCap) return hipErrorInvalidValue;
   hipLaunchKernelGGL(k_radix_topk, dim3(rows), dim3(kSelThreads), 0, st, in, in_stride, L, k, out, out_stride,
-                     row_len, 1, L);
+                     row_len, 1, L, gate);
   return hipGetLastError();
 }
 
 hipError_t launch_radix_topk_chunks(const uint64_t* in, long in_stride, int rows, long L, int k, int chunks,
-                                    long chunk_len, uint64_t* out, hipStream_t st) {
+                                    long chunk_len, uint64_t* out, hipStream_t st, const uint32_t* gate) {
   if (k > kSelCap || chunks < 1 || static_cast<long>(chunks) * chunk_len < L) return hipErrorInvalidValue;
   hipLaunchKernelGGL(k_radix_topk, dim3(rows * chunks), dim3(kSelThreads), 0, st, in, in_stride, L, k, out,
-                     static_cast<long>(k), nullptr, chunks, chunk_len);
+                     static_cast<long>(k), nullptr, chunks, chunk_len, gate);
   return hipGetLastError();
 }
 

@@ -21,6 +21,7 @@ MOL_F32, MOL_BF16 = 0, 1
 (MOL_OP_SCORE, MOL_OP_TOPK_EXACT, MOL_OP_TOPK_PER_EMBD, MOL_OP_RERANK, MOL_OP_TOPK_MAXDOT,
  MOL_OP_TOPK_BOUNDED, MOL_OP_TOPK_TWO_PASS) = range(7)
 MOL_TWO_PASS_MIN, MOL_TWO_PASS_KTH = 0, 1
+MOL_FLAG_F32_GATING = 1
 
 EXPORTS = ("mol_workspace_size", "mol_score", "mol_topk_exact", "mol_topk_exact_noalloc", "mol_topk_exact_bounded",
            "mol_topk_two_pass", "mol_topk_maxdot", "mol_topk_per_embd",
@@ -44,7 +45,7 @@ class MolProblemC(ctypes.Structure):
                 ("Q", ctypes.c_void_p), ("X", ctypes.c_void_p),
                 ("a_q", ctypes.c_void_p), ("a_x", ctypes.c_void_p),
                 ("W1", ctypes.c_void_p), ("b1", ctypes.c_void_p),
-                ("W2", ctypes.c_void_p), ("b2", ctypes.c_void_p)]
+                ("W2", ctypes.c_void_p), ("b2", ctypes.c_void_p), ("flags", ctypes.c_uint32)]
 
 
 _lib: Optional[ctypes.CDLL] = None
@@ -118,7 +119,7 @@ class Problem:
     Gating tensors may be None for mol_topk_per_embd.
     """
 
-    def __init__(self, Q, X, a_q=None, a_x=None, W1=None, b1=None, W2=None, b2=None):
+    def __init__(self, Q, X, a_q=None, a_x=None, W1=None, b1=None, W2=None, b2=None, flags: int = 0):
         self.tensors = (Q, X, a_q, a_x, W1, b1, W2, b2)
         if Q.dtype == torch.bfloat16:
             dtype = MOL_BF16
@@ -131,14 +132,14 @@ class Problem:
         H = W1.shape[0] if W1 is not None else 1
         self.c = MolProblemC(B, N, Pq, Px, d if d == d2 else -1, H, dtype,
                              _ptr(Q), _ptr(X), _ptr(a_q), _ptr(a_x), _ptr(W1), _ptr(b1),
-                             _ptr(W2), _ptr(b2))
+                             _ptr(W2), _ptr(b2), flags)
         self.B, self.N, self.Pq, self.Px, self.d, self.H = B, N, Pq, Px, d, H
         self.P = Pq * Px
         self.device = Q.device
 
     @classmethod
-    def from_inputs(cls, inp) -> "Problem":
-        return cls(inp.Q, inp.X, inp.a_q, inp.a_x, inp.W1, inp.b1, inp.W2, inp.b2)
+    def from_inputs(cls, inp, flags: int = 0) -> "Problem":
+        return cls(inp.Q, inp.X, inp.a_q, inp.a_x, inp.W1, inp.b1, inp.W2, inp.b2, flags)
 
     @property
     def ref(self):

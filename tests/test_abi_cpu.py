@@ -213,3 +213,14 @@ def test_noalloc_entry_point_validates_on_the_host():
     assert rc == mol.MOL_OK and need > 16 << 20
     assert lib.mol_topk_exact_noalloc(ctypes.byref(big), 100, 256, 256, None) == mol.MOL_EWORKSPACE
     assert b"scratch" in lib.mol_last_error()
+
+
+def test_unknown_problem_flags_are_rejected():
+    lib = mol.load()
+    c = _problem()
+    c.flags = 0x6
+    rc, _ = _ws(c, mol.MOL_OP_TOPK_EXACT, k=5)
+    assert rc == mol.MOL_EINVAL and b"flag" in lib.mol_last_error()
+    c.flags = mol.MOL_FLAG_F32_GATING
+    rc, _ = _ws(c, mol.MOL_OP_TOPK_EXACT, k=5)
+    assert rc == mol.MOL_OK

@@ -186,6 +186,58 @@ def test_topk_per_embd_adversarial_order_and_ties():
             check_topk_row(s_all[:, p], ids[b, p], dots[b, p], kp, f"adversarial b={b} p={p}")
 
 
+@pytest.mark.parametrize("name,spec,kp", [
+    # more than 256 query vectors: the bucket scan, the per-bucket hot-vector
+    # lists and the pruned pass (lists of up to 256 keys)
+    ("pruned_p64", W["exact_1m"].scaled(B=40, N=20011, clusters=64), 128),
+    ("pruned_p64_k37", W["exact_1m"].scaled(B=36, N=9001, clusters=32), 37),
+    ("pruned_d128", W["hybrid_8m"].scaled(B=40, N=40009, clusters=64), 256),
+    ("pruned_d32", W["paper_books"].scaled(B=40, N=30011, clusters=32), 100),
+])
+def test_pruned_per_embd_matches_oracle(name, spec, kp):
+    log(f"[per_embd pruned] {name} B={spec.B} N={spec.N} P={spec.P} k'={kp}")
+    inp = cuda_inputs(spec, seed=25)
+    prob = mol.Problem(inp.Q, inp.X)
+    dots, ids = mol.topk_per_embd(prob, kp)
+    torch.cuda.synchronize()
+    op = oracle_problem(inp)
+    dots, ids = dots.cpu().numpy(), ids.cpu().numpy()
+    for b in range(spec.B):
+        s = mo.all_dots(op, b)
+        for p in range(spec.P):
+            check_topk_row(s[:, p], ids[b, p], dots[b, p], kp, f"{name} b={b} p={p}")
+
+
+def test_pruned_per_embd_overflow_and_ties():
+    """More than 256 query vectors with a tied block of 3000 identical items
+    on top of one list and an all-zero query vector: those lists receive far
+    more keys than their buffers hold, the device flag routes every list
+    through the threshold scan, and ties resolve to the lowest indices."""
+    spec = W["exact_1m"].scaled(B=40, N=24000, clusters=32)
+    kp = 128
+    inp = cuda_inputs(spec, seed=26)
+    blk0, blk1 = 2000, 5000
+    inp.X[0, blk0:blk1, :] = inp.Q[1, 0, :]
+    inp.Q[2, 3, :] = 0
+    log(f"[per_embd pruned overflow] B={spec.B} N={spec.N} k'={kp}")
+    prob = mol.Problem(inp.Q, inp.X)
+    dots, ids = mol.topk_per_embd(prob, kp)
+    torch.cuda.synchronize()
+    dots, ids = dots.cpu().numpy(), ids.cpu().numpy()
+    Px = spec.Px
+    assert ids[1, 0].tolist() == list(range(blk0, blk0 + kp))
+    assert np.all(dots[1, 0] == dots[1, 0, 0])
+    for px in range(Px):
+        p = 3 * Px + px
+        assert ids[2, p].tolist() == list(range(kp)), f"zero query, component {p}"
+        assert np.all(dots[2, p] == 0.0)
+    op = oracle_problem(inp)
+    for b in range(spec.B):
+        s_all = mo.all_dots(op, b)
+        for p in range(spec.P):
+            check_topk_row(s_all[:, p], ids[b, p], dots[b, p], kp, f"pruned overflow b={b} p={p}")
+
+
 def test_thresholded_per_embd_adversarial_order_and_ties():
     """Generic-shape lists (d = 768) long enough for the sampled threshold:
     a tied block on top that lies wholly in tiles the sample skips (every
@@ -503,6 +555,53 @@ def test_radix_chunked_first_pass_few_long_rows():
             check_topk_row(s_all[:, p], ids[b, p], dots[b, p], 50, f"radix_chunks f32 b={b} p={p}")
     for px in range(spec2.Px):
         assert ids[1, px].tolist() == list(range(50))
+
+
+def test_f32_gating_on_skewed_weights_matches_oracle():
+    """Gating weights of standard deviation 0.5 (the skewed workload, whose
+    largest gating weight per pair averages 0.23) lie outside the fused
+    f16-operand chain's range; with MOL_FLAG_F32_GATING the gating MLP,
+    softmax and phi run in float32 and mol_score, the exact top-k and the
+    rerank meet the 1e-4 bar."""
+    spec = W["exact_1m_skewed"].scaled(B=12, N=4099, clusters=64)
+    log(f"[f32 gating] skewed B={spec.B} N={spec.N} std={spec.gating_std}")
+    inp = cuda_inputs(spec, seed=28)
+    prob = mol.Problem.from_inputs(inp, flags=mol.MOL_FLAG_F32_GATING)
+    phi = mol.score(prob)
+    s, i = mol.topk_exact(prob, 100)
+    g = torch.Generator(device="cuda").manual_seed(7)
+    cand = torch.randint(-1, spec.N, (spec.B, 700), device="cuda", generator=g, dtype=torch.int32)
+    rs, ri, nu = mol.rerank(prob, cand, 100)
+    torch.cuda.synchronize()
+    op = oracle_problem(inp)
+    want = mo.mol_scores(op, list(range(spec.B)))
+    check_scores(phi.cpu().numpy(), want, what="f32_gating phi")
+    s, i = s.cpu().numpy(), i.cpu().numpy()
+    rs, ri, nu = rs.cpu().numpy(), ri.cpu().numpy(), nu.cpu().numpy()
+    cand_np = cand.cpu().numpy()
+    for b in range(spec.B):
+        check_topk_row(want[b], i[b], s[b], 100, f"f32_gating exact query {b}")
+        uniq = mo.union_dedup([cand_np[b]])
+        full = np.full(spec.N, -np.inf)
+        full[uniq] = want[b][uniq]
+        check_topk_row(full, ri[b], rs[b], 100, f"f32_gating rerank query {b}")
+
+
+def test_fused_gating_at_the_edge_of_its_range():
+    """The fused chain at the edge of its stated range (gating entries of
+    standard deviation 0.3) still meets the 1e-4 bar for scores and top-k."""
+    spec = dataclasses.replace(W["exact_1m"].scaled(B=12, N=4099, clusters=64), gating_std=0.3)
+    log(f"[fused gating] std={spec.gating_std} B={spec.B} N={spec.N}")
+    inp = cuda_inputs(spec, seed=29)
+    prob = mol.Problem.from_inputs(inp)
+    phi = mol.score(prob)
+    s, i = mol.topk_exact(prob, 100)
+    torch.cuda.synchronize()
+    want = mo.mol_scores(oracle_problem(inp), list(range(spec.B)))
+    check_scores(phi.cpu().numpy(), want, what="fused_std0.3 phi")
+    s, i = s.cpu().numpy(), i.cpu().numpy()
+    for b in range(spec.B):
+        check_topk_row(want[b], i[b], s[b], 100, f"fused_std0.3 exact query {b}")
 
 
 def test_worked_example_through_the_abi():
