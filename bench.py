@@ -42,6 +42,7 @@ CSRC = os.path.join(ROOT, "paper_2407_15462_amd", "csrc")
 # sources is stale and is not reported
 FUSED_SOURCES = ("mol_fused.hip", "mol_tile.h", "mol_device.h")
 TRAFFIC_FILE = "traffic_k_mol_fused_{workload}.txt"
+COUNTER_FILE = "counters_k_mol_fused_{workload}.txt"
 
 
 def parse():
@@ -80,11 +81,10 @@ def source_digest(names=FUSED_SOURCES) -> str:
     return h.hexdigest()
 
 
-def measured_traffic(workload: str):
-    """HBM bytes per launch of the fused exact scan from the committed
-    counter summary of this workload, or None when it is missing or was
-    taken on other kernel sources."""
-    path = os.path.join(PROFILES, TRAFFIC_FILE.format(workload=workload))
+def profile_values(name: str):
+    """key: value lines of a committed profile summary of the fused exact
+    scan, or None when it is missing or was taken on other kernel sources."""
+    path = os.path.join(PROFILES, name)
     if not os.path.exists(path):
         return None
     kv = {}
@@ -92,10 +92,30 @@ def measured_traffic(workload: str):
         if ":" in line and not line.startswith("#"):
             k, v = line.split(":", 1)
             kv[k.strip()] = v.strip()
-    if kv.get("source_sha256") != source_digest():
-        return None
+    return kv if kv.get("source_sha256") == source_digest() else None
+
+
+def measured_traffic(workload: str):
+    """HBM bytes per launch of the fused exact scan (FETCH_SIZE + WRITE_SIZE
+    counters, copy-calibrated), or None."""
+    kv = profile_values(TRAFFIC_FILE.format(workload=workload))
     try:
-        return float(kv["traffic_bytes_per_launch"])
+        return float(kv["traffic_bytes_per_launch"]) if kv else None
+    except (KeyError, ValueError):
+        return None
+
+
+def measured_counters(workload: str):
+    """Matrix-core and vector-ALU occupancy of the fused exact scan from its
+    committed counter summary (SQ_VALU_MFMA_BUSY_CYCLES, SQ_ACTIVE_INST_VALU,
+    SQ_VALU_MFMA_COEXEC_CYCLES, GRBM_GUI_ACTIVE), or None."""
+    kv = profile_values(COUNTER_FILE.format(workload=workload))
+    if not kv:
+        return None
+    keys = ("mfma_busy_frac", "valu_active_frac", "mfma_valu_coexec_frac", "simd_busy_frac",
+            "gpu_clock_ghz", "valu_insts_per_mfma", "trans_insts_per_mfma")
+    try:
+        return {k: float(kv[k]) for k in keys}
     except (KeyError, ValueError):
         return None
 
@@ -292,7 +312,8 @@ def run_workload(spec, steps, warmup, paths, seed):
         out["roofline"] = {"bound": "mfma", "achieved": ach, "peak": PEAK_BF16_TFLOPS,
                            "unit": "TFLOP/s", "frac": ach / PEAK_BF16_TFLOPS, "traffic": traffic,
                            "kernel": "k_mol_fused (MoL scoring + per-range top-k scan)",
-                           "flops_per_launch": B * N * flops_pair}
+                           "flops_per_launch": B * N * flops_pair,
+                           "counters": measured_counters(spec.name)}
     if ms["per_embd"]:
         t = (ms["per_embd"] + ms["topk_avg"] + ms["rerank"]) / 1e3
         recall = None
