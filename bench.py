@@ -168,8 +168,8 @@ def main():
     }
     line.update(out)
     if not args.no_cpu_baseline:
-        nq = args.cpu_baseline_queries or max(1, (8 << 20) // spec.N)
-        line["cpu_baseline"] = cpu_baseline(inp, spec, nq)
+        nq = args.cpu_baseline_queries or max(1, (16 << 20) // spec.N)
+        line["cpu_baseline"] = cpu_baseline(inp, spec, nq, max(1, nq // 8))
     del inp
     extras = [e for e in args.extras.split(",") if e and e != spec.name] if spec.name == "exact_1m" else []
     for name in extras:
@@ -558,7 +558,7 @@ def cpu_baseline(inp, spec, nq, nq_single=1):
     return {"value": nq / dt, "unit": "queries/s", "cores": used, "kind": "oracle",
             "sample": f"exact top-{spec.k} for {nq} of {spec.B} queries over all "
                       f"{spec.N} items (FP64 NumPy, BLAS threads={used}); single-thread leg: "
-                      f"{nq_single} query",
+                      f"the first {nq_single} of them",
             "seconds": dt, "threads": used,
             "thread_cap": f"{CPU_THREAD_CAP} (the host CPU share of one GPU)",
             "single_thread_queries_per_s": nq_single / dt1, "single_thread_seconds": dt1,
