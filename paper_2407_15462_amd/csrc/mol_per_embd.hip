@@ -368,23 +368,33 @@ __global__ __launch_bounds__(64 * waves_for(KL), 1) void k_topk_per_embd(
       // keys reaching the list's threshold go to the lane's LDS slots (the
       // item's end appends them with one atomic per lane); beyond the slots,
       // straight to the list's key buffer
+      // a block is entered when one of its lanes reaches the threshold
+      // (most blocks: about 5 lanes of a wave's 256 hit per tile); inside,
+      // each group of three values is tested on its maximum first, so the
+      // per-value tests run only in the groups that hold a hit
 #pragma unroll
       for (int nb = 0; nb < S::NB; ++nb) {
         if (m[nb] >= th[nb]) {
 #pragma unroll
-          for (int v = 0; v < 16; ++v) {
-            if (acc[nb][v] >= th[nb] && ((vmask >> v) & 1u)) {
-              const int item = n0 + (v >> 2) * 8 + 4 * half + (v & 3);
-              const uint64_t key = make_key(acc[nb][v], item);
-              const int used = (hitc >> (8 * nb)) & 0xFF;
-              if (used < kHitSlots) {
-                sHit[((wave * S::NB + nb) * kHitSlots + used) * 64 + lane] = key;
-                hitc += 1u << (8 * nb);
-              } else {
-                const long list = static_cast<long>(vv[nb]) * Px + px;
-                const uint32_t slot = atomicAdd(pa.cnt + list, 1u);
-                if (slot < static_cast<uint32_t>(pa.cap)) pa.keys[list * pa.cap + slot] = key;
-                else *pa.flag = 1u;
+          for (int g3 = 0; g3 < 6; ++g3) {
+            const int v0 = 3 * g3, v1 = g3 < 5 ? v0 + 3 : 16;
+            const float gmax = g3 < 5 ? fmaxf(fmaxf(acc[nb][v0], acc[nb][v0 + 1]), acc[nb][v0 + 2]) : acc[nb][15];
+            if (gmax < th[nb]) continue;
+#pragma unroll
+            for (int v = v0; v < v1; ++v) {
+              if (acc[nb][v] >= th[nb] && ((vmask >> v) & 1u)) {
+                const int item = n0 + (v >> 2) * 8 + 4 * half + (v & 3);
+                const uint64_t key = make_key(acc[nb][v], item);
+                const int used = (hitc >> (8 * nb)) & 0xFF;
+                if (used < kHitSlots) {
+                  sHit[((wave * S::NB + nb) * kHitSlots + used) * 64 + lane] = key;
+                  hitc += 1u << (8 * nb);
+                } else {
+                  const long list = static_cast<long>(vv[nb]) * Px + px;
+                  const uint32_t slot = atomicAdd(pa.cnt + list, 1u);
+                  if (slot < static_cast<uint32_t>(pa.cap)) pa.keys[list * pa.cap + slot] = key;
+                  else *pa.flag = 1u;
+                }
               }
             }
           }
