@@ -406,17 +406,24 @@ __global__ __launch_bounds__(64 * waves_for(KL), 1) void k_topk_per_embd(
 #pragma unroll
     for (int nb = 0; nb < S::NB; ++nb) hit = hit || m[nb] >= th[nb];
     if (__ballot(hit) == 0ull) return;
-    // append survivors to the lane's own staging region
+    // append survivors to the lane's own staging region (groups of three
+    // values tested on their maximum first, as in the pruned pass)
 #pragma unroll
     for (int nb = 0; nb < S::NB; ++nb) {
       if (m[nb] >= th[nb]) {
         uint64_t* sp = stg_ptr(nb, col, half);
 #pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          if (acc[nb][v] >= th[nb] && ((vmask >> v) & 1u)) {
-            const int item = n0 + (v >> 2) * 8 + 4 * half + (v & 3);
-            sp[cnt[nb]] = make_key(acc[nb][v], item);
-            ++cnt[nb];
+        for (int g3 = 0; g3 < 6; ++g3) {
+          const int v0 = 3 * g3, v1 = g3 < 5 ? v0 + 3 : 16;
+          const float gmax = g3 < 5 ? fmaxf(fmaxf(acc[nb][v0], acc[nb][v0 + 1]), acc[nb][v0 + 2]) : acc[nb][15];
+          if (gmax < th[nb]) continue;
+#pragma unroll
+          for (int v = v0; v < v1; ++v) {
+            if (acc[nb][v] >= th[nb] && ((vmask >> v) & 1u)) {
+              const int item = n0 + (v >> 2) * 8 + 4 * half + (v & 3);
+              sp[cnt[nb]] = make_key(acc[nb][v], item);
+              ++cnt[nb];
+            }
           }
         }
       }

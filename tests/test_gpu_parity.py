@@ -238,6 +238,37 @@ def test_pruned_per_embd_overflow_and_ties():
             check_topk_row(s_all[:, p], ids[b, p], dots[b, p], kp, f"pruned overflow b={b} p={p}")
 
 
+def test_pruned_per_embd_dense_bucket():
+    """60 distinct near-copies of one query vector placed in consecutive
+    items: two or three buckets then hold about half of that list's top k',
+    so its lanes find far more hits in one work item than their LDS slots
+    keep and append the rest with one atomic each.  The list's keys (the 60,
+    about one per other hot bucket and a few collisions: near 210) stay below
+    its buffer's 256, so the pruned result stands (no fallback)."""
+    spec = W["exact_1m"].scaled(B=40, N=24000, clusters=32)
+    kp = 128
+    inp = cuda_inputs(spec, seed=27)
+    g = torch.Generator(device="cpu").manual_seed(27)
+    n0, n1 = 6000, 6060
+    base = inp.Q[1, 0, :].float().cpu()
+    noise = torch.randn((n1 - n0, base.numel()), generator=g) * 0.05
+    near = base[None, :] + noise
+    near = near / near.norm(dim=1, keepdim=True)
+    inp.X[0, n0:n1, :] = near.to(inp.X.dtype).to(inp.X.device)
+    log(f"[per_embd pruned dense bucket] B={spec.B} N={spec.N} k'={kp}")
+    prob = mol.Problem(inp.Q, inp.X)
+    dots, ids = mol.topk_per_embd(prob, kp)
+    torch.cuda.synchronize()
+    dots, ids = dots.cpu().numpy(), ids.cpu().numpy()
+    # list (query 1, component 0) ranks the planted block first
+    assert set(range(n0, n1)) <= set(ids[1, 0].tolist())
+    op = oracle_problem(inp)
+    for b in range(spec.B):
+        s_all = mo.all_dots(op, b)
+        for p in range(spec.P):
+            check_topk_row(s_all[:, p], ids[b, p], dots[b, p], kp, f"pruned dense bucket b={b} p={p}")
+
+
 def test_thresholded_per_embd_adversarial_order_and_ties():
     """Generic-shape lists (d = 768) long enough for the sampled threshold:
     a tied block on top that lies wholly in tiles the sample skips (every
