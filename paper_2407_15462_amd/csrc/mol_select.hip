@@ -46,6 +46,23 @@ __global__ __launch_bounds__(kSelThreads) void k_radix_topk(const uint64_t* __re
   const uint64_t* src = in + row * in_stride + j * chunk_len;
   const long L = max(0l, min(chunk_len, Lrow - j * chunk_len));
 
+  // f(key) for every key of the range (keys past its end read as empty):
+  // eight loads per thread are issued before any is used, so a pass over
+  // global memory keeps that many in flight instead of one
+  auto for_keys = [&](auto&& f) {
+    constexpr int U = 8;
+    for (long i0 = tid; i0 < L; i0 += static_cast<long>(U) * kSelThreads) {
+      uint64_t kv[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const long i = i0 + static_cast<long>(u) * kSelThreads;
+        kv[u] = i < L ? src[i] : 0ull;
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u) f(kv[u]);
+    }
+  };
+
   uint64_t prefix = 0;
   uint32_t kk = static_cast<uint32_t>(k);   // rank of T among the keys sharing the prefix
   bool in_lds = false;
@@ -60,10 +77,9 @@ __global__ __launch_bounds__(kSelThreads) void k_radix_topk(const uint64_t* __re
         if (has_prefix(key, prefix, shift)) atomicAdd(&hist[digit_of(key, shift)], 1u);
       }
     } else {
-      for (long i = tid; i < L; i += kSelThreads) {
-        const uint64_t key = src[i];
+      for_keys([&](uint64_t key) {
         if (key != 0 && has_prefix(key, prefix, shift)) atomicAdd(&hist[digit_of(key, shift)], 1u);
-      }
+      });
     }
     __syncthreads();
     // wave 0: bins in descending order, 4 per lane (lane 0 holds 255..252);
@@ -116,13 +132,12 @@ __global__ __launch_bounds__(kSelThreads) void k_radix_topk(const uint64_t* __re
     if (!in_lds && shift > 0 && inbin <= static_cast<uint32_t>(kSelCap)) {
       if (tid == 0) s_count = 0u;
       __syncthreads();
-      for (long i = tid; i < L; i += kSelThreads) {
-        const uint64_t key = src[i];
+      for_keys([&](uint64_t key) {
         if (key != 0 && has_prefix(key, prefix, shift - 8)) {
           const uint32_t pos = atomicAdd(&s_count, 1u);
           if (pos < static_cast<uint32_t>(kSelCap)) buf[pos] = key;   // (inbin of them: always)
         }
-      }
+      });
       __syncthreads();
       n_lds = min(s_count, static_cast<uint32_t>(kSelCap));
       in_lds = true;
@@ -133,13 +148,12 @@ __global__ __launch_bounds__(kSelThreads) void k_radix_topk(const uint64_t* __re
   __syncthreads();
   if (tid == 0) s_count = 0u;
   __syncthreads();
-  for (long i = tid; i < L; i += kSelThreads) {
-    const uint64_t key = src[i];
+  for_keys([&](uint64_t key) {
     if (key >= T && key != 0) {
       const uint32_t pos = atomicAdd(&s_count, 1u);
       if (pos < static_cast<uint32_t>(kSelCap)) buf[pos] = key;   // (at most k of them: always)
     }
-  }
+  });
   __syncthreads();
   const uint32_t n = min(s_count, static_cast<uint32_t>(kSelCap));   // == min(k, nonzero keys)
   int S = 64;
