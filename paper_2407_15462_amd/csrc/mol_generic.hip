@@ -173,21 +173,44 @@ __global__ __launch_bounds__(256) void k_dots_generic(DevProb pr, int n_begin, i
 // descending, one ascending), the elementwise maximum (a bitonic sequence
 // holding the C largest of the pair) and bitonic-merging it, until one
 // descending run of C remains.  Where C >= S this is a full bitonic sort.
+// Empty keys sort last and never reach the result, so the segment's
+// nonzero keys are packed to the front first and the network runs over the
+// smallest power of two (at least C) that holds them.
 // ---------------------------------------------------------------------------
 template <int S, int NT>
 __global__ __launch_bounds__(NT) void k_segment_topk(const uint64_t* __restrict__ in, long in_stride,
                                                      int L, int k, uint64_t* __restrict__ out,
                                                      long out_stride, const uint32_t* __restrict__ gate) {
+  static_assert(NT % 64 == 0, "whole waves");
   __shared__ uint64_t sk[S];
+  __shared__ int s_nz;
   if (gate && *gate == 0u) return;             // whole workgroup: a path that is not taken
   const long row = blockIdx.y;
   const long base = static_cast<long>(blockIdx.x) * S;
   const uint64_t* src = in + row * in_stride + base;
   const int len = static_cast<int>(min(static_cast<long>(S), static_cast<long>(L) - base));
-  for (int t = threadIdx.x; t < S; t += NT) sk[t] = t < len ? src[t] : 0ull;
+  const int lane = threadIdx.x & 63;
+  if (threadIdx.x == 0) s_nz = 0;
   __syncthreads();
+  // nonzero keys to the front (in any order: the network sorts them), one
+  // LDS atomic per wave and pass
+  for (int t0 = 0; t0 < S; t0 += NT) {
+    const int t = t0 + static_cast<int>(threadIdx.x);
+    const uint64_t key = t < len ? src[t] : 0ull;
+    const uint64_t m = __ballot(key != 0ull);
+    int at = 0;
+    if (lane == 0 && m != 0ull) at = atomicAdd(&s_nz, __popcll(m));
+    at = __shfl(at, 0);
+    if (key != 0ull) sk[at + __popcll(m & ((1ull << lane) - 1ull))] = key;
+  }
+  __syncthreads();
+  const int nz = s_nz;
   int C = 64;
   while (C < k && C < S) C <<= 1;
+  int n0 = C;                                  // keys the network runs over: <= S
+  while (n0 < nz) n0 <<= 1;
+  for (int t = nz + static_cast<int>(threadIdx.x); t < n0; t += NT) sk[t] = 0ull;
+  __syncthreads();
   // one compare-exchange stage over the first n keys: pairs at distance
   // stride, direction alternating every dirspan keys
   auto stage = [&](int n, int stride, int dirspan) {
@@ -205,8 +228,8 @@ __global__ __launch_bounds__(NT) void k_segment_topk(const uint64_t* __restrict_
   };
   // runs of C keys, sorted descending / ascending in turn
   for (int size = 2; size <= C; size <<= 1)
-    for (int stride = size >> 1; stride > 0; stride >>= 1) stage(S, stride, size);
-  for (int n = S; n > C; n >>= 1) {
+    for (int stride = size >> 1; stride > 0; stride >>= 1) stage(n0, stride, size);
+  for (int n = n0; n > C; n >>= 1) {
     // run pair (2m, 2m+1) -> run m: the elementwise maximum, kept in
     // registers until every thread has read its pair
     uint64_t keep[S / (2 * NT) > 0 ? S / (2 * NT) : 1];
