@@ -2,12 +2,12 @@
 //
 // One wave scores 2 queries against 16 items per step.  GEMM1 (bf16
 // 16x16x32) forms S[(q, pq)][item] = Q[q][pq] . X[px][item] for every px with
-// rows 8 q + pq, so a lane of group g = lane / 16 holds query g / 2 and
-// pq in {4 (g%2) .. 4 (g%2) + 3}.  One permlane32 swap per register pair then
-// hands each query's 64 dot products to all 64 lanes in the run layout of
-// mol_tile.h, whose chained f16 MFMAs evaluate the gating MLP, the softmax
-// and phi (Eq. 1 / Eq. 2 with the SiLU gating MLP of Appendix A.3) without
-// any LDS re-layout.
+// rows 2 pq + q, so a lane of group g = lane / 16 holds pq in {2 g, 2 g + 1}
+// of both queries: each query's 64 dot products are already spread over the
+// 64 lanes in the run layout of mol_tile.h, whose chained f16 MFMAs evaluate
+// the gating MLP, the softmax and phi (Eq. 1 / Eq. 2 with the SiLU gating MLP
+// of Appendix A.3) with no lane exchange and no LDS re-layout.  (The max-dot
+// form keeps rows 8 q + pq, so that a lane group holds one query.)
 //
 // Epilogues (EPI):
 //  - kEpiTopk: a running per-query top-k of phi (Definition 1) kept in LDS
@@ -172,10 +172,11 @@ __global__ __launch_bounds__(64 * kWaves, EPI == kEpiMaxDot ? 2 : 1) void k_mol_
     qbound[qb] = EPI == kEpiBounded && qwv + qb < pr.B ? bound[qwv + qb] : __builtin_inff();
   Mlp mlp;
   if (MLP) mlp.load(pr, c, g);
-  // Q as GEMM1 A operands: row c = 8 q + pq, K slot 8g+e <-> d = 32 kk + 8 g + e
+  // Q as GEMM1 A operands: row c = 2 pq + q (gating forms) or 8 q + pq
+  // (max-dot form), K slot 8g+e <-> d = 32 kk + 8 g + e
   uint4 qop[S::KD];
   {
-    const int b = qwv + (c >> 3), pq = c & 7;
+    const int b = MLP ? qwv + (c & 1) : qwv + (c >> 3), pq = MLP ? c >> 1 : c & 7;
 #pragma unroll
     for (int kk = 0; kk < S::KD; ++kk)
       qop[kk] = b < pr.B
@@ -230,7 +231,7 @@ __global__ __launch_bounds__(64 * kWaves, EPI == kEpiMaxDot ? 2 : 1) void k_mol_
         for (int kk = 0; kk < S::KD; ++kk) acc1[px] = mfma_bf16(qop[kk], xb[px][kk], acc1[px]);
       }
       mfma_priority_end();
-      // separate the two queries: s[q][mu] holds p = base(g) + mu
+      // the two queries' runs: s2[q][mu] holds p = base(g) + mu
       float s2[2][S::RUN];
       float mrow = 0.f;
       if constexpr (EPI == kEpiMaxDot) {
@@ -247,13 +248,12 @@ __global__ __launch_bounds__(64 * kWaves, EPI == kEpiMaxDot ? 2 : 1) void k_mol_
         auto sw = __builtin_amdgcn_permlane16_swap(u, u, false, false);
         mrow = fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1]));
       } else {
+        // accumulator row 4 g + i is pq = 2 g + i / 2 of query i % 2, i.e.
+        // p = base(g) + (i / 2) PX + px
 #pragma unroll
         for (int mu = 0; mu < S::RUN; ++mu) {
-          const float a = acc1[mu % PX][mu / PX];
-          const float b = acc1[mu % PX][2 + mu / PX];
-          auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(a), __float_as_uint(b), false, false);
-          s2[0][mu] = __uint_as_float(sw[0]);
-          s2[1][mu] = __uint_as_float(sw[1]);
+          s2[0][mu] = acc1[mu % PX][2 * (mu / PX)];
+          s2[1][mu] = acc1[mu % PX][2 * (mu / PX) + 1];
         }
       }
       float phi[2];

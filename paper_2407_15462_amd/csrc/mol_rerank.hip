@@ -6,9 +6,9 @@
 // logits are gathered straight from the component-major corpus into MFMA
 // operand registers (one 16-byte load per lane per component and K block),
 // GEMM1 forms the 8 x 16 dot products of the query's components with the
-// items' components (rows 8..15 of the 16x16x32 tile are zero), one
-// permlane32 swap spreads them into the run layout of mol_tile.h, and the
-// shared MFMA epilogue evaluates the gating MLP, softmax and phi.  A running
+// items' components in rows 2 pq of the 16x16x32 tile (the odd rows are
+// zero), which leaves them in the run layout of mol_tile.h, and the shared
+// MFMA epilogue evaluates the gating MLP, softmax and phi.  A running
 // top-k per wave is merged across chunks afterwards by segmented sorts.
 #include "mol_tile.h"
 
@@ -55,12 +55,13 @@ __global__ __launch_bounds__(64 * kWaves, 2) void k_mol_rerank(
       const int p = base + 4 * pt + i;
       cbf[pt][i] = kLog2e * (pr.a_q[static_cast<long>(b) * P + p] + pr.b2[p]);
     }
-  // query b's components as GEMM1 rows 0..7 (rows 8..15 zero)
+  // query b's component pq as GEMM1 row 2 pq (odd rows zero)
   uint4 qop[KD];
 #pragma unroll
   for (int kk = 0; kk < KD; ++kk)
-    qop[kk] = c < 8 ? *reinterpret_cast<const uint4*>(Q + (static_cast<long>(b) * 8 + c) * D + 32 * kk + 8 * g)
-                    : make_uint4(0, 0, 0, 0);
+    qop[kk] = (c & 1) == 0
+                  ? *reinterpret_cast<const uint4*>(Q + (static_cast<long>(b) * 8 + (c >> 1)) * D + 32 * kk + 8 * g)
+                  : make_uint4(0, 0, 0, 0);
 
   for (int s0 = i0; s0 < i1; s0 += 16) {
     const int pos = s0 + c;
@@ -87,13 +88,10 @@ __global__ __launch_bounds__(64 * kWaves, 2) void k_mol_rerank(
 #pragma unroll
       for (int kk = 0; kk < KD; ++kk) acc1[px] = mfma_bf16(qop[kk], xop[px][kk], acc1[px]);
     }
+    // accumulator row 4 g + i with i even is pq = 2 g + i / 2: p = base(g) + (i / 2) PX + px
     float s[1][RUN];
 #pragma unroll
-    for (int mu = 0; mu < RUN; ++mu) {
-      auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(acc1[mu % PX][mu / PX]),
-                                                 __float_as_uint(acc1[mu % PX][2 + mu / PX]), false, false);
-      s[0][mu] = __uint_as_float(sw[0]);
-    }
+    for (int mu = 0; mu < RUN; ++mu) s[0][mu] = acc1[mu % PX][2 * (mu / PX)];
     float phi[1];
     mlp.template phi<1>(s, c0, phi);
     top.offer_score(NEG ? -phi[0] : phi[0], item, g == 0 && ok, lane);

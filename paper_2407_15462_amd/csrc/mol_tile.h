@@ -4,9 +4,10 @@
 //
 // Lane l of a wave: item column c = l % 16, group g = l / 16.  For one query
 // the lane holds the component dot products s_p for the contiguous run
-// p = base(g) + mu, mu < 2 Px, base(g) = (4 (g%2) + 2 (g/2)) Px.  This is the
-// layout a 16x16x32 GEMM over rows (query, pq) produces after one permlane32
-// swap (see mol_fused.hip).
+// p = base(g) + mu, mu < 2 Px, base(g) = 2 g Px.  This is the layout a
+// 16x16x32 GEMM over rows r = 2 pq + q (two queries q) produces directly:
+// lane group g receives rows 4 g .. 4 g + 3, i.e. pq in {2 g, 2 g + 1} of
+// both queries (see mol_fused.hip).
 //
 //   GEMM2 (f16)   U^T[j][item] = W1'[j][:] . s[:, item] + b1'[j]
 //                 s is the B operand: K slot 8g + e <-> p = base(g) + 8m + e.
@@ -91,7 +92,7 @@ __device__ __forceinline__ float max_groups(float x) {
 // than 100 times that.
 __device__ __forceinline__ float bound_margin(float mabs) { return 0x1p-12f * (1.f + mabs); }
 
-__device__ __forceinline__ int lane_base(int g, int PX) { return (4 * (g & 1) + 2 * (g >> 1)) * PX; }
+__device__ __forceinline__ int lane_base(int g, int PX) { return 2 * g * PX; }
 
 // s_waitcnt immediate that waits until at most n vector-memory operations
 // of this wave are outstanding (expcnt and lgkmcnt left unconstrained).
