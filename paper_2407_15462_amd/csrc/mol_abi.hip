@@ -306,7 +306,7 @@ RerankPlan plan_rerank(const DevProb& pr, int C, int k) {
 struct FusedExactPlan {
   StreamPlan s;  // offA = partial lists (stride R*k), offB = ping-pong
   int R = 0, range_len = 0, G = 0;
-  size_t offFinal = 0, bytes = 0;
+  size_t offFinal = 0, offRedo = 0, bytes = 0;
 };
 
 FusedExactPlan plan_fused_exact(const DevProb& pr, int k, bool maxdot = false) {
@@ -323,6 +323,7 @@ FusedExactPlan plan_fused_exact(const DevProb& pr, int k, bool maxdot = false) {
   s.offA = off;     off = align_up(off + 8ul * pr.B * s.strideA);
   s.offB = off;     off = align_up(off + 8ul * pr.B * s.strideB);
   f.offFinal = off; off = align_up(off + 8ul * pr.B * k);
+  f.offRedo = off;  off = align_up(off + 4ul * fused_redo_flags(f.R, f.G));
   f.bytes = off;
   return f;
 }
@@ -497,7 +498,8 @@ int run_exact(const DevProb& pr, int k, const float* bound, float* out_score, in
     const FusedExactPlan f = plan_fused_exact(pr, k);
     uint64_t* partial = reinterpret_cast<uint64_t*>(w + f.s.offA);
     uint64_t* fin = reinterpret_cast<uint64_t*>(w + f.offFinal);
-    MOL_TIMED_LAUNCH(timed_op, st, launch_fused_topk(pr, k, f.R, f.range_len, f.G, bound, partial, st),
+    int* redo = reinterpret_cast<int*>(w + f.offRedo);
+    MOL_TIMED_LAUNCH(timed_op, st, launch_fused_topk(pr, k, f.R, f.range_len, f.G, bound, partial, redo, st),
                      "fused MoL top-k");
     if ((rc = reduce_rows(f.s, w, static_cast<long>(f.R) * k, fin, k, st))) return rc;
     MOL_TRY_HIP(launch_decode(fin, k, pr.B, k, out_score, out_idx, st), "decode");

@@ -36,7 +36,7 @@ using namespace tile;
 
 namespace {
 
-enum FusedEpi { kEpiTopk = 0, kEpiDense = 1, kEpiBounded = 2, kEpiMaxDot = 3 };
+enum FusedEpi { kEpiTopk = 0, kEpiDense = 1, kEpiBounded = 2, kEpiMaxDot = 3, kEpiTopkPipe = 4 };
 
 constexpr int kWaves = 8;
 constexpr int kQueriesPerWG = 2 * kWaves;
@@ -92,9 +92,12 @@ template <int PX, int D, int H, int EPI>
 __global__ __launch_bounds__(64 * kWaves, EPI == kEpiMaxDot ? 2 : 1) void k_mol_fused(
     DevProb pr, int k, int R, int range_len, int G, int n_begin, int n_end,
     const float* __restrict__ bound, uint64_t* __restrict__ partial, float* __restrict__ phi_out,
-    long phi_stride) {
+    long phi_stride, int* __restrict__ redo) {
   constexpr bool DENSE = EPI == kEpiDense;
   constexpr bool MLP = EPI != kEpiMaxDot;
+  // software-pipelined top-k scan (hand-interleaved chain, H <= 64)
+  constexpr bool PIPE = EPI == kEpiTopkPipe;
+  static_assert(!PIPE || H <= 64, "the pipelined scan uses the hand-interleaved chain");
   using S = FusedShape<PX, D, H, MLP>;
   using Mlp = MolMlp<PX, H>;
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
@@ -107,6 +110,14 @@ __global__ __launch_bounds__(64 * kWaves, EPI == kEpiMaxDot ? 2 : 1) void k_mol_
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform
   const int c = lane & 15, g = lane >> 4;
   const int base = lane_base(g, PX);
+  // second launch after the pipelined scan: only the workgroups whose
+  // range it flagged run (uniform per workgroup, before any barrier)
+  if (EPI == kEpiTopk && redo) {
+    int any = 0;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) any |= redo[blockIdx.x * kWaves + w];
+    if (!any) return;
+  }
   int r, qg;
   wg_coords(blockIdx.x, R, G, r, qg);
   const int qwg = qg * kQueriesPerWG;     // first query of the workgroup
@@ -188,6 +199,147 @@ __global__ __launch_bounds__(64 * kWaves, EPI == kEpiMaxDot ? 2 : 1) void k_mol_
   if (ntiles >= kRing - 1) ring_barrier<(kRing - 2) * S::LOADS>();
   else ring_barrier<0>();
 
+  if constexpr (PIPE) {
+    // Software-pipelined top-k scan (H <= 64).  Each step's chain is split
+    // in two: stage A (both queries' GEMM2 -> SiLU -> GEMM3 and query 0's
+    // softmax sums) and stage B (query 1's softmax sums and the sums over an
+    // item's four lanes).  Stage B of step s is issued in one scheduling
+    // region with the LDS reads and GEMM1 of step s + 1, so that GEMM1's
+    // matrix instructions run under the wave's own vector work; then step s
+    // is finished (reciprocal, top-k offers) and stage A of step s + 1
+    // follows.  The arithmetic of every pair is that of phi2_interleaved.
+    //
+    // Ring discipline: one barrier per stage, in the step that is about to
+    // read the next stage.  A stage is last read in the first step of its
+    // own tile (the second step's reads are issued one step earlier), so past
+    // the barrier of tile t's second step every wave is done with tile t - 1
+    // and its buffer is refilled right away.
+    auto x_reads = [&](int t, int st, uint4(&xb)[PX][S::KD]) {
+      const unsigned char* xs = sX + (t % kRing) * S::XSTAGE;
+      const int n = 16 * st + c;
+#pragma unroll
+      for (int px = 0; px < PX; ++px) {
+        const unsigned char* row = xs + (px * S::TILE + n) * (D * 2);
+#pragma unroll
+        for (int kk = 0; kk < S::KD; ++kk) {
+          const int phys = (4 * kk + g) ^ (n % S::XROWCH);
+          xb[px][kk] = *reinterpret_cast<const uint4*>(row + 16 * phys);
+        }
+      }
+    };
+    auto ax_reads = [&](int t, int st, float4(&axv)[S::PT]) {
+      const unsigned char* as = sAx + (t % kRing) * S::ASTAGE;
+      const int n = 16 * st + c;
+#pragma unroll
+      for (int q4 = 0; q4 < S::PT; ++q4) {
+        const int phys = (base / 4 + q4) ^ (n % S::AROWCH);
+        axv[q4] = *reinterpret_cast<const float4*>(as + n * (P * 4) + 16 * phys);
+      }
+    };
+    // GEMM1: accumulator row 4 g + i is pq = 2 g + i / 2 of query i % 2
+    auto gemm1 = [&](const uint4(&xb)[PX][S::KD], float(&s2)[2][S::RUN]) {
+      f32x4_t acc1[PX];
+#pragma unroll
+      for (int px = 0; px < PX; ++px) {
+        acc1[px] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int kk = 0; kk < S::KD; ++kk) acc1[px] = mfma_bf16(qop[kk], xb[px][kk], acc1[px]);
+      }
+#pragma unroll
+      for (int mu = 0; mu < S::RUN; ++mu) {
+        s2[0][mu] = acc1[mu % PX][2 * (mu / PX)];
+        s2[1][mu] = acc1[mu % PX][2 * (mu / PX) + 1];
+      }
+    };
+    // GEMM3 accumulator inputs of both queries: log2(e) a_x + log2(e) (a_q + b2)
+    auto gate_bias2 = [&](const float4(&axv)[S::PT], f32x4_t(&c0)[2][S::PT]) {
+#pragma unroll
+      for (int qb = 0; qb < 2; ++qb)
+#pragma unroll
+        for (int pt = 0; pt < S::PT; ++pt) {
+          const float4 cb = *reinterpret_cast<const float4*>(sCb + (2 * wave + qb) * P + base + 4 * pt);
+          c0[qb][pt] = f32x4_t{fmaf(axv[pt].x, kLog2e, cb.x), fmaf(axv[pt].y, kLog2e, cb.y),
+                               fmaf(axv[pt].z, kLog2e, cb.z), fmaf(axv[pt].w, kLog2e, cb.w)};
+        }
+    };
+    bool redo_wave = false;
+    f32x4_t lg1[S::PT];     // query 1's logits of the step in flight
+    float s1[S::RUN];       // query 1's dot products of the step in flight
+    float den0 = 0.f, num0 = 0.f;
+    if (ntiles > 0) {
+      uint4 xb[PX][S::KD];
+      float4 axv[S::PT];
+      float s2[2][S::RUN];
+      f32x4_t c0[2][S::PT];
+      x_reads(0, 0, xb);
+      ax_reads(0, 0, axv);
+      gemm1(xb, s2);
+      gate_bias2(axv, c0);
+      mlp.template phi2_stage_a<5>(s2, c0, lg1, den0, num0);
+#pragma unroll
+      for (int mu = 0; mu < S::RUN; ++mu) s1[mu] = s2[1][mu];
+    }
+    for (int t = 0; t < ntiles; ++t) {
+#pragma unroll
+      for (int st = 0; st < 2; ++st) {
+        const int item = nr0 + S::TILE * t + 16 * st + c;
+        const bool item_ok = item < nr1;
+        const bool has_next = st == 0 || t + 1 < ntiles;
+        if (st == 1 && t + 1 < ntiles) {
+          ring_barrier<0>();
+          if (t + 2 < ntiles) stage(t + 2, (t + 2) % kRing);
+        }
+        // the next step's X reads and GEMM1 with this step's stage B (past
+        // the last step the current step's stage is read again, unused)
+        const int tn = st == 0 ? t : (has_next ? t + 1 : t), stn = st == 0 ? 1 : (has_next ? 0 : 1);
+        float s2n[2][S::RUN];
+        float Dn, Nm;
+        __builtin_amdgcn_sched_barrier(0);
+        {
+          uint4 xb[PX][S::KD];
+          x_reads(tn, stn, xb);
+          gemm1(xb, s2n);
+        }
+        mlp.phi2_stage_b(lg1, s1, den0, num0, Dn, Nm);
+        {
+          constexpr int kMfma = 0x008, kValu = 0x002 | 0x400, kDsRead = 0x100;
+          __builtin_amdgcn_sched_group_barrier(kDsRead, PX * S::KD, 0);
+#pragma unroll
+          for (int i = 0; i < PX * S::KD; ++i) {
+            __builtin_amdgcn_sched_group_barrier(kMfma, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(kValu, 3, 0);
+          }
+        }
+        // the next step's dot products are read after the branches below
+        mfma_drain();
+        // finish this step.  A sum outside [2^-60, 2^60] (logits far from
+        // zero) marks the wave: its workgroup's range is then scored again by
+        // the non-pipelined scan, which subtracts the row maximum (this
+        // launch's lists of that range are overwritten)
+        const float v = Nm * __builtin_amdgcn_rcpf(Dn);
+        redo_wave |= !__all(Dn >= 0x1p-60f && Dn <= 0x1p60f);
+        // one ballot decides whether either query has a candidate
+        {
+          const bool m0 = g == 0 && item_ok && v >= top[0].theta_score;
+          const bool m1 = g == 2 && item_ok && v >= top[1].theta_score;
+          if (__ballot(m0 || m1)) {
+            top[0].offer(m0 ? make_key(v, item) : 0ull, lane);
+            top[1].offer(m1 ? make_key(v, item) : 0ull, lane);
+          }
+        }
+        float4 axv[S::PT];
+        ax_reads(tn, stn, axv);
+        if (has_next) {
+          f32x4_t c0[2][S::PT];
+          gate_bias2(axv, c0);
+          mlp.template phi2_stage_a<5>(s2n, c0, lg1, den0, num0);
+#pragma unroll
+          for (int mu = 0; mu < S::RUN; ++mu) s1[mu] = s2n[1][mu];
+        }
+      }
+    }
+    if (lane == 0) redo[blockIdx.x * kWaves + wave] = redo_wave ? 1 : 0;
+  } else {
   for (int t = 0; t < ntiles; ++t) {
     const int buf = t % kRing;
     const unsigned char* xs = sX + buf * S::XSTAGE;
@@ -352,6 +504,7 @@ __global__ __launch_bounds__(64 * kWaves, EPI == kEpiMaxDot ? 2 : 1) void k_mol_
       ring_barrier<0>();
     }
   }
+  }
 
   if constexpr (!DENSE) {
 #pragma unroll
@@ -397,45 +550,58 @@ void fused_grid(const DevProb& pr, int n_count, int& R, int& range_len, int& G, 
 template <int PX, int D, int H, int EPI>
 static hipError_t launch_fused_t(const DevProb& pr, int k, int R, int range_len, int G, int n_begin,
                                  int n_end, const float* bound, uint64_t* partial, float* phi,
-                                 long phi_stride, hipStream_t st) {
+                                 long phi_stride, int* redo, hipStream_t st) {
   using S = FusedShape<PX, D, H, EPI != kEpiMaxDot>;
   auto kern = &k_mol_fused<PX, D, H, EPI>;
   hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                      hipFuncAttributeMaxDynamicSharedMemorySize, S::LDS_TOTAL);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(kern, dim3(R * G), dim3(64 * kWaves), S::LDS_TOTAL, st, pr, k, R, range_len,
-                     G, n_begin, n_end, bound, partial, phi, phi_stride);
+                     G, n_begin, n_end, bound, partial, phi, phi_stride, redo);
   return hipGetLastError();
 }
 
 template <int EPI>
 static hipError_t launch_fused_d(const DevProb& pr, int k, int R, int range_len, int G, int n_begin,
                                  int n_end, const float* bound, uint64_t* partial, float* phi,
-                                 long phi_stride, hipStream_t st) {
+                                 long phi_stride, int* redo, hipStream_t st) {
   // the max-dot epilogue has no gating MLP: one instantiation per (Px, d)
   if (pr.Px == 8 && pr.d == 32)
     return launch_fused_t<8, 32, 64, EPI>(pr, k, R, range_len, G, n_begin, n_end, bound, partial, phi,
-                                          phi_stride, st);
+                                          phi_stride, redo, st);
   if (pr.Px == 8)
     return launch_fused_t<8, 64, 64, EPI>(pr, k, R, range_len, G, n_begin, n_end, bound, partial, phi,
-                                          phi_stride, st);
-  if (pr.d == 128)
-    return launch_fused_t<4, 128, 128, EPI>(pr, k, R, range_len, G, n_begin, n_end, bound, partial, phi,
-                                            phi_stride, st);
+                                          phi_stride, redo, st);
+  if constexpr (EPI != kEpiTopkPipe) {
+    if (pr.d == 128)
+      return launch_fused_t<4, 128, 128, EPI>(pr, k, R, range_len, G, n_begin, n_end, bound, partial, phi,
+                                              phi_stride, redo, st);
+  }
   return launch_fused_t<4, 64, 64, EPI>(pr, k, R, range_len, G, n_begin, n_end, bound, partial, phi,
-                                        phi_stride, st);
+                                        phi_stride, redo, st);
 }
 
+long fused_redo_flags(int R, int G) { return static_cast<long>(R) * G * kWaves; }
+
 hipError_t launch_fused_topk(const DevProb& pr, int k, int R, int range_len, int G,
-                             const float* bound, uint64_t* partial, hipStream_t st) {
+                             const float* bound, uint64_t* partial, int* redo, hipStream_t st) {
   if (bound)
-    return launch_fused_d<kEpiBounded>(pr, k, R, range_len, G, 0, pr.N, bound, partial, nullptr, 0, st);
-  return launch_fused_d<kEpiTopk>(pr, k, R, range_len, G, 0, pr.N, nullptr, partial, nullptr, 0, st);
+    return launch_fused_d<kEpiBounded>(pr, k, R, range_len, G, 0, pr.N, bound, partial, nullptr, 0, nullptr,
+                                       st);
+  if (redo && pr.H <= 64) {
+    // pipelined scan, then the plain scan over the ranges it flagged
+    hipError_t e = launch_fused_d<kEpiTopkPipe>(pr, k, R, range_len, G, 0, pr.N, nullptr, partial, nullptr, 0,
+                                                redo, st);
+    if (e != hipSuccess) return e;
+    return launch_fused_d<kEpiTopk>(pr, k, R, range_len, G, 0, pr.N, nullptr, partial, nullptr, 0, redo, st);
+  }
+  return launch_fused_d<kEpiTopk>(pr, k, R, range_len, G, 0, pr.N, nullptr, partial, nullptr, 0, nullptr, st);
 }
 
 hipError_t launch_fused_maxdot(const DevProb& pr, int k, int R, int range_len, int G,
                                uint64_t* partial, hipStream_t st) {
-  return launch_fused_d<kEpiMaxDot>(pr, k, R, range_len, G, 0, pr.N, nullptr, partial, nullptr, 0, st);
+  return launch_fused_d<kEpiMaxDot>(pr, k, R, range_len, G, 0, pr.N, nullptr, partial, nullptr, 0, nullptr,
+                                    st);
 }
 
 hipError_t launch_fused_dense(const DevProb& pr, int n_begin, int n_count, float* phi,
@@ -443,7 +609,7 @@ hipError_t launch_fused_dense(const DevProb& pr, int n_begin, int n_count, float
   int R, range_len, G;
   fused_grid(pr, n_count, R, range_len, G, false);
   return launch_fused_d<kEpiDense>(pr, 1, R, range_len, G, n_begin, n_begin + n_count, nullptr, nullptr,
-                                   phi, n_count, st);
+                                   phi, n_count, nullptr, st);
 }
 
 }  // namespace mol

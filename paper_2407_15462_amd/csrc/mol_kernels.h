@@ -103,9 +103,14 @@ bool fused_supported(const DevProb& pr, int k);
 bool fused_maxdot_supported(const DevProb& pr, int k);
 void fused_grid(const DevProb& pr, int n_count, int& R, int& range_len, int& G, bool maxdot);
 // bound: NULL, or [B] floats: only items with max_p s_p (plus the rounding
-// margin) at or above bound[b] are ranked for query b
+// margin) at or above bound[b] are ranked for query b.  redo: NULL, or
+// fused_redo_flags(R, G) ints of workspace; with it (and no bound) shapes
+// with H <= 64 take the software-pipelined scan, whose workgroups flag a
+// range where a softmax sum left its safe range, and a second launch
+// rescores only the flagged ranges.
+long fused_redo_flags(int R, int G);
 hipError_t launch_fused_topk(const DevProb& pr, int k, int R, int range_len, int G,
-                             const float* bound, uint64_t* partial, hipStream_t st);
+                             const float* bound, uint64_t* partial, int* redo, hipStream_t st);
 hipError_t launch_fused_maxdot(const DevProb& pr, int k, int R, int range_len, int G,
                                uint64_t* partial, hipStream_t st);
 hipError_t launch_fused_dense(const DevProb& pr, int n_begin, int n_count, float* phi,

@@ -141,6 +141,18 @@ __device__ __forceinline__ void mfma_priority_end() {
   __builtin_amdgcn_sched_barrier(0);
 }
 
+// Waits out the result latency of every matrix instruction issued before it
+// (21 wait states: more than a 16-pass MFMA needs before a vector ALU read)
+// at the end of a block whose successors read MFMA results.  The compiler's
+// hazard padding does not cover every path into such a successor when the
+// MFMAs are followed by scheduling-group pseudo-instructions: a skipped
+// conditional block then left a GEMM3 result read with no wait states.
+__device__ __forceinline__ void mfma_drain() {
+  __builtin_amdgcn_sched_barrier(0);
+  asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 4");
+  __builtin_amdgcn_sched_barrier(0);
+}
+
 typedef __attribute__((address_space(3))) uint64_t lds_u64_t;
 
 // LDS offset of a pointer into shared memory.
@@ -497,6 +509,48 @@ struct MolMlp {
     const float v = Nm * __builtin_amdgcn_rcpf(D);
     out[0] = v;
     out[1] = v;
+  }
+
+  // The two-query chain split for a software-pipelined scan (the same
+  // instructions on the same operands as phi2_interleaved, so the sums are
+  // bit-identical).  Stage A: both queries' GEMM2 -> SiLU -> GEMM3 and query
+  // 0's softmax sums, scheduled as in phi2_interleaved; query 1's base-2
+  // logits are handed to stage B, which the caller issues together with the
+  // next step's GEMM1.
+  template <int VA>
+  __device__ void phi2_stage_a(const float (&s)[2][RUN], const f32x4_t (&c0)[2][PT], f32x4_t (&lg1)[PT],
+                               float& den0, float& num0) const {
+    uint4 sop[2][KP];
+    f32x4_t u[2][JT];
+    uint4 hop[2][KH];
+    f32x4_t lg0[PT];
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      pack_s(s[q], sop[q]);
+      gemm2(sop[q], u[q]);
+    }
+#pragma unroll
+    for (int q = 0; q < 2; ++q) silu(u[q], hop[q]);
+    gemm3(hop[0], c0[0], lg0);
+    gemm3(hop[1], c0[1], lg1);
+    weights(lg0, s[0], 0.f, den0, num0);
+    constexpr int kMfma = 0x008, kValu = 0x002 | 0x400;
+    __builtin_amdgcn_sched_group_barrier(kMfma, JT * KP, 0);
+#pragma unroll
+    for (int i = 0; i < JT * KP + 2 * PT * KH; ++i) {
+      __builtin_amdgcn_sched_group_barrier(kMfma, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(kValu, VA, 0);
+    }
+    // query 1's logits are read after the caller's next branch
+    mfma_drain();
+  }
+  // Stage B: query 1's softmax sums and the sums over an item's four lanes
+  // (D and Nm in the layout of row_sums).
+  __device__ static void phi2_stage_b(const f32x4_t (&lg1)[PT], const float (&s1)[RUN], float den0, float num0,
+                                      float& D, float& Nm) {
+    float den1, num1;
+    weights(lg1, s1, 0.f, den1, num1);
+    row_sums(den0, num0, den1, num1, D, Nm);
   }
 
   // phi for the lane's item under NQ (1 or 2) queries: out[q] is valid in
