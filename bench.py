@@ -60,6 +60,9 @@ def parse():
                          "(comma list; empty for none)")
     ap.add_argument("--extra-steps", type=int, default=3)
     ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--issue-probe", action="store_true",
+                    help="only time the issue-rate probe of the fused scan's per-step instruction "
+                         "mix (libmol_probe.so) at 1-4 waves per SIMD and print the implied floor")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy three times (the "
                          "reference dispatch that scales FETCH_SIZE / WRITE_SIZE counters)")
@@ -133,6 +136,49 @@ def copy_calibration():
     print(json.dumps({"copy_bytes": n, "dispatches": 3}), flush=True)
 
 
+def issue_probe(iters=2000):
+    """Time the probe kernel of include/mol_probe.h: the fused scan's
+    per-step instruction mix (48 MFMA, 97 transcendental, 221 plain vector
+    instructions, 32 pack conversions per wave-step) issued with no
+    dependencies, no memory traffic and no barriers, at 1-4 waves per SIMD.
+    Prints ns per wave-step per SIMD and the floor it implies for the fused
+    exact scan at exact_1m (1024 x 2^20 pairs = 32768 wave-steps per SIMD)."""
+    import ctypes
+
+    import torch
+    lib = ctypes.CDLL(os.path.join(ROOT, "paper_2407_15462_amd", "libmol_probe.so"))
+    lib.mol_probe_issue_mix.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p]
+    names = {0: "mix_interleaved", 1: "vector_only", 2: "mfma_only", 3: "mix_phased"}
+    stream = torch.cuda.current_stream()
+    out = {}
+    for w in (1, 2, 3, 4):
+        sink = torch.empty(256 * w * 256, dtype=torch.float32, device="cuda")
+        for p, name in names.items():
+            for n_it in (iters // 10, iters):
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record()
+                rc = lib.mol_probe_issue_mix(p, w, n_it, ctypes.c_void_p(sink.data_ptr()),
+                                             ctypes.c_void_p(stream.cuda_stream))
+                e1.record()
+                if rc != 0:
+                    raise RuntimeError(f"mol_probe_issue_mix failed ({rc})")
+            torch.cuda.synchronize()
+            ns = e0.elapsed_time(e1) * 1e6 / (w * iters)
+            out[f"{name}_w{w}_ns_per_wave_step"] = ns
+            print(f"# issue probe {name} waves/SIMD={w}: {ns:.1f} ns per wave-step", file=sys.stderr, flush=True)
+    steps_per_simd = (1024 // 2) * (1 << 20) // 16 // 1024
+    flops = 1024 * (1 << 20) * (2 * 64 * 64 + 4 * 64 * 64)
+    for w in (1, 2, 3, 4):
+        best = min(out[f"mix_interleaved_w{w}_ns_per_wave_step"], out[f"mix_phased_w{w}_ns_per_wave_step"])
+        ms = best * steps_per_simd / 1e6
+        out[f"exact_1m_floor_ms_w{w}"] = ms
+        out[f"exact_1m_frac_max_w{w}"] = flops / (ms / 1e3) / 1e12 / PEAK_BF16_TFLOPS
+    print(json.dumps({"issue_probe": out, "iters": iters,
+                      "mix_per_wave_step": {"mfma_16x16x32": 48, "transcendental": 97, "plain_valu": 221,
+                                            "cvt_pk_f16_f32": 32},
+                      "wave_steps_per_simd_exact_1m": steps_per_simd}), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
@@ -141,6 +187,9 @@ def main():
         sys.exit(2)
     if args.copy_calibration:
         copy_calibration()
+        return
+    if args.issue_probe:
+        issue_probe()
         return
     import torch
 

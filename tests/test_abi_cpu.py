@@ -26,6 +26,24 @@ def test_library_exports_every_declared_function():
         assert hasattr(lib, n), n
 
 
+def test_probe_library_exports_its_declared_function():
+    # the measurement aid of include/mol_probe.h, built next to libmol.so
+    path = os.path.join(ROOT, "paper_2407_15462_amd", "libmol_probe.so")
+    text = re.sub(r"/\*.*?\*/", "", open(os.path.join(ROOT, "include", "mol_probe.h")).read(), flags=re.S)
+    names = sorted(set(re.findall(r"\b(mol_[a-z_]+)\s*\(", text)))
+    assert names == ["mol_probe_issue_mix"]
+    lib = ctypes.CDLL(path)
+    for n in names:
+        assert hasattr(lib, n), n
+    # arguments are checked before any launch: nothing runs without a GPU
+    f = lib.mol_probe_issue_mix
+    f.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p]
+    assert f(0, 0, 10, 256, None) == -1
+    assert f(7, 1, 10, 256, None) == -1
+    assert f(0, 1, 0, 256, None) == -1
+    assert f(0, 1, 10, None, None) == -1
+
+
 def _problem(**kw):
     # Non-null dummy pointers: validation must reject before any launch.
     fake = 256
