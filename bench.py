@@ -123,6 +123,30 @@ def measured_counters(workload: str):
         return None
 
 
+def measured_issue_floor(workload: str):
+    """The issue-rate floor of the fused scan's instruction stream at its two
+    waves per SIMD (bench.py --issue-probe, summarised in profiles/), reported
+    while the kernel's counter summary -- whose per-step counts the probe
+    issues -- still matches the sources; else None."""
+    if measured_counters(workload) is None:
+        return None
+    path = os.path.join(PROFILES, f"issue_floor_k_mol_fused_{workload}.txt")
+    if not os.path.exists(path):
+        return None
+    kv = {}
+    for line in open(path):
+        if ":" in line and not line.startswith("#"):
+            k, v = line.split(":", 1)
+            kv[k.strip()] = v.strip()
+    try:
+        return {"waves_per_simd": int(kv["kernel_waves_per_simd"]),
+                "mix_floor_ms": float(kv["mix_floor_ms_w2"]), "mix_frac_max": float(kv["mix_frac_max_w2"]),
+                "full_stream_floor_ms": float(kv["full_stream_floor_ms_w2"]),
+                "full_stream_frac_max": float(kv["full_stream_frac_max_w2"])}
+    except (KeyError, ValueError):
+        return None
+
+
 def copy_calibration():
     import torch
     n = 1 << 30
@@ -148,7 +172,7 @@ def issue_probe(iters=2000):
     import torch
     lib = ctypes.CDLL(os.path.join(ROOT, "paper_2407_15462_amd", "libmol_probe.so"))
     lib.mol_probe_issue_mix.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p]
-    names = {0: "mix_interleaved", 1: "vector_only", 2: "mfma_only", 3: "mix_phased"}
+    names = {0: "mix_interleaved", 1: "vector_only", 2: "mfma_only", 3: "mix_phased", 4: "full_stream"}
     stream = torch.cuda.current_stream()
     out = {}
     for w in (1, 2, 3, 4):
@@ -173,6 +197,9 @@ def issue_probe(iters=2000):
         ms = best * steps_per_simd / 1e6
         out[f"exact_1m_floor_ms_w{w}"] = ms
         out[f"exact_1m_frac_max_w{w}"] = flops / (ms / 1e3) / 1e12 / PEAK_BF16_TFLOPS
+        full = out[f"full_stream_w{w}_ns_per_wave_step"] * steps_per_simd / 1e6
+        out[f"exact_1m_full_stream_floor_ms_w{w}"] = full
+        out[f"exact_1m_full_stream_frac_max_w{w}"] = flops / (full / 1e3) / 1e12 / PEAK_BF16_TFLOPS
     print(json.dumps({"issue_probe": out, "iters": iters,
                       "mix_per_wave_step": {"mfma_16x16x32": 48, "transcendental": 97, "plain_valu": 221,
                                             "cvt_pk_f16_f32": 32},
@@ -362,7 +389,8 @@ def run_workload(spec, steps, warmup, paths, seed):
                            "unit": "TFLOP/s", "frac": ach / PEAK_BF16_TFLOPS, "traffic": traffic,
                            "kernel": "k_mol_fused (MoL scoring + per-range top-k scan)",
                            "flops_per_launch": B * N * flops_pair,
-                           "counters": measured_counters(spec.name)}
+                           "counters": measured_counters(spec.name),
+                           "issue_floor": measured_issue_floor(spec.name)}
     if ms["per_embd"]:
         t = (ms["per_embd"] + ms["topk_avg"] + ms["rerank"]) / 1e3
         recall = None

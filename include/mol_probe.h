@@ -18,6 +18,9 @@
  *   pattern 1: the vector ALU part alone (no MFMA)
  *   pattern 2: the MFMA part alone
  *   pattern 3: the mix in two phases per iteration (48 MFMAs, then the rest)
+ *   pattern 4: pattern 0 plus the rest of the kernel's per-step stream: 28
+ *              LDS reads of 16 bytes per lane, 39 scalar ALU instructions and
+ *              45 one-slot hazard nops (still no dependencies)
  *
  * The launch holds waves_per_simd waves on each of the 1024 SIMDs
  * (256 x waves_per_simd workgroups of 4 waves); each wave runs `iters`

@@ -142,14 +142,15 @@ __device__ __forceinline__ void mfma_priority_end() {
 }
 
 // Waits out the result latency of every matrix instruction issued before it
-// (21 wait states: more than a 16-pass MFMA needs before a vector ALU read)
-// at the end of a block whose successors read MFMA results.  The compiler's
+// (11 wait states: a v_mfma_f32_16x16x32 result is readable 7 issue slots
+// after the MFMA, measured on gfx950; the kernels that use this issue no
+// larger MFMA) at the end of a block whose successors read MFMA results.  The compiler's
 // hazard padding does not cover every path into such a successor when the
 // MFMAs are followed by scheduling-group pseudo-instructions: a skipped
 // conditional block then left a GEMM3 result read with no wait states.
 __device__ __forceinline__ void mfma_drain() {
   __builtin_amdgcn_sched_barrier(0);
-  asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 4");
+  asm volatile("s_nop 7\n\ts_nop 2");
   __builtin_amdgcn_sched_barrier(0);
 }
 

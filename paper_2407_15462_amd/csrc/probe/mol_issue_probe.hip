@@ -16,6 +16,8 @@ typedef float f32x4_t __attribute__((ext_vector_type(4)));
 constexpr int kGroups = 48;        // MFMAs per wave-step
 
 struct Regs {
+  uint4 ld[2];     // LDS read results (never read in the loop)
+  uint32_t sc;     // scalar counter
   f32x4_t acc[4];
   float x[8];      // transcendental inputs (never written in the loop)
   float t[8];      // transcendental results (never read in the loop)
@@ -58,10 +60,29 @@ __device__ __forceinline__ void vector_share(Regs& r) {
   if (G % 3 != 2) cvt<G>(r);
 }
 
+// the rest of the fused scan's per-step stream (counters: 28.5 LDS and 39
+// scalar instructions per wave-step; about 45 hazard-nop slots in its
+// listing): in group G, an LDS read of 16 bytes per lane in 28 of the 48
+// groups, a scalar multiply in 39, and a one-slot s_nop in 45
+template <int G>
+__device__ __forceinline__ void rest_share(Regs& r, uint32_t lds_off) {
+  if constexpr ((G * 28) % 48 < 28) {
+    asm volatile("ds_read_b128 %0, %1" : "=v"(r.ld[G & 1]) : "v"(lds_off));
+  }
+  // s_mul_i32 leaves SCC alone; the clobber keeps the compiler from relying
+  // on it across the statement regardless
+  if constexpr ((G * 39) % 48 < 39) asm volatile("s_mul_i32 %0, %0, 3" : "+s"(r.sc) : : "scc");
+  if constexpr ((G * 45) % 48 < 45) asm volatile("s_nop 0");
+}
+
 template <int PATTERN, int G>
-__device__ __forceinline__ void groups(Regs& r) {
+__device__ __forceinline__ void groups(Regs& r, uint32_t lds_off = 0) {
   if constexpr (G < kGroups) {
-    if constexpr (PATTERN == 0) {
+    if constexpr (PATTERN == 4) {
+      mfma<G>(r);
+      vector_share<G>(r);
+      rest_share<G>(r, lds_off);
+    } else if constexpr (PATTERN == 0) {
       mfma<G>(r);
       vector_share<G>(r);
     } else if constexpr (PATTERN == 1) {
@@ -69,7 +90,7 @@ __device__ __forceinline__ void groups(Regs& r) {
     } else if constexpr (PATTERN == 2) {
       mfma<G>(r);
     }
-    groups<PATTERN, G + 1>(r);
+    groups<PATTERN, G + 1>(r, lds_off);
   }
 }
 template <int G>
@@ -82,7 +103,16 @@ __device__ __forceinline__ void mfmas_only(Regs& r) {
 
 template <int PATTERN>
 __global__ __launch_bounds__(256) void k_issue_probe(float* __restrict__ sink, int iters) {
+  __shared__ __attribute__((aligned(16))) unsigned char lds[256 * 16];
+  for (int i = threadIdx.x; i < 256 * 16; i += blockDim.x) lds[i] = static_cast<unsigned char>(i);
+  __syncthreads();
+  // each lane reads its own 16 bytes of its wave's 1 KB (in bounds: 4 waves x 1 KB)
+  const uint32_t lds_off =
+      static_cast<uint32_t>(reinterpret_cast<uintptr_t>((__attribute__((address_space(3))) void*)(lds))) +
+      16u * threadIdx.x;
   Regs r;
+  r.ld[0] = r.ld[1] = make_uint4(0, 0, 0, 0);
+  r.sc = 0u;
 #pragma unroll
   for (int i = 0; i < 4; ++i) r.acc[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -99,13 +129,14 @@ __global__ __launch_bounds__(256) void k_issue_probe(float* __restrict__ sink, i
       mfmas_only<0>(r);
       groups<1, 0>(r);
     } else {
-      groups<PATTERN, 0>(r);
+      groups<PATTERN, 0>(r, lds_off);
     }
   }
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
   // drain the matrix pipe before reading its registers (the asm above is
   // opaque to the compiler's hazard padding)
   asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7\n\ts_nop 7");
-  float s = static_cast<float>(r.pk & 0xffu);
+  float s = static_cast<float>((r.pk ^ r.ld[0].x ^ r.ld[1].y ^ r.sc) & 0xffu);
 #pragma unroll
   for (int i = 0; i < 8; ++i) s += r.a[i] + r.t[i];
 #pragma unroll
@@ -116,14 +147,16 @@ __global__ __launch_bounds__(256) void k_issue_probe(float* __restrict__ sink, i
 }  // namespace
 
 extern "C" int mol_probe_issue_mix(int pattern, int waves_per_simd, int iters, float* sink, void* stream) {
-  if (waves_per_simd < 1 || waves_per_simd > 8 || iters < 1 || pattern < 0 || pattern > 3 || !sink) return -1;
+  if (waves_per_simd < 1 || waves_per_simd > 8 || iters < 1 || pattern < 0 || pattern > 4 || !sink) return -1;
   const dim3 grid(256 * waves_per_simd), block(256);
   hipStream_t st = static_cast<hipStream_t>(stream);
   switch (pattern) {
     case 0: hipLaunchKernelGGL(k_issue_probe<0>, grid, block, 0, st, sink, iters); break;
     case 1: hipLaunchKernelGGL(k_issue_probe<1>, grid, block, 0, st, sink, iters); break;
     case 2: hipLaunchKernelGGL(k_issue_probe<2>, grid, block, 0, st, sink, iters); break;
-    default: hipLaunchKernelGGL(k_issue_probe<3>, grid, block, 0, st, sink, iters); break;
+    case 4: hipLaunchKernelGGL(k_issue_probe<4>, grid, block, 0, st, sink, iters); break;
+    case 3: hipLaunchKernelGGL(k_issue_probe<3>, grid, block, 0, st, sink, iters); break;
+    default: return -1;
   }
   return static_cast<int>(hipGetLastError());
 }

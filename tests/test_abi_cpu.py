@@ -40,6 +40,7 @@ def test_probe_library_exports_its_declared_function():
     f.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p]
     assert f(0, 0, 10, 256, None) == -1
     assert f(7, 1, 10, 256, None) == -1
+    assert f(5, 1, 10, 256, None) == -1
     assert f(0, 1, 0, 256, None) == -1
     assert f(0, 1, 10, None, None) == -1
 
