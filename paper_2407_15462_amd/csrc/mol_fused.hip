@@ -303,11 +303,16 @@ __global__ __launch_bounds__(64 * kWaves, EPI == kEpiMaxDot ? 2 : 1) void k_mol_
         mlp.phi2_stage_b(lg1, s1, den0, num0, Dn, Nm);
         {
           constexpr int kMfma = 0x008, kValu = 0x002 | 0x400, kDsRead = 0x100;
+          // the X reads, then 20 of stage B's vector instructions while they
+          // land, then one MFMA per two vector instructions (A/B at
+          // exact_1m: 0 / 8 / 16 / 20 / 24 leading instructions 38.4 / 38.2 /
+          // 38.0 / 37.7 / 38.2 ms)
           __builtin_amdgcn_sched_group_barrier(kDsRead, PX * S::KD, 0);
+          __builtin_amdgcn_sched_group_barrier(kValu, 20, 0);
 #pragma unroll
           for (int i = 0; i < PX * S::KD; ++i) {
             __builtin_amdgcn_sched_group_barrier(kMfma, 1, 0);
-            __builtin_amdgcn_sched_group_barrier(kValu, 3, 0);
+            __builtin_amdgcn_sched_group_barrier(kValu, 2, 0);
           }
         }
         // the next step's dot products are read after the branches below
