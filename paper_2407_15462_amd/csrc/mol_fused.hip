@@ -21,7 +21,11 @@
 //    RangeDotProduct + BruteForceTopKMoL in one pass);
 //  - kEpiMaxDot: a running top-k of m itself, without the gating MLP
 //    (Section 3's max approximation of MoL, a subsection cut from the
-//    published text).
+//    published text);
+//  - kEpiTopkPipe: kEpiTopk as a software-pipelined loop (each step's
+//    softmax tail issued with the next step's GEMM1); a step whose softmax
+//    sum leaves its safe range flags its workgroup's range, which a second
+//    launch of kEpiTopk rescores.
 //
 // Workgroup: 8 waves (2 per SIMD) = 16 queries sharing an LDS-staged
 // stream of 32-item tiles (a three-deep ring) loaded with direct
@@ -95,9 +99,8 @@ __global__ __launch_bounds__(64 * kWaves, EPI == kEpiMaxDot ? 2 : 1) void k_mol_
     long phi_stride, int* __restrict__ redo) {
   constexpr bool DENSE = EPI == kEpiDense;
   constexpr bool MLP = EPI != kEpiMaxDot;
-  // software-pipelined top-k scan (hand-interleaved chain, H <= 64)
+  // software-pipelined top-k scan
   constexpr bool PIPE = EPI == kEpiTopkPipe;
-  static_assert(!PIPE || H <= 64, "the pipelined scan uses the hand-interleaved chain");
   using S = FusedShape<PX, D, H, MLP>;
   using Mlp = MolMlp<PX, H>;
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
@@ -200,7 +203,7 @@ __global__ __launch_bounds__(64 * kWaves, EPI == kEpiMaxDot ? 2 : 1) void k_mol_
   else ring_barrier<0>();
 
   if constexpr (PIPE) {
-    // Software-pipelined top-k scan (H <= 64).  Each step's chain is split
+    // Software-pipelined top-k scan.  Each step's chain is split
     // in two: stage A (both queries' GEMM2 -> SiLU -> GEMM3 and query 0's
     // softmax sums) and stage B (query 1's softmax sums and the sums over an
     // item's four lanes).  Stage B of step s is issued in one scheduling
@@ -303,16 +306,19 @@ __global__ __launch_bounds__(64 * kWaves, EPI == kEpiMaxDot ? 2 : 1) void k_mol_
         mlp.phi2_stage_b(lg1, s1, den0, num0, Dn, Nm);
         {
           constexpr int kMfma = 0x008, kValu = 0x002 | 0x400, kDsRead = 0x100;
-          // the X reads, then 20 of stage B's vector instructions while they
-          // land, then one MFMA per two vector instructions (A/B at
-          // exact_1m: 0 / 8 / 16 / 20 / 24 leading instructions 38.4 / 38.2 /
-          // 38.0 / 37.7 / 38.2 ms)
+          // the X reads, then some of stage B's vector instructions while
+          // they land, then the MFMAs each followed by vector instructions
+          // (A/B: H = 64, exact_1m, 0 / 8 / 16 / 20 / 24 leading and two per
+          // MFMA: 38.4 / 38.2 / 38.0 / 37.7 / 38.2 ms; H = 128, hybrid_8m,
+          // whose stage B is shorter (P = 32): 20 and two per MFMA 86.9 ms,
+          // 16 and one 86.1, none 88.8 without pipelining)
+          constexpr int kLead = H > 64 ? 16 : 20, kPer = H > 64 ? 1 : 2;
           __builtin_amdgcn_sched_group_barrier(kDsRead, PX * S::KD, 0);
-          __builtin_amdgcn_sched_group_barrier(kValu, 20, 0);
+          __builtin_amdgcn_sched_group_barrier(kValu, kLead, 0);
 #pragma unroll
           for (int i = 0; i < PX * S::KD; ++i) {
             __builtin_amdgcn_sched_group_barrier(kMfma, 1, 0);
-            __builtin_amdgcn_sched_group_barrier(kValu, 2, 0);
+            __builtin_amdgcn_sched_group_barrier(kValu, kPer, 0);
           }
         }
         // the next step's dot products are read after the branches below
@@ -577,11 +583,9 @@ static hipError_t launch_fused_d(const DevProb& pr, int k, int R, int range_len,
   if (pr.Px == 8)
     return launch_fused_t<8, 64, 64, EPI>(pr, k, R, range_len, G, n_begin, n_end, bound, partial, phi,
                                           phi_stride, redo, st);
-  if constexpr (EPI != kEpiTopkPipe) {
-    if (pr.d == 128)
-      return launch_fused_t<4, 128, 128, EPI>(pr, k, R, range_len, G, n_begin, n_end, bound, partial, phi,
-                                              phi_stride, redo, st);
-  }
+  if (pr.d == 128)
+    return launch_fused_t<4, 128, 128, EPI>(pr, k, R, range_len, G, n_begin, n_end, bound, partial, phi,
+                                            phi_stride, redo, st);
   return launch_fused_t<4, 64, 64, EPI>(pr, k, R, range_len, G, n_begin, n_end, bound, partial, phi,
                                         phi_stride, redo, st);
 }
@@ -593,7 +597,7 @@ hipError_t launch_fused_topk(const DevProb& pr, int k, int R, int range_len, int
   if (bound)
     return launch_fused_d<kEpiBounded>(pr, k, R, range_len, G, 0, pr.N, bound, partial, nullptr, 0, nullptr,
                                        st);
-  if (redo && pr.H <= 64) {
+  if (redo) {
     // pipelined scan, then the plain scan over the ranges it flagged
     hipError_t e = launch_fused_d<kEpiTopkPipe>(pr, k, R, range_len, G, 0, pr.N, nullptr, partial, nullptr, 0,
                                                 redo, st);

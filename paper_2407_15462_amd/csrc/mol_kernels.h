@@ -104,8 +104,8 @@ bool fused_maxdot_supported(const DevProb& pr, int k);
 void fused_grid(const DevProb& pr, int n_count, int& R, int& range_len, int& G, bool maxdot);
 // bound: NULL, or [B] floats: only items with max_p s_p (plus the rounding
 // margin) at or above bound[b] are ranked for query b.  redo: NULL, or
-// fused_redo_flags(R, G) ints of workspace; with it (and no bound) shapes
-// with H <= 64 take the software-pipelined scan, whose workgroups flag a
+// fused_redo_flags(R, G) ints of workspace; with it (and no bound) the
+// software-pipelined scan runs, whose workgroups flag a
 // range where a softmax sum left its safe range, and a second launch
 // rescores only the flagged ranges.
 long fused_redo_flags(int R, int G);

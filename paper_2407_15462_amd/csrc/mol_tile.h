@@ -513,14 +513,25 @@ struct MolMlp {
   }
 
   // The two-query chain split for a software-pipelined scan (the same
-  // instructions on the same operands as phi2_interleaved, so the sums are
-  // bit-identical).  Stage A: both queries' GEMM2 -> SiLU -> GEMM3 and query
-  // 0's softmax sums, scheduled as in phi2_interleaved; query 1's base-2
+  // instructions on the same operands as phi2_interleaved and phi<2>, so the
+  // sums are bit-identical).  Stage A: both queries' GEMM2 -> SiLU -> GEMM3
+  // and query 0's softmax sums, scheduled as in phi2_interleaved for
+  // H <= 64 and as two priority-raised chains (logits) for larger H, where
+  // the matrix chains are long against the SiLU work; query 1's base-2
   // logits are handed to stage B, which the caller issues together with the
   // next step's GEMM1.
   template <int VA>
   __device__ void phi2_stage_a(const float (&s)[2][RUN], const f32x4_t (&c0)[2][PT], f32x4_t (&lg1)[PT],
                                float& den0, float& num0) const {
+    if constexpr (H > 64) {
+      f32x4_t lg0[PT];
+      logits(s[0], c0[0], lg0);
+      logits(s[1], c0[1], lg1);
+      weights(lg0, s[0], 0.f, den0, num0);
+      // query 1's logits are read after the caller's next branch
+      mfma_drain();
+      return;
+    }
     uint4 sop[2][KP];
     f32x4_t u[2][JT];
     uint4 hop[2][KH];
