@@ -323,6 +323,10 @@ __global__ __launch_bounds__(64 * kWaves, EPI == kEpiMaxDot ? 2 : 1) void k_mol_
         }
         // the next step's dot products are read after the branches below
         mfma_drain();
+        // the next step's a_x reads go out before the offers, which then
+        // cover their LDS latency
+        float4 axv[S::PT];
+        ax_reads(tn, stn, axv);
         // finish this step.  A sum outside [2^-60, 2^60] (logits far from
         // zero) marks the wave: its workgroup's range is then scored again by
         // the non-pipelined scan, which subtracts the row maximum (this
@@ -338,8 +342,6 @@ __global__ __launch_bounds__(64 * kWaves, EPI == kEpiMaxDot ? 2 : 1) void k_mol_
             top[1].offer(m1 ? make_key(v, item) : 0ull, lane);
           }
         }
-        float4 axv[S::PT];
-        ax_reads(tn, stn, axv);
         if (has_next) {
           f32x4_t c0[2][S::PT];
           gate_bias2(axv, c0);
