@@ -520,7 +520,7 @@ struct MolMlp {
   // the matrix chains are long against the SiLU work; query 1's base-2
   // logits are handed to stage B, which the caller issues together with the
   // next step's GEMM1.
-  template <int VA>
+  template <int VA, int NDS = 0>
   __device__ void phi2_stage_a(const float (&s)[2][RUN], const f32x4_t (&c0)[2][PT], f32x4_t (&lg1)[PT],
                                float& den0, float& num0) const {
     if constexpr (H > 64) {
@@ -546,7 +546,10 @@ struct MolMlp {
     gemm3(hop[0], c0[0], lg0);
     gemm3(hop[1], c0[1], lg1);
     weights(lg0, s[0], 0.f, den0, num0);
-    constexpr int kMfma = 0x008, kValu = 0x002 | 0x400;
+    constexpr int kMfma = 0x008, kValu = 0x002 | 0x400, kDsRead = 0x100;
+    // the caller's NDS LDS reads (the GEMM3 accumulator inputs) go first, so
+    // that GEMM2 and the SiLU cover their latency
+    if constexpr (NDS > 0) __builtin_amdgcn_sched_group_barrier(kDsRead, NDS, 0);
     __builtin_amdgcn_sched_group_barrier(kMfma, JT * KP, 0);
 #pragma unroll
     for (int i = 0; i < JT * KP + 2 * PT * KH; ++i) {
