@@ -162,7 +162,7 @@ def copy_calibration():
 
 def issue_probe(iters=2000):
     """Time the probe kernel of include/mol_probe.h: the fused scan's
-    per-step instruction mix (48 MFMA, 97 transcendental, 221 plain vector
+    per-step instruction mix (48 MFMA, 97 transcendental, 206 plain vector
     instructions, 32 pack conversions per wave-step) issued with no
     dependencies, no memory traffic and no barriers, at 1-4 waves per SIMD.
     Prints ns per wave-step per SIMD and the floor it implies for the fused
@@ -201,7 +201,7 @@ def issue_probe(iters=2000):
         out[f"exact_1m_full_stream_floor_ms_w{w}"] = full
         out[f"exact_1m_full_stream_frac_max_w{w}"] = flops / (full / 1e3) / 1e12 / PEAK_BF16_TFLOPS
     print(json.dumps({"issue_probe": out, "iters": iters,
-                      "mix_per_wave_step": {"mfma_16x16x32": 48, "transcendental": 97, "plain_valu": 221,
+                      "mix_per_wave_step": {"mfma_16x16x32": 48, "transcendental": 97, "plain_valu": 206,
                                             "cvt_pk_f16_f32": 32},
                       "wave_steps_per_simd_exact_1m": steps_per_simd}), flush=True)
 

@@ -7,7 +7,7 @@
  * H = 64: 2 queries x 16 items per wave) issues 48 matrix instructions
  * (v_mfma_f32_16x16x32 bf16/f16), 97 transcendental vector instructions
  * (the SiLU's exp2 and reciprocal, the softmax's exp2, the reciprocal of
- * phi) and 253 other vector ALU instructions, 32 of them f32 -> f16 pack
+ * phi) and 238 other vector ALU instructions, 32 of them f32 -> f16 pack
  * conversions (the counts of the SQ_INSTS_* hardware counters per
  * wave-step).  The probe
  * kernel issues exactly that mix per iteration with no data dependencies
@@ -20,7 +20,8 @@
  *   pattern 3: the mix in two phases per iteration (48 MFMAs, then the rest)
  *   pattern 4: pattern 0 plus the rest of the kernel's per-step stream: 28
  *              LDS reads of 16 bytes per lane, 39 scalar ALU instructions and
- *              45 one-slot hazard nops (still no dependencies)
+ *              the listing's hazard nops: two 11-slot MFMA drains and 25
+ *              three-slot nops (still no dependencies)
  *
  * The launch holds waves_per_simd waves on each of the 1024 SIMDs
  * (256 x waves_per_simd workgroups of 4 waves); each wave runs `iters`

@@ -346,9 +346,11 @@ __global__ __launch_bounds__(64 * kWaves, EPI == kEpiMaxDot ? 2 : 1) void k_mol_
           f32x4_t c0[2][S::PT];
           gate_bias2(axv, c0);   // 2 PT LDS reads of a_q + b2
           mlp.template phi2_stage_a<5, 2 * S::PT>(s2n, c0, lg1, den0, num0);
-#pragma unroll
-          for (int mu = 0; mu < S::RUN; ++mu) s1[mu] = s2n[1][mu];
         }
+        // unconditional (past the last step s1 is dead): a copy under
+        // has_next cost 32 register moves per two steps
+#pragma unroll
+        for (int mu = 0; mu < S::RUN; ++mu) s1[mu] = s2n[1][mu];
       }
     }
     if (lane == 0) redo[blockIdx.x * kWaves + wave] = redo_wave ? 1 : 0;

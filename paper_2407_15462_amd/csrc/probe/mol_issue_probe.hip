@@ -44,8 +44,8 @@ __device__ __forceinline__ void cvt(Regs& r) {
 }
 
 // the vector share of group G: 2 transcendental (3 in group 0), 4 plain
-// (5 in 29 of the 48 groups) and a conversion in two groups of three:
-// 97 / 221 / 32 per step, the fused scan's counts (SQ_INSTS_VALU_TRANS_F32
+// (5 in 14 of the 48 groups) and a conversion in two groups of three:
+// 97 / 206 / 32 per step, the fused scan's counts (SQ_INSTS_VALU_TRANS_F32
 // and SQ_INSTS_VALU less the MFMAs, per wave-step of k_mol_fused)
 template <int G>
 __device__ __forceinline__ void vector_share(Regs& r) {
@@ -55,15 +55,16 @@ __device__ __forceinline__ void vector_share(Regs& r) {
   trans<2 * G + 1>(r);
   plain<5 * G + 2>(r);
   plain<5 * G + 3>(r);
-  if ((G * 29) % 48 < 29) plain<5 * G + 4>(r);
+  if ((G * 14) % 48 < 14) plain<5 * G + 4>(r);
   if (G == 0) trans<101>(r);
   if (G % 3 != 2) cvt<G>(r);
 }
 
 // the rest of the fused scan's per-step stream (counters: 28.5 LDS and 39
-// scalar instructions per wave-step; about 45 hazard-nop slots in its
-// listing): in group G, an LDS read of 16 bytes per lane in 28 of the 48
-// groups, a scalar multiply in 39, and a one-slot s_nop in 45
+// scalar instructions per wave-step; its listing's nops: two 11-slot MFMA
+// drains and about 25 more nops of 2.8 slots on average per step): in group
+// G, an LDS read of 16 bytes per lane in 28 of the 48 groups, a scalar
+// multiply in 39, a three-slot s_nop in 25 and an 11-slot drain in two
 template <int G>
 __device__ __forceinline__ void rest_share(Regs& r, uint32_t lds_off) {
   if constexpr ((G * 28) % 48 < 28) {
@@ -72,7 +73,8 @@ __device__ __forceinline__ void rest_share(Regs& r, uint32_t lds_off) {
   // s_mul_i32 leaves SCC alone; the clobber keeps the compiler from relying
   // on it across the statement regardless
   if constexpr ((G * 39) % 48 < 39) asm volatile("s_mul_i32 %0, %0, 3" : "+s"(r.sc) : : "scc");
-  if constexpr ((G * 45) % 48 < 45) asm volatile("s_nop 0");
+  if constexpr ((G * 25) % 48 < 25) asm volatile("s_nop 2");
+  if constexpr (G == 0 || G == 24) asm volatile("s_nop 7\n\ts_nop 2");
 }
 
 template <int PATTERN, int G>
