@@ -280,30 +280,39 @@ __global__ void k_copy_rows(const uint64_t* __restrict__ src, long src_stride, i
 // ---------------------------------------------------------------------------
 // Candidate union + dedup (the deduplicated set G of Algorithm 2): one block
 // per query inserts its C candidate ids into an LDS open-addressing hash set
-// (linear probing, capacity a power of two >= 1.5 C) and appends each id the
-// first time it is seen.  Ids outside [0, N) are empty slots.
+// (linear probing, capacity a power of two >= 1.5 C) and counts each new id
+// in one of kDedupBins bins of consecutive ids (id >> bin_shift); the ids are
+// then written bin by bin (a counting sort: ascending bins, arbitrary order
+// inside a bin), so that the rerank walks every query's candidates from the
+// front of the corpus to its end and concurrent waves gather nearby items.
+// Ids outside [0, N) are empty slots.
 // ---------------------------------------------------------------------------
+constexpr int kDedupBins = 1024;
 __global__ __launch_bounds__(1024) void k_dedup(const int32_t* __restrict__ cand, int C,
                                                 const int32_t* __restrict__ cand2, int C2, int N,
-                                                int cap_log2, int32_t* __restrict__ uniq,
+                                                int cap_log2, int bin_shift, int32_t* __restrict__ uniq,
                                                 int32_t* __restrict__ n_unique) {
-  extern __shared__ int32_t table[];
+  extern __shared__ int32_t table[];     // cap slots, then kDedupBins bin counters
   __shared__ int count;
+  __shared__ int wsum[1024 / 64];
   const int cap = 1 << cap_log2;
+  int32_t* bins = table + cap;
   const long b = blockIdx.x;
-  for (int i = threadIdx.x; i < cap; i += blockDim.x) table[i] = -1;
-  if (threadIdx.x == 0) count = 0;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  for (int i = tid; i < cap; i += blockDim.x) table[i] = -1;
+  for (int i = tid; i < kDedupBins; i += blockDim.x) bins[i] = 0;
+  if (tid == 0) count = 0;
   __syncthreads();
   const int CT = C + C2;                 // both sets; uniq rows hold CT slots
-  for (int i = threadIdx.x; i < CT; i += blockDim.x) {
+  for (int i = tid; i < CT; i += blockDim.x) {
     const int32_t id = i < C ? cand[b * C + i] : cand2[b * C2 + (i - C)];
     if (id < 0 || id >= N) continue;
     uint32_t h = (static_cast<uint32_t>(id) * 0x9E3779B1u) >> (32 - cap_log2);
     for (int probe = 0; probe < cap; ++probe) {
       const int32_t prev = atomicCAS(&table[h], -1, id);
       if (prev == -1) {
-        const int pos = atomicAdd(&count, 1);
-        uniq[b * CT + pos] = id;
+        atomicAdd(&count, 1);
+        atomicAdd(&bins[id >> bin_shift], 1);
         break;
       }
       if (prev == id) break;
@@ -311,7 +320,25 @@ __global__ __launch_bounds__(1024) void k_dedup(const int32_t* __restrict__ cand
     }
   }
   __syncthreads();
-  if (threadIdx.x == 0) n_unique[b] = count;
+  // exclusive prefix sum of the bin counts (blockDim.x == kDedupBins)
+  const int v = bins[tid];
+  int incl = v;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int t = __shfl_up(incl, o);
+    if (lane >= o) incl += t;
+  }
+  if (lane == 63) wsum[wave] = incl;
+  __syncthreads();
+  int before = 0;
+  for (int w = 0; w < wave; ++w) before += wsum[w];
+  bins[tid] = before + incl - v;
+  __syncthreads();
+  for (int s = tid; s < cap; s += blockDim.x) {
+    const int32_t id = table[s];
+    if (id >= 0) uniq[b * CT + atomicAdd(&bins[id >> bin_shift], 1)] = id;
+  }
+  if (tid == 0) n_unique[b] = count;
 }
 
 // ---------------------------------------------------------------------------
@@ -590,14 +617,17 @@ int dedup_cap_log2(int C) {
 hipError_t launch_dedup(const int32_t* cand, int C, const int32_t* cand2, int C2, int B, int N,
                         int32_t* uniq, int32_t* n_unique, hipStream_t st) {
   const int lg = dedup_cap_log2(C + C2);
-  const size_t smem = sizeof(int32_t) << lg;
+  const size_t smem = (sizeof(int32_t) << lg) + sizeof(int32_t) * kDedupBins;
+  int bin_shift = 0;                     // (N - 1) >> bin_shift < kDedupBins
+  while (((static_cast<long>(N) - 1) >> bin_shift) >= kDedupBins) ++bin_shift;
   if (smem > 65536) {
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_dedup),
                                        hipFuncAttributeMaxDynamicSharedMemorySize,
                                        static_cast<int>(smem));
     if (e != hipSuccess) return e;
   }
-  hipLaunchKernelGGL(k_dedup, dim3(B), dim3(1024), smem, st, cand, C, cand2, C2, N, lg, uniq, n_unique);
+  hipLaunchKernelGGL(k_dedup, dim3(B), dim3(kDedupBins), smem, st, cand, C, cand2, C2, N, lg, bin_shift, uniq,
+                     n_unique);
   return hipGetLastError();
 }
 
