@@ -192,7 +192,11 @@ __global__ __launch_bounds__(64 * waves_for(KL), 1) void k_topk_per_embd(
 #pragma unroll
   for (int nb = 0; nb < S::NB; ++nb) {
     if constexpr (PRUNED) {
-      const int slot = chunk * S::VEC_WG + wave * S::VEC_WAVE + 32 * nb + col;
+      // slots interleaved over the waves: a chunk's hot vectors (about 80 %
+      // of its slots) then load every wave alike, and the waves, which meet
+      // at every stage's barrier, wait less for the one with the most hits
+      // (exact_1m: 9.15 -> 8.89 ms for the call; hybrid_8m: 16.67 -> 16.79)
+      const int slot = chunk * S::VEC_WG + (32 * nb + col) * S::WAVES + wave;
       vv[nb] = slot < pa.hot_n[grp] ? pa.hot_v[static_cast<long>(grp) * nvec + slot] : -1;
     } else {
       const int v = vwave + 32 * nb + col;
