@@ -451,16 +451,19 @@ def test_rerank_matches_oracle(C, k):
         assert np.all(i[b, kk:] == -1) and np.all(np.isneginf(s[b, kk:]))
 
 
-@pytest.mark.parametrize("C,C2", [(700, 0), (4096, 0), (1000, 300)])
-def test_dedup_union_is_exact_set(C, C2):
+@pytest.mark.parametrize("C,C2,N", [(700, 0, 3000), (4096, 0, 3000), (1000, 300, 3000),
+                                     (900, 0, 700), (1500, 200, 1025)])
+def test_dedup_union_is_exact_set(C, C2, N):
     """Algorithm 2's deduplicated set G, checked as a set: mol_rerank with
     k = C + C2 returns every distinct candidate of a query (the rest padded),
     so the id set must equal the union computed by the oracle, integer for
     integer -- a dedup that dropped one id and kept another twice, or emitted
-    a wrong id, fails here even where counts and the top-k agree."""
-    spec = W["exact_1m"].scaled(B=7, N=3000, clusters=32)
+    a wrong id, fails here even where counts and the top-k agree.  The dedup
+    writes ids bin by bin (1024 bins of consecutive ids): N = 700 puts one id
+    in a bin, N = 1025 two per bin but one in the last."""
+    spec = W["exact_1m"].scaled(B=7, N=N, clusters=32)
     k = C + C2
-    log(f"[dedup set] C={C} C2={C2} k={k}")
+    log(f"[dedup set] C={C} C2={C2} N={N} k={k}")
     inp = cuda_inputs(spec, seed=27)
     prob = mol.Problem.from_inputs(inp)
     g = torch.Generator(device="cuda").manual_seed(9)
