@@ -2,9 +2,11 @@
 // (Algorithm 2, BruteForceTopKMoL over the candidate set G).
 //
 // Each wave takes one query and one chunk of its distinct candidate ids and
-// walks it 16 items at a time: the items' component embeddings and gating
-// logits are gathered straight from the component-major corpus into MFMA
-// operand registers (one 16-byte load per lane per component and K block),
+// walks it 16 items at a time: the items' component embeddings are gathered
+// from the component-major corpus one step ahead, by direct global -> LDS
+// copies (one 16-byte copy per lane per component and K block) into a
+// buffer of the wave (Px d / 32 KB), and read back as MFMA operands at the start of their
+// step (their gating logits a_x are prefetched into registers);
 // GEMM1 forms the 8 x 16 dot products of the query's components with the
 // items' components in rows 2 pq of the 16x16x32 tile (the odd rows are
 // zero), which leaves them in the run layout of mol_tile.h, and the shared
@@ -28,6 +30,9 @@ __global__ __launch_bounds__(64 * kWaves, 2) void k_mol_rerank(
   using Mlp = MolMlp<PX, H>;
   constexpr int P = 8 * PX, RUN = 2 * PX, KD = D / 32, PT = P / 16;
   __shared__ uint64_t sTop[kWaves * kTopkRegion];
+  // the wave's gather buffer: block (px, kk) of 1 KB holds lane i's 16 bytes
+  // of component px, K block kk at byte 16 i (a direct global -> LDS copy)
+  extern __shared__ __attribute__((aligned(16))) unsigned char sGather[];
 
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int c = lane & 15, g = lane >> 4;
@@ -63,23 +68,51 @@ __global__ __launch_bounds__(64 * kWaves, 2) void k_mol_rerank(
                   ? *reinterpret_cast<const uint4*>(Q + (static_cast<long>(b) * 8 + (c >> 1)) * D + 32 * kk + 8 * g)
                   : make_uint4(0, 0, 0, 0);
 
+  // Each step's 16 items are gathered one step ahead: the component
+  // operands by direct global -> LDS copies into the wave's buffer (read
+  // back into registers at the start of the step, after which the next
+  // step's copies are issued into it), the item logits a_x into registers.
+  unsigned char* gbuf = sGather + __builtin_amdgcn_readfirstlane(wave) * (PX * KD * 1024);
+  auto item_at = [&](int pos) { return pos < i1 ? min(max(ids[pos], 0), N - 1) : 0; };   // ids are in range
+  float4 axn[PT];
+  auto gather = [&](int it) {
+#pragma unroll
+    for (int px = 0; px < PX; ++px)
+#pragma unroll
+      for (int kk = 0; kk < KD; ++kk)
+        copy16_to_lds(X + (static_cast<long>(px) * N + it) * D + 32 * kk + 8 * g,
+                      lds_addr(gbuf + (px * KD + kk) * 1024));
+#pragma unroll
+    for (int pt = 0; pt < PT; ++pt)
+      axn[pt] = *reinterpret_cast<const float4*>(pr.a_x + static_cast<long>(it) * P + base + 4 * pt);
+  };
+  int item_n = item_at(i0 + c);
+  if (i0 < i1) gather(item_n);
+  int item_nn = item_at(i0 + 16 + c);
   for (int s0 = i0; s0 < i1; s0 += 16) {
     const int pos = s0 + c;
     const bool ok = pos < i1;
-    int item = ok ? ids[pos] : 0;
-    item = min(max(item, 0), N - 1);       // ids come from the dedup pass: in range
-    // gather the 16 items' components as GEMM1 B operands
+    const int item = item_n;
+    // this step's copies have landed (only the younger id load may be
+    // outstanding); read the operands, then refill the buffer
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_waitcnt(waitcnt_vm(1));
+    asm volatile("" ::: "memory");
     uint4 xop[PX][KD];
 #pragma unroll
     for (int px = 0; px < PX; ++px)
 #pragma unroll
       for (int kk = 0; kk < KD; ++kk)
-        xop[px][kk] = *reinterpret_cast<const uint4*>(X + (static_cast<long>(px) * N + item) * D + 32 * kk + 8 * g);
+        xop[px][kk] = *reinterpret_cast<const uint4*>(gbuf + (px * KD + kk) * 1024 + 16 * lane);
     f32x4_t c0[1][PT];
 #pragma unroll
-    for (int pt = 0; pt < PT; ++pt) {
-      const float4 a = *reinterpret_cast<const float4*>(pr.a_x + static_cast<long>(item) * P + base + 4 * pt);
-      c0[0][pt] = f32x4_t{kLog2e * a.x, kLog2e * a.y, kLog2e * a.z, kLog2e * a.w} + cbf[pt];
+    for (int pt = 0; pt < PT; ++pt)
+      c0[0][pt] = f32x4_t{kLog2e * axn[pt].x, kLog2e * axn[pt].y, kLog2e * axn[pt].z, kLog2e * axn[pt].w} + cbf[pt];
+    wave_lds_sync();
+    if (s0 + 16 < i1) {
+      item_n = item_nn;
+      gather(item_n);
+      item_nn = item_at(s0 + 32 + c);
     }
     f32x4_t acc1[PX];
 #pragma unroll
@@ -119,21 +152,28 @@ int rerank_chunk(int B, int C) {
   return 256;
 }
 
+template <int PX, int D, int H, bool NEG>
+static hipError_t launch_rerank_one(const DevProb& pr, dim3 grid, const int32_t* uniq, const int32_t* n_unique,
+                                    int C, int k, int chunk, int nchunks, uint64_t* partial, hipStream_t st) {
+  constexpr int kGather = kWaves * PX * (D / 32) * 1024;   // the waves' gather buffers
+  auto kern = &k_mol_rerank<PX, D, H, NEG>;
+  const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                           hipFuncAttributeMaxDynamicSharedMemorySize, kGather);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(kern, grid, dim3(64 * kWaves), kGather, st, pr, uniq, n_unique, C, k, chunk, nchunks, partial);
+  return hipGetLastError();
+}
+
 template <bool NEG>
-static void launch_rerank_t(const DevProb& pr, dim3 grid, const int32_t* uniq, const int32_t* n_unique,
-                            int C, int k, int chunk, int nchunks, uint64_t* partial, hipStream_t st) {
+static hipError_t launch_rerank_t(const DevProb& pr, dim3 grid, const int32_t* uniq, const int32_t* n_unique,
+                                  int C, int k, int chunk, int nchunks, uint64_t* partial, hipStream_t st) {
   if (pr.Px == 8 && pr.d == 32)
-    hipLaunchKernelGGL((k_mol_rerank<8, 32, 64, NEG>), grid, dim3(64 * kWaves), 0, st, pr, uniq, n_unique, C,
-                       k, chunk, nchunks, partial);
-  else if (pr.Px == 8)
-    hipLaunchKernelGGL((k_mol_rerank<8, 64, 64, NEG>), grid, dim3(64 * kWaves), 0, st, pr, uniq, n_unique, C,
-                       k, chunk, nchunks, partial);
-  else if (pr.d == 128)
-    hipLaunchKernelGGL((k_mol_rerank<4, 128, 128, NEG>), grid, dim3(64 * kWaves), 0, st, pr, uniq, n_unique,
-                       C, k, chunk, nchunks, partial);
-  else
-    hipLaunchKernelGGL((k_mol_rerank<4, 64, 64, NEG>), grid, dim3(64 * kWaves), 0, st, pr, uniq, n_unique, C,
-                       k, chunk, nchunks, partial);
+    return launch_rerank_one<8, 32, 64, NEG>(pr, grid, uniq, n_unique, C, k, chunk, nchunks, partial, st);
+  if (pr.Px == 8)
+    return launch_rerank_one<8, 64, 64, NEG>(pr, grid, uniq, n_unique, C, k, chunk, nchunks, partial, st);
+  if (pr.d == 128)
+    return launch_rerank_one<4, 128, 128, NEG>(pr, grid, uniq, n_unique, C, k, chunk, nchunks, partial, st);
+  return launch_rerank_one<4, 64, 64, NEG>(pr, grid, uniq, n_unique, C, k, chunk, nchunks, partial, st);
 }
 
 hipError_t launch_rerank(const DevProb& pr, const int32_t* uniq, const int32_t* n_unique, int C, int k,
@@ -142,11 +182,8 @@ hipError_t launch_rerank(const DevProb& pr, const int32_t* uniq, const int32_t* 
   const int nchunks = (C + chunk - 1) / chunk;
   const long waves = static_cast<long>(pr.B) * nchunks;
   const dim3 grid(static_cast<unsigned>((waves + kWaves - 1) / kWaves));
-  if (negate)
-    launch_rerank_t<true>(pr, grid, uniq, n_unique, C, k, chunk, nchunks, partial, st);
-  else
-    launch_rerank_t<false>(pr, grid, uniq, n_unique, C, k, chunk, nchunks, partial, st);
-  return hipGetLastError();
+  return negate ? launch_rerank_t<true>(pr, grid, uniq, n_unique, C, k, chunk, nchunks, partial, st)
+                : launch_rerank_t<false>(pr, grid, uniq, n_unique, C, k, chunk, nchunks, partial, st);
 }
 
 }  // namespace mol
