@@ -43,10 +43,15 @@ namespace {
 enum FusedEpi { kEpiTopk = 0, kEpiDense = 1, kEpiBounded = 2, kEpiMaxDot = 3, kEpiTopkPipe = 4 };
 
 constexpr int kWaves = 8;
-constexpr int kQueriesPerWG = 2 * kWaves;
+constexpr int kQueriesPerWG = 2 * kWaves;   // the gating forms
+// queries per wave: two in the gating forms; four in the max-dot form, whose
+// step is GEMM1 alone: each LDS read of the X tile then feeds two GEMM1s (the
+// 64 KB of top-k lists leave one workgroup per CU; at exact_1m 9.5 ms against
+// 9.8 ms for two queries per wave and two workgroups per CU)
+template <bool AX>
+constexpr int queries_per_wave() { return AX ? 2 : 4; }
 // items per LDS stage: two 16-item steps with the gating MLP; one step in
-// the max-dot form, whose smaller ring (with no a_x stream) lets two
-// workgroups share a CU
+// the max-dot form (no a_x stream)
 template <bool AX>
 constexpr int tile_items() { return AX ? 32 : 16; }
 constexpr int kRing = 3;         // item stages in flight
@@ -67,7 +72,9 @@ struct FusedShape {
   static constexpr int LDS_X = kRing * XSTAGE;
   static constexpr int LDS_AX = kRing * ASTAGE;
   static constexpr int LDS_CB = AX ? kQueriesPerWG * P * 4 : 0;   // [query][p] log2(e) (a_q + b2), f32
-  static constexpr int LDS_TOPK = kQueriesPerWG * kTopkRegion * 8;
+  static constexpr int QPW = queries_per_wave<AX>();   // queries per wave
+  static constexpr int QWG = QPW * kWaves;             // queries per workgroup
+  static constexpr int LDS_TOPK = QWG * kTopkRegion * 8;
   static constexpr int LDS_TOTAL = LDS_X + LDS_AX + LDS_CB + LDS_TOPK;
   // 16-byte global->LDS copies per stage, in 1 KB blocks of one wave each
   static constexpr int XBLOCKS = XSTAGE / 1024;
@@ -93,7 +100,7 @@ __device__ __forceinline__ void wg_coords(int g, int R, int G, int& r, int& qg) 
 }  // namespace
 
 template <int PX, int D, int H, int EPI>
-__global__ __launch_bounds__(64 * kWaves, EPI == kEpiMaxDot ? 2 : 1) void k_mol_fused(
+__global__ __launch_bounds__(64 * kWaves, 1) void k_mol_fused(
     DevProb pr, int k, int R, int range_len, int G, int n_begin, int n_end,
     const float* __restrict__ bound, uint64_t* __restrict__ partial, float* __restrict__ phi_out,
     long phi_stride, int* __restrict__ redo) {
@@ -123,8 +130,8 @@ __global__ __launch_bounds__(64 * kWaves, EPI == kEpiMaxDot ? 2 : 1) void k_mol_
   }
   int r, qg;
   wg_coords(blockIdx.x, R, G, r, qg);
-  const int qwg = qg * kQueriesPerWG;     // first query of the workgroup
-  const int qwv = qwg + 2 * wave;         // first of this wave's 2 queries
+  const int qwg = qg * S::QWG;            // first query of the workgroup
+  const int qwv = qwg + S::QPW * wave;    // first of this wave's QPW queries
   const int nr0 = n_begin + r * range_len;
   const int nr1 = min(n_end, nr0 + range_len);
   const int ntiles = nr1 > nr0 ? (nr1 - nr0 + S::TILE - 1) / S::TILE : 0;
@@ -174,10 +181,10 @@ __global__ __launch_bounds__(64 * kWaves, EPI == kEpiMaxDot ? 2 : 1) void k_mol_
       const int qi = i / P, p = i % P, b = qwg + qi;
       sCb[i] = b < pr.B ? kLog2e * (pr.a_q[static_cast<long>(b) * P + p] + pr.b2[p]) : 0.f;
     }
-  WaveTopk top[2];
+  WaveTopk top[S::QPW];
   if (!DENSE) {
-    top[0].init(sTop + (2 * wave + 0) * kTopkRegion, k, lane);
-    top[1].init(sTop + (2 * wave + 1) * kTopkRegion, k, lane);
+#pragma unroll
+    for (int qb = 0; qb < S::QPW; ++qb) top[qb].init(sTop + (S::QPW * wave + qb) * kTopkRegion, k, lane);
   }
   // per-query bound of the bounded epilogue (queries past B: +inf, skipped)
   float qbound[2];
@@ -187,15 +194,17 @@ __global__ __launch_bounds__(64 * kWaves, EPI == kEpiMaxDot ? 2 : 1) void k_mol_
   Mlp mlp;
   if (MLP) mlp.load(pr, c, g);
   // Q as GEMM1 A operands: row c = 2 pq + q (gating forms) or 8 q + pq
-  // (max-dot form), K slot 8g+e <-> d = 32 kk + 8 g + e
-  uint4 qop[S::KD];
-  {
-    const int b = MLP ? qwv + (c & 1) : qwv + (c >> 3), pq = MLP ? c >> 1 : c & 7;
+  // (max-dot form, queries 2 h and 2 h + 1 in set h), K slot 8g+e <-> d =
+  // 32 kk + 8 g + e
+  uint4 qop[S::QPW / 2][S::KD];
+#pragma unroll
+  for (int h = 0; h < S::QPW / 2; ++h) {
+    const int b = MLP ? qwv + (c & 1) : qwv + 2 * h + (c >> 3), pq = MLP ? c >> 1 : c & 7;
 #pragma unroll
     for (int kk = 0; kk < S::KD; ++kk)
-      qop[kk] = b < pr.B
-                    ? *reinterpret_cast<const uint4*>(Q + (static_cast<long>(b) * 8 + pq) * D + 32 * kk + 8 * g)
-                    : make_uint4(0, 0, 0, 0);
+      qop[h][kk] = b < pr.B
+                       ? *reinterpret_cast<const uint4*>(Q + (static_cast<long>(b) * 8 + pq) * D + 32 * kk + 8 * g)
+                       : make_uint4(0, 0, 0, 0);
   }
 
   // stage 0 complete; later stages' copies may still be in flight
@@ -246,7 +255,7 @@ __global__ __launch_bounds__(64 * kWaves, EPI == kEpiMaxDot ? 2 : 1) void k_mol_
       for (int px = 0; px < PX; ++px) {
         acc1[px] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int kk = 0; kk < S::KD; ++kk) acc1[px] = mfma_bf16(qop[kk], xb[px][kk], acc1[px]);
+        for (int kk = 0; kk < S::KD; ++kk) acc1[px] = mfma_bf16(qop[0][kk], xb[px][kk], acc1[px]);
       }
 #pragma unroll
       for (int mu = 0; mu < S::RUN; ++mu) {
@@ -388,32 +397,40 @@ __global__ __launch_bounds__(64 * kWaves, EPI == kEpiMaxDot ? 2 : 1) void k_mol_
       }
       __builtin_amdgcn_sched_barrier(0);
 
-      // GEMM1: both queries x 16 items x all px
+      // GEMM1: the wave's queries (set h: two of them) x 16 items x all px
       __builtin_amdgcn_s_setprio(1);
-      f32x4_t acc1[PX];
+      f32x4_t acc1[PX], acc2[PX];
 #pragma unroll
       for (int px = 0; px < PX; ++px) {
         acc1[px] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+        acc2[px] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int kk = 0; kk < S::KD; ++kk) acc1[px] = mfma_bf16(qop[kk], xb[px][kk], acc1[px]);
+        for (int kk = 0; kk < S::KD; ++kk) {
+          acc1[px] = mfma_bf16(qop[0][kk], xb[px][kk], acc1[px]);
+          if constexpr (S::QPW == 4) acc2[px] = mfma_bf16(qop[S::QPW / 2 - 1][kk], xb[px][kk], acc2[px]);
+        }
       }
       mfma_priority_end();
       // the two queries' runs: s2[q][mu] holds p = base(g) + mu
       float s2[2][S::RUN];
-      float mrow = 0.f;
+      float mrow[2] = {0.f, 0.f};
       if constexpr (EPI == kEpiMaxDot) {
-        // no split: lane group g holds query g / 2's rows pq = 4 (g % 2) ..
-        // + 3 for every px, so the maximum over its 4 PX values and the
+        // no split: lane group g holds query 2 h + g / 2's rows pq = 4 (g % 2)
+        // .. + 3 for every px, so the maximum over its 4 PX values and the
         // other group of the query (one permlane16 swap) is m, valid in the
         // lanes of rows 2 q and 2 q + 1 as the offers expect
-        float mx = acc1[0][0];
 #pragma unroll
-        for (int px = 0; px < PX; ++px)
+        for (int h = 0; h < S::QPW / 2; ++h) {
+          const f32x4_t(&acc)[PX] = h == 0 ? acc1 : acc2;
+          float mx = acc[0][0];
 #pragma unroll
-          for (int e = 0; e < 4; ++e) mx = fmaxf(mx, acc1[px][e]);
-        const uint32_t u = __float_as_uint(mx);
-        auto sw = __builtin_amdgcn_permlane16_swap(u, u, false, false);
-        mrow = fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1]));
+          for (int px = 0; px < PX; ++px)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) mx = fmaxf(mx, acc[px][e]);
+          const uint32_t u = __float_as_uint(mx);
+          auto sw = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+          mrow[h] = fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1]));
+        }
       } else {
         // accumulator row 4 g + i is pq = 2 g + i / 2 of query i % 2, i.e.
         // p = base(g) + (i / 2) PX + px
@@ -423,9 +440,11 @@ __global__ __launch_bounds__(64 * kWaves, EPI == kEpiMaxDot ? 2 : 1) void k_mol_
           s2[1][mu] = acc1[mu % PX][2 * (mu / PX) + 1];
         }
       }
-      float phi[2];
-      bool offer[2] = {item_ok, item_ok};
+      float phi[S::QPW];
+      bool offer[S::QPW];
       bool need[2] = {true, true};   // bounded form: the query's chain runs
+#pragma unroll
+      for (int qb = 0; qb < S::QPW; ++qb) offer[qb] = item_ok;
       // GEMM3 accumulator input of query qb: log2(e) a_x (the item's, from
       // the stage) + log2(e) (a_q + b2) (the query's), at the lane's
       // p = base(g) + 4 pt + i
@@ -450,7 +469,8 @@ __global__ __launch_bounds__(64 * kWaves, EPI == kEpiMaxDot ? 2 : 1) void k_mol_
 #pragma unroll
       for (int qb = 0; qb < 2 && (EPI == kEpiBounded || EPI == kEpiMaxDot); ++qb) {
         if constexpr (EPI == kEpiMaxDot) {
-          phi[qb] = mrow;
+          phi[qb] = mrow[0];
+          phi[qb + 2] = mrow[1];
           continue;
         }
         if constexpr (EPI == kEpiBounded) {
@@ -499,15 +519,16 @@ __global__ __launch_bounds__(64 * kWaves, EPI == kEpiMaxDot ? 2 : 1) void k_mol_
           }
         }
       }
-      // phi[qb] is valid in the lanes of rows 2 qb and 2 qb + 1 (the two-query
-      // chain leaves each query's result there; the other forms in every lane)
+      // phi[qb] is valid in the lanes of rows 2 (qb % 2) and 2 (qb % 2) + 1
+      // (the two-query chain and the max-dot sets leave each query's result
+      // there; the other forms in every lane)
 #pragma unroll
-      for (int qb = 0; qb < 2; ++qb) {
+      for (int qb = 0; qb < S::QPW; ++qb) {
         const int b = qwv + qb;
         if constexpr (DENSE) {
           if (g == 2 * qb && item_ok && b < pr.B) phi_out[b * phi_stride + (item - n_begin)] = phi[qb];
         } else {
-          top[qb].offer_score(phi[qb], item, g == 2 * qb && offer[qb], lane);
+          top[qb].offer_score(phi[qb], item, g == 2 * (qb % 2) && offer[qb], lane);
         }
       }
     }
@@ -523,7 +544,7 @@ __global__ __launch_bounds__(64 * kWaves, EPI == kEpiMaxDot ? 2 : 1) void k_mol_
 
   if constexpr (!DENSE) {
 #pragma unroll
-    for (int qb = 0; qb < 2; ++qb) {
+    for (int qb = 0; qb < S::QPW; ++qb) {
       top[qb].flush(lane);
       const int b = qwv + qb;
       if (b < pr.B) {
@@ -551,9 +572,10 @@ bool fused_maxdot_supported(const DevProb& pr, int k) {
 }
 
 void fused_grid(const DevProb& pr, int n_count, int& R, int& range_len, int& G, bool maxdot) {
-  G = (pr.B + kQueriesPerWG - 1) / kQueriesPerWG;
-  // about one workgroup per CU (two in the max-dot form)
-  R = std::max(1, (maxdot ? 512 : 256) / G);
+  const int qwg = queries_per_wave<false>() * kWaves;   // max-dot form
+  G = maxdot ? (pr.B + qwg - 1) / qwg : (pr.B + kQueriesPerWG - 1) / kQueriesPerWG;
+  // about one workgroup per CU
+  R = std::max(1, 256 / G);
   // ranges of at least 128 items (4 tiles): small corpora still fill the chip
   const int max_r = std::max(1, n_count / 128);
   R = std::min(R, max_r);
