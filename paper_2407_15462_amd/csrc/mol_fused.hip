@@ -7,7 +7,7 @@
 // 64 lanes in the run layout of mol_tile.h, whose chained f16 MFMAs evaluate
 // the gating MLP, the softmax and phi (Eq. 1 / Eq. 2 with the SiLU gating MLP
 // of Appendix A.3) with no lane exchange and no LDS re-layout.  (The max-dot
-// form keeps rows 8 q + pq, so that a lane group holds one query.)
+// form keeps rows 8 q + pq, so that two lane groups hold one query.)
 //
 // Epilogues (EPI):
 //  - kEpiTopk: a running per-query top-k of phi (Definition 1) kept in LDS
@@ -29,9 +29,9 @@
 //
 // Workgroup: 8 waves (2 per SIMD) = 16 queries sharing an LDS-staged
 // stream of 32-item tiles (a three-deep ring) loaded with direct
-// global->LDS copies.  The max-dot form stages 16-item tiles, so that two
-// workgroups share a CU (4 waves per SIMD), and takes m straight from
-// GEMM1's tile without splitting the two queries.
+// global->LDS copies.  The max-dot form stages 16-item tiles, gives each
+// wave four queries (32 per workgroup, one workgroup per CU) and takes m
+// straight from GEMM1's tiles without splitting the queries.
 #include "mol_tile.h"
 
 namespace mol {
