@@ -77,7 +77,8 @@ typedef enum {
 } mol_two_pass_mode;
 
 /* Problem flags (mol_problem.flags). */
-#define MOL_FLAG_F32_GATING 1u  /* gating MLP in float32 (see mol_problem) */
+#define MOL_FLAG_F32_GATING 1u     /* gating MLP in float32 (see mol_problem)        */
+#define MOL_FLAG_BF16X2_GATING 2u  /* gating MLP on two-term bf16 operands (ditto)    */
 
 /* Limits of the kernel set. */
 #define MOL_MAX_B 65535   /* queries per call                                */
@@ -99,10 +100,21 @@ typedef enum {
  * over 16 x 4096 pairs is 2.2e-6 for entries of standard deviation 0.1,
  * 7.8e-6 for 0.2, 2.0e-5 for 0.3 and 1.5e-4 for 0.5.  The fused path is
  * meant for gating weights with entries of RMS up to 0.3.  Beyond that,
- * set MOL_FLAG_F32_GATING: the gating MLP, softmax and phi then run in
- * float32 in the pair-wise kernel (component dots still on matrix cores,
- * exact products, float32 sums), several times slower.  float32 problems
- * always take that path. */
+ * set one of two flags:
+ *  - MOL_FLAG_BF16X2_GATING: the fused kernels take W1 and W2 exactly (bf16)
+ *    and carry -log2(e) s and the hidden activations as two bf16 terms each
+ *    (hi + lo, about 16 significant bits), with float32 accumulation: twice
+ *    the matrix work of the chain's two gating products.  Its error on the
+ *    same recipe: 4.3e-6 for entries of standard deviation 0.5, 7.6e-6 to
+ *    2.0e-5 for 1.0, but up to 7.0e-5 for 2.0, so it is meant for entries
+ *    of RMS up to 1.  Shapes without a fused kernel take the float32 path
+ *    below.
+ *  - MOL_FLAG_F32_GATING: the gating MLP, softmax and phi run in float32 in
+ *    the pair-wise kernel (component dots still on matrix cores, exact
+ *    products, float32 sums), more than ten times slower than the fused
+ *    path, with no limit on the weights.  It takes precedence when both
+ *    flags are set.
+ * float32 problems always take the float32 path. */
 typedef struct mol_problem {
   int32_t B;      /* number of queries                                      */
   int32_t N;      /* number of items                                        */

@@ -111,7 +111,8 @@ int check_problem(const mol_problem* p, bool gating) {
   if (p->B > MOL_MAX_B) return fail(MOL_EUNSUPPORTED, "B = %d exceeds %d", p->B, MOL_MAX_B);
   if (p->dtype != MOL_F32 && p->dtype != MOL_BF16)
     return fail(MOL_EUNSUPPORTED, "dtype %d is not MOL_F32 or MOL_BF16", p->dtype);
-  if (p->flags & ~MOL_FLAG_F32_GATING) return fail(MOL_EINVAL, "unknown flag bits 0x%x", p->flags);
+  if (p->flags & ~(MOL_FLAG_F32_GATING | MOL_FLAG_BF16X2_GATING))
+    return fail(MOL_EINVAL, "unknown flag bits 0x%x", p->flags);
   if (p->Pq > MOL_MAX_P || p->Px > MOL_MAX_P || p->Pq * p->Px > MOL_MAX_P)
     return fail(MOL_EUNSUPPORTED, "P = Pq*Px = %d*%d exceeds %d", p->Pq, p->Px, MOL_MAX_P);
   if (p->d > MOL_MAX_D) return fail(MOL_EUNSUPPORTED, "d = %d exceeds %d", p->d, MOL_MAX_D);

@@ -99,7 +99,7 @@ __device__ __forceinline__ void wg_coords(int g, int R, int G, int& r, int& qg) 
 
 }  // namespace
 
-template <int PX, int D, int H, int EPI>
+template <int PX, int D, int H, int EPI, bool X2>
 __global__ __launch_bounds__(64 * kWaves, 1) void k_mol_fused(
     DevProb pr, int k, int R, int range_len, int G, int n_begin, int n_end,
     const float* __restrict__ bound, uint64_t* __restrict__ partial, float* __restrict__ phi_out,
@@ -109,7 +109,9 @@ __global__ __launch_bounds__(64 * kWaves, 1) void k_mol_fused(
   // software-pipelined top-k scan
   constexpr bool PIPE = EPI == kEpiTopkPipe;
   using S = FusedShape<PX, D, H, MLP>;
-  using Mlp = MolMlp<PX, H>;
+  // X2: the two-term chain (plain loop only: top-k, dense and bounded forms)
+  static_assert(!X2 || EPI == kEpiTopk || EPI == kEpiDense || EPI == kEpiBounded, "two-term forms");
+  using Mlp = MolMlp<PX, H, X2>;
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   unsigned char* sX = smem;
   unsigned char* sAx = smem + S::LDS_X;
@@ -463,7 +465,7 @@ __global__ __launch_bounds__(64 * kWaves, 1) void k_mol_fused(
         f32x4_t c0[2][S::PT];
         gate_bias(0, c0[0]);
         gate_bias(1, c0[1]);
-        if constexpr (H <= 64) mlp.template phi2_interleaved<5>(s2, c0, phi);
+        if constexpr (H <= 64 && !X2) mlp.template phi2_interleaved<5>(s2, c0, phi);
         else mlp.template phi<2>(s2, c0, phi);
       }
 #pragma unroll
@@ -501,7 +503,7 @@ __global__ __launch_bounds__(64 * kWaves, 1) void k_mol_fused(
           f32x4_t c0[2][S::PT];
           gate_bias(0, c0[0]);
           gate_bias(1, c0[1]);
-          if constexpr (H <= 64) mlp.template phi2_interleaved<5>(s2, c0, phi);
+          if constexpr (H <= 64 && !X2) mlp.template phi2_interleaved<5>(s2, c0, phi);
           else mlp.template phi<2>(s2, c0, phi);
         } else {
 #pragma unroll
@@ -584,18 +586,32 @@ void fused_grid(const DevProb& pr, int n_count, int& R, int& range_len, int& G, 
   R = (n_count + range_len - 1) / range_len;
 }
 
-template <int PX, int D, int H, int EPI>
-static hipError_t launch_fused_t(const DevProb& pr, int k, int R, int range_len, int G, int n_begin,
+template <int PX, int D, int H, int EPI, bool X2>
+static hipError_t launch_fused_x(const DevProb& pr, int k, int R, int range_len, int G, int n_begin,
                                  int n_end, const float* bound, uint64_t* partial, float* phi,
                                  long phi_stride, int* redo, hipStream_t st) {
   using S = FusedShape<PX, D, H, EPI != kEpiMaxDot>;
-  auto kern = &k_mol_fused<PX, D, H, EPI>;
+  auto kern = &k_mol_fused<PX, D, H, EPI, X2>;
   hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                      hipFuncAttributeMaxDynamicSharedMemorySize, S::LDS_TOTAL);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(kern, dim3(R * G), dim3(64 * kWaves), S::LDS_TOTAL, st, pr, k, R, range_len,
                      G, n_begin, n_end, bound, partial, phi, phi_stride, redo);
   return hipGetLastError();
+}
+
+// the two-term chain where the problem asks for it (MOL_FLAG_BF16X2_GATING)
+template <int PX, int D, int H, int EPI>
+static hipError_t launch_fused_t(const DevProb& pr, int k, int R, int range_len, int G, int n_begin,
+                                 int n_end, const float* bound, uint64_t* partial, float* phi,
+                                 long phi_stride, int* redo, hipStream_t st) {
+  if constexpr (EPI == kEpiTopk || EPI == kEpiDense || EPI == kEpiBounded) {
+    if (pr.flags & MOL_FLAG_BF16X2_GATING)
+      return launch_fused_x<PX, D, H, EPI, true>(pr, k, R, range_len, G, n_begin, n_end, bound, partial, phi,
+                                                 phi_stride, redo, st);
+  }
+  return launch_fused_x<PX, D, H, EPI, false>(pr, k, R, range_len, G, n_begin, n_end, bound, partial, phi,
+                                              phi_stride, redo, st);
 }
 
 template <int EPI>
@@ -623,7 +639,7 @@ hipError_t launch_fused_topk(const DevProb& pr, int k, int R, int range_len, int
   if (bound)
     return launch_fused_d<kEpiBounded>(pr, k, R, range_len, G, 0, pr.N, bound, partial, nullptr, 0, nullptr,
                                        st);
-  if (redo) {
+  if (redo && !(pr.flags & MOL_FLAG_BF16X2_GATING)) {
     // pipelined scan, then the plain scan over the ranges it flagged
     hipError_t e = launch_fused_d<kEpiTopkPipe>(pr, k, R, range_len, G, 0, pr.N, nullptr, partial, nullptr, 0,
                                                 redo, st);

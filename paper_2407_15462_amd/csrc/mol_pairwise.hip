@@ -180,7 +180,9 @@ __global__ __launch_bounds__(256) void k_phi_mfma(
 }
 
 bool phi_mfma_supported(const DevProb& pr) {
-  return !(pr.flags & MOL_FLAG_F32_GATING) && pr.dtype == MOL_BF16 && pr.P <= 64 && pr.H <= 128;
+  // the f16 chain only: both precision flags take the float32 kernel here
+  return !(pr.flags & (MOL_FLAG_F32_GATING | MOL_FLAG_BF16X2_GATING)) && pr.dtype == MOL_BF16 && pr.P <= 64 &&
+         pr.H <= 128;
 }
 
 // Waves of one k_phi_mfma instantiation that the device holds at once.

@@ -23,11 +23,11 @@ constexpr int kWaves = 4;
 constexpr int kTopkRegion = WaveTopk::kList + WaveTopk::kStage;
 }  // namespace
 
-template <int PX, int D, int H, bool NEG>
+template <int PX, int D, int H, bool NEG, bool X2>
 __global__ __launch_bounds__(64 * kWaves, 2) void k_mol_rerank(
     DevProb pr, const int32_t* __restrict__ uniq, const int32_t* __restrict__ n_unique, int C,
     int k, int chunk, int nchunks, uint64_t* __restrict__ partial) {
-  using Mlp = MolMlp<PX, H>;
+  using Mlp = MolMlp<PX, H, X2>;   // X2: the two-term gating chain
   constexpr int P = 8 * PX, RUN = 2 * PX, KD = D / 32, PT = P / 16;
   __shared__ uint64_t sTop[kWaves * kTopkRegion];
   // the wave's gather buffer: block (px, kk) of 1 KB holds lane i's 16 bytes
@@ -152,16 +152,24 @@ int rerank_chunk(int B, int C) {
   return 256;
 }
 
-template <int PX, int D, int H, bool NEG>
-static hipError_t launch_rerank_one(const DevProb& pr, dim3 grid, const int32_t* uniq, const int32_t* n_unique,
-                                    int C, int k, int chunk, int nchunks, uint64_t* partial, hipStream_t st) {
+template <int PX, int D, int H, bool NEG, bool X2>
+static hipError_t launch_rerank_x(const DevProb& pr, dim3 grid, const int32_t* uniq, const int32_t* n_unique,
+                                  int C, int k, int chunk, int nchunks, uint64_t* partial, hipStream_t st) {
   constexpr int kGather = kWaves * PX * (D / 32) * 1024;   // the waves' gather buffers
-  auto kern = &k_mol_rerank<PX, D, H, NEG>;
+  auto kern = &k_mol_rerank<PX, D, H, NEG, X2>;
   const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                            hipFuncAttributeMaxDynamicSharedMemorySize, kGather);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(kern, grid, dim3(64 * kWaves), kGather, st, pr, uniq, n_unique, C, k, chunk, nchunks, partial);
   return hipGetLastError();
+}
+
+template <int PX, int D, int H, bool NEG>
+static hipError_t launch_rerank_one(const DevProb& pr, dim3 grid, const int32_t* uniq, const int32_t* n_unique,
+                                    int C, int k, int chunk, int nchunks, uint64_t* partial, hipStream_t st) {
+  if (pr.flags & MOL_FLAG_BF16X2_GATING)
+    return launch_rerank_x<PX, D, H, NEG, true>(pr, grid, uniq, n_unique, C, k, chunk, nchunks, partial, st);
+  return launch_rerank_x<PX, D, H, NEG, false>(pr, grid, uniq, n_unique, C, k, chunk, nchunks, partial, st);
 }
 
 template <bool NEG>

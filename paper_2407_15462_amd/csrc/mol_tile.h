@@ -273,8 +273,26 @@ __device__ __forceinline__ void row_sums(float da, float na, float db, float nb,
 }
 
 
+// f32 pair -> bf16 pair (nearest-even), a in the low half
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint32_t pack_bf16(float a, float b) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{a, b}, bf16x2_t));
+}
+// (a, b) as two bf16 terms: hi = bf16(x), lo = bf16(x - hi), so that hi + lo
+// carries x to about 2^-17 relative (16 significant bits against f16's 11)
+__device__ __forceinline__ void split_bf16(float a, float b, uint32_t& hi, uint32_t& lo) {
+  hi = pack_bf16(a, b);
+  lo = pack_bf16(a - __uint_as_float(hi << 16), b - __uint_as_float(hi & 0xffff0000u));
+}
+
 // Per-wave constants of the gating MLP in MFMA operand layouts.
-template <int PX, int H>
+//
+// X2 (the two-term form): W1 and -W2 enter as their own bf16 values (exact),
+// and the two operands computed on the way, -log2(e) s and h', as two bf16
+// terms each (split_bf16), so GEMM2 and GEMM3 take two bf16 MFMAs per K
+// block; the chain then holds phi to float32-like accuracy for gating
+// weights far beyond the f16 form's range (Appendix A.3's MLP, unchanged).
+template <int PX, int H, bool X2 = false>
 struct MolMlp {
   static constexpr int P = 8 * PX;
   static constexpr int RUN = 2 * PX;
@@ -302,8 +320,9 @@ struct MolMlp {
         uint32_t w[4];
 #pragma unroll
         for (int e = 0; e < 4; ++e)
-          w[e] = neg_bf16_to_f16_bits(src[2 * e], kLog2e) |
-                 (neg_bf16_to_f16_bits(src[2 * e + 1], kLog2e) << 16);
+          w[e] = X2 ? static_cast<uint32_t>(src[2 * e]) | (static_cast<uint32_t>(src[2 * e + 1]) << 16)
+                    : neg_bf16_to_f16_bits(src[2 * e], kLog2e) |
+                          (neg_bf16_to_f16_bits(src[2 * e + 1], kLog2e) << 16);
         w1op[jt][m] = make_uint4(w[0], w[1], w[2], w[3]);
       }
     // -W2: row 16 pt + c <-> p = base(c/4) + 4 pt + c%4; K slot 8g+e <-> j
@@ -318,8 +337,10 @@ struct MolMlp {
           const int e0 = 2 * e2, e1 = 2 * e2 + 1;
           const int j0 = 32 * m + 16 * (e0 >> 2) + 4 * g + (e0 & 3);
           const int j1 = 32 * m + 16 * (e1 >> 2) + 4 * g + (e1 & 3);
-          w[e2] = neg_bf16_to_f16_bits(W2[p * H + j0], 1.f) |
-                  (neg_bf16_to_f16_bits(W2[p * H + j1], 1.f) << 16);
+          w[e2] = X2 ? (static_cast<uint32_t>(W2[p * H + j0]) ^ 0x8000u) |
+                           ((static_cast<uint32_t>(W2[p * H + j1]) ^ 0x8000u) << 16)
+                     : neg_bf16_to_f16_bits(W2[p * H + j0], 1.f) |
+                           (neg_bf16_to_f16_bits(W2[p * H + j1], 1.f) << 16);
         }
         w2op[pt][m] = make_uint4(w[0], w[1], w[2], w[3]);
       }
@@ -334,6 +355,7 @@ struct MolMlp {
   // padded hidden units give h' = 0 and the padded components' logits keep
   // their accumulator input (set to -inf by the caller: zero weight).
   __device__ void load_padded(const DevProb& pr, int c, int g) {
+    static_assert(!X2, "the padded form has no two-term variant");
     const bf16_t* W1 = static_cast<const bf16_t*>(pr.W1);
     const bf16_t* W2 = static_cast<const bf16_t*>(pr.W2);
     const int Pr = pr.P, Hr = pr.H;
@@ -428,6 +450,10 @@ struct MolMlp {
   // Base-2 gating logits l' of one query for the lane's items (GEMM2 ->
   // SiLU -> GEMM3), each matrix chain issued at raised wave priority.
   __device__ void logits(const float (&s)[RUN], const f32x4_t (&c0)[PT], f32x4_t (&lg)[PT]) const {
+    if constexpr (X2) {
+      logits_x2(s, c0, lg);
+      return;
+    }
     uint4 sop[KP];
     pack_s(s, sop);
     f32x4_t u[JT];
@@ -438,6 +464,60 @@ struct MolMlp {
     silu(u, hop);
     mfma_priority_begin();
     gemm3(hop, c0, lg);
+    mfma_priority_end();
+  }
+
+  // The two-term chain: x = -log2(e) s and h' = u' / (1 + 2^u') as hi + lo
+  // bf16 pairs; each K block of GEMM2 and GEMM3 takes the hi and the lo
+  // operand against the same exact weights.
+  __device__ void logits_x2(const float (&s)[RUN], const f32x4_t (&c0)[PT], f32x4_t (&lg)[PT]) const {
+    uint4 shi[KP], slo[KP];
+#pragma unroll
+    for (int m = 0; m < KP; ++m) {
+      uint32_t h[4], l[4];
+#pragma unroll
+      for (int e2 = 0; e2 < 4; ++e2)
+        split_bf16(-kLog2e * s[8 * m + 2 * e2], -kLog2e * s[8 * m + 2 * e2 + 1], h[e2], l[e2]);
+      shi[m] = make_uint4(h[0], h[1], h[2], h[3]);
+      slo[m] = make_uint4(l[0], l[1], l[2], l[3]);
+    }
+    f32x4_t u[JT];
+    mfma_priority_begin();
+#pragma unroll
+    for (int jt = 0; jt < JT; ++jt) {
+      u[jt] = b1acc[jt];
+#pragma unroll
+      for (int m = 0; m < KP; ++m) {
+        u[jt] = mfma_bf16(w1op[jt][m], shi[m], u[jt]);
+        u[jt] = mfma_bf16(w1op[jt][m], slo[m], u[jt]);
+      }
+    }
+    mfma_priority_end();
+    uint4 hhi[KH], hlo[KH];
+#pragma unroll
+    for (int m = 0; m < KH; ++m) {
+      float hv[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float x = u[2 * m + (e >> 2)][e & 3];
+        hv[e] = x * __builtin_amdgcn_rcpf(1.f + __builtin_amdgcn_exp2f(x));
+      }
+      uint32_t h[4], l[4];
+#pragma unroll
+      for (int e2 = 0; e2 < 4; ++e2) split_bf16(hv[2 * e2], hv[2 * e2 + 1], h[e2], l[e2]);
+      hhi[m] = make_uint4(h[0], h[1], h[2], h[3]);
+      hlo[m] = make_uint4(l[0], l[1], l[2], l[3]);
+    }
+    mfma_priority_begin();
+#pragma unroll
+    for (int pt = 0; pt < PT; ++pt) {
+      lg[pt] = c0[pt];
+#pragma unroll
+      for (int m = 0; m < KH; ++m) {
+        lg[pt] = mfma_bf16(w2op[pt][m], hhi[m], lg[pt]);
+        lg[pt] = mfma_bf16(w2op[pt][m], hlo[m], lg[pt]);
+      }
+    }
     mfma_priority_end();
   }
 
@@ -474,6 +554,7 @@ struct MolMlp {
   // a query whose sum left [2^-60, 2^60] is redone by phi<2>.
   template <int VA>
   __device__ void phi2_interleaved(const float (&s)[2][RUN], const f32x4_t (&c0)[2][PT], float (&out)[2]) const {
+    static_assert(!X2, "the interleaved chain is the f16 form");
     uint4 sop[2][KP];
     f32x4_t u[2][JT];
     uint4 hop[2][KH];
@@ -523,6 +604,7 @@ struct MolMlp {
   template <int VA, int NDS = 0>
   __device__ void phi2_stage_a(const float (&s)[2][RUN], const f32x4_t (&c0)[2][PT], f32x4_t (&lg1)[PT],
                                float& den0, float& num0) const {
+    static_assert(!X2, "the pipelined chain is the f16 form");
     if constexpr (H > 64) {
       f32x4_t lg0[PT];
       logits(s[0], c0[0], lg0);

@@ -22,6 +22,7 @@ MOL_F32, MOL_BF16 = 0, 1
  MOL_OP_TOPK_BOUNDED, MOL_OP_TOPK_TWO_PASS) = range(7)
 MOL_TWO_PASS_MIN, MOL_TWO_PASS_KTH = 0, 1
 MOL_FLAG_F32_GATING = 1
+MOL_FLAG_BF16X2_GATING = 2
 
 EXPORTS = ("mol_workspace_size", "mol_score", "mol_topk_exact", "mol_topk_exact_noalloc", "mol_topk_exact_bounded",
            "mol_topk_two_pass", "mol_topk_maxdot", "mol_topk_per_embd",

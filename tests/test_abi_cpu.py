@@ -240,6 +240,8 @@ def test_unknown_problem_flags_are_rejected():
     c.flags = 0x6
     rc, _ = _ws(c, mol.MOL_OP_TOPK_EXACT, k=5)
     assert rc == mol.MOL_EINVAL and b"flag" in lib.mol_last_error()
-    c.flags = mol.MOL_FLAG_F32_GATING
-    rc, _ = _ws(c, mol.MOL_OP_TOPK_EXACT, k=5)
-    assert rc == mol.MOL_OK
+    for flags in (mol.MOL_FLAG_F32_GATING, mol.MOL_FLAG_BF16X2_GATING,
+                  mol.MOL_FLAG_F32_GATING | mol.MOL_FLAG_BF16X2_GATING):
+        c.flags = flags
+        rc, _ = _ws(c, mol.MOL_OP_TOPK_EXACT, k=5)
+        assert rc == mol.MOL_OK

@@ -38,13 +38,15 @@ def test_source_digest_ignores_comments_and_layout(tmp_path, monkeypatch):
 
 
 def test_gating_range_matches_the_header():
-    # the bench sends gating beyond the fused chain's stated range to the
-    # float32 path; the range is the one include/mol.h states
+    # the bench sends gating beyond the f16 chain's stated range to the
+    # two-term chain, and beyond that to the float32 path; the ranges are the
+    # ones include/mol.h states
     bench = load_bench()
     text = open(os.path.join(ROOT, "include", "mol.h")).read()
-    m = re.search(r"entries of\s+\*?\s*RMS up to ([0-9]+(?:\.[0-9]+)?)", text)
-    assert m, "include/mol.h states the fused chain's gating range"
-    assert float(m.group(1)) == pytest.approx(bench.F32_GATING_STD)
+    found = re.findall(r"entries\s+\*?\s*of\s+\*?\s*RMS up to ([0-9]+(?:\.[0-9]+)?)", text)
+    assert len(found) == 2, "include/mol.h states the f16 and the two-term chains' gating ranges"
+    assert float(found[0]) == pytest.approx(bench.F32_GATING_STD)
+    assert float(found[1]) == pytest.approx(bench.X2_GATING_STD)
 
 
 def test_issue_floor_summary_is_consistent():

@@ -621,6 +621,39 @@ def test_f32_gating_on_skewed_weights_matches_oracle():
         check_topk_row(full, ri[b], rs[b], 100, f"f32_gating rerank query {b}")
 
 
+@pytest.mark.parametrize("wl,std", [("exact_1m", 0.5), ("exact_1m", 1.0), ("exact_32k", 1.0), ("hybrid_8m", 1.0),
+                                    ("paper_books", 1.0)])
+def test_bf16x2_gating_matches_oracle(wl, std):
+    """MOL_FLAG_BF16X2_GATING: every fused shape (P = 8 x 8 at d = 64 and 32,
+    8 x 4 at d = 64 and 128) with gating weights of standard deviation 1,
+    the top of the two-term chain's stated range and far outside the f16
+    chain's, and 0.5 (the skewed workload): mol_score, the exact top-k, the
+    bounded pass at the k-th score and the rerank meet the 1e-4 bar."""
+    spec = dataclasses.replace(W[wl].scaled(B=12, N=4099, clusters=64), gating_std=std)
+    log(f"[bf16x2 gating] {wl} std={std} B={spec.B} N={spec.N}")
+    inp = cuda_inputs(spec, seed=31)
+    prob = mol.Problem.from_inputs(inp, flags=mol.MOL_FLAG_BF16X2_GATING)
+    phi = mol.score(prob)
+    s, i = mol.topk_exact(prob, 100)
+    bs, bi = mol.topk_exact_bounded(prob, 100, s[:, 99].contiguous())
+    g = torch.Generator(device="cuda").manual_seed(8)
+    cand = torch.randint(-1, spec.N, (spec.B, 700), device="cuda", generator=g, dtype=torch.int32)
+    rs, ri, nu = mol.rerank(prob, cand, 100)
+    torch.cuda.synchronize()
+    want = mo.mol_scores(oracle_problem(inp), list(range(spec.B)))
+    check_scores(phi.cpu().numpy(), want, what=f"bf16x2_{wl}_{std} phi")
+    s, i, bs, bi = s.cpu().numpy(), i.cpu().numpy(), bs.cpu().numpy(), bi.cpu().numpy()
+    rs, ri = rs.cpu().numpy(), ri.cpu().numpy()
+    cand_np = cand.cpu().numpy()
+    for b in range(spec.B):
+        check_topk_row(want[b], i[b], s[b], 100, f"bf16x2_{wl}_{std} exact query {b}")
+        check_topk_row(want[b], bi[b], bs[b], 100, f"bf16x2_{wl}_{std} bounded query {b}")
+        uniq = mo.union_dedup([cand_np[b]])
+        full = np.full(spec.N, -np.inf)
+        full[uniq] = want[b][uniq]
+        check_topk_row(full, ri[b], rs[b], 100, f"bf16x2_{wl}_{std} rerank query {b}")
+
+
 def test_fused_gating_at_the_edge_of_its_range():
     """The fused chain at the edge of its stated range (gating entries of
     standard deviation 0.3) still meets the 1e-4 bar for scores and top-k."""
