@@ -628,7 +628,8 @@ def test_bf16x2_gating_matches_oracle(wl, std):
     8 x 4 at d = 64 and 128) with gating weights of standard deviation 1,
     the top of the two-term chain's stated range and far outside the f16
     chain's, and 0.5 (the skewed workload): mol_score, the exact top-k, the
-    bounded pass at the k-th score and the rerank meet the 1e-4 bar."""
+    bounded pass at the k-th score, Algorithm 1's two passes, the
+    allocation-free exact top-k and the rerank meet the 1e-4 bar."""
     spec = dataclasses.replace(W[wl].scaled(B=12, N=4099, clusters=64), gating_std=std)
     log(f"[bf16x2 gating] {wl} std={std} B={spec.B} N={spec.N}")
     inp = cuda_inputs(spec, seed=31)
@@ -636,6 +637,9 @@ def test_bf16x2_gating_matches_oracle(wl, std):
     phi = mol.score(prob)
     s, i = mol.topk_exact(prob, 100)
     bs, bi = mol.topk_exact_bounded(prob, 100, s[:, 99].contiguous())
+    ts, ti, _ = mol.topk_two_pass(prob, 100, mol.MOL_TWO_PASS_KTH)
+    ns, ni = torch.empty_like(s), torch.empty_like(i)
+    mol.mol_topk_exact_noalloc(prob, 100, ns, ni)
     g = torch.Generator(device="cuda").manual_seed(8)
     cand = torch.randint(-1, spec.N, (spec.B, 700), device="cuda", generator=g, dtype=torch.int32)
     rs, ri, nu = mol.rerank(prob, cand, 100)
@@ -643,11 +647,14 @@ def test_bf16x2_gating_matches_oracle(wl, std):
     want = mo.mol_scores(oracle_problem(inp), list(range(spec.B)))
     check_scores(phi.cpu().numpy(), want, what=f"bf16x2_{wl}_{std} phi")
     s, i, bs, bi = s.cpu().numpy(), i.cpu().numpy(), bs.cpu().numpy(), bi.cpu().numpy()
+    ts, ti, ns, ni = ts.cpu().numpy(), ti.cpu().numpy(), ns.cpu().numpy(), ni.cpu().numpy()
     rs, ri = rs.cpu().numpy(), ri.cpu().numpy()
     cand_np = cand.cpu().numpy()
     for b in range(spec.B):
         check_topk_row(want[b], i[b], s[b], 100, f"bf16x2_{wl}_{std} exact query {b}")
         check_topk_row(want[b], bi[b], bs[b], 100, f"bf16x2_{wl}_{std} bounded query {b}")
+        check_topk_row(want[b], ti[b], ts[b], 100, f"bf16x2_{wl}_{std} two-pass query {b}")
+        check_topk_row(want[b], ni[b], ns[b], 100, f"bf16x2_{wl}_{std} no-alloc query {b}")
         uniq = mo.union_dedup([cand_np[b]])
         full = np.full(spec.N, -np.inf)
         full[uniq] = want[b][uniq]
