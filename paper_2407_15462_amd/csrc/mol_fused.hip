@@ -462,11 +462,29 @@ __global__ __launch_bounds__(64 * kWaves, 1) void k_mol_fused(
         // both queries' MLP chains in one call: interleaved by hand where the
         // matrix chains are short against the SiLU work (H <= 64), else
         // left to the compiler with raised priority around each chain
-        f32x4_t c0[2][S::PT];
-        gate_bias(0, c0[0]);
-        gate_bias(1, c0[1]);
-        if constexpr (H <= 64 && !X2) mlp.template phi2_interleaved<5>(s2, c0, phi);
-        else mlp.template phi<2>(s2, c0, phi);
+        if constexpr (X2) {
+          // the two-term chains one query after the other, each with its own
+          // gate inputs: both at once spilled 3-12 VGPRs (exact_1m_skewed
+          // top-k 60.3 ms against 54.4 ms this way)
+#pragma unroll
+          for (int qb = 0; qb < 2; ++qb) {
+            float sq[1][S::RUN];
+#pragma unroll
+            for (int mu = 0; mu < S::RUN; ++mu) sq[0][mu] = s2[qb][mu];
+            f32x4_t c0[1][S::PT];
+            gate_bias(qb, c0[0]);
+            float pq[1];
+            mlp.template phi<1>(sq, c0, pq);
+            phi[qb] = pq[0];
+            __builtin_amdgcn_sched_barrier(0);
+          }
+        } else {
+          f32x4_t c0[2][S::PT];
+          gate_bias(0, c0[0]);
+          gate_bias(1, c0[1]);
+          if constexpr (H <= 64) mlp.template phi2_interleaved<5>(s2, c0, phi);
+          else mlp.template phi<2>(s2, c0, phi);
+        }
       }
 #pragma unroll
       for (int qb = 0; qb < 2 && (EPI == kEpiBounded || EPI == kEpiMaxDot); ++qb) {
@@ -498,8 +516,9 @@ __global__ __launch_bounds__(64 * kWaves, 1) void k_mol_fused(
         }
       }
       if constexpr (EPI == kEpiBounded) {
-        if (need[0] && need[1]) {
-          // both chains run: as one two-query call (the same arithmetic)
+        if (need[0] && need[1] && !X2) {
+          // both chains run: as one two-query call (the same arithmetic; the
+          // two-term form takes the per-query calls below, whose registers fit)
           f32x4_t c0[2][S::PT];
           gate_bias(0, c0[0]);
           gate_bias(1, c0[1]);
