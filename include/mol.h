@@ -107,8 +107,9 @@ typedef enum {
  *    the matrix work of the chain's two gating products.  Its error on the
  *    same recipe: 4.3e-6 for entries of standard deviation 0.5, 7.6e-6 to
  *    2.0e-5 for 1.0, but up to 7.0e-5 for 2.0, so it is meant for entries
- *    of RMS up to 1.  Shapes without a fused kernel take the float32 path
- *    below.
+ *    of RMS up to 1.  bf16 shapes without a fused kernel take the same
+ *    two-term chain in the pair-wise kernel (P <= 64, H <= 128), others
+ *    the float32 path below.
  *  - MOL_FLAG_F32_GATING: the gating MLP, softmax and phi run in float32 in
  *    the pair-wise kernel (component dots still on matrix cores, exact
  *    products, float32 sums), more than ten times slower than the fused

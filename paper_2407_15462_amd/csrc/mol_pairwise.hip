@@ -40,13 +40,14 @@ constexpr int kPairMinIters = 16;
 // BOUNDED: Algorithm 1's second pass (kGenBounded); otherwise phi, negated
 // when `neg` is set (kGenPhi, kGenNegPhi).  GATHER: per-query candidate
 // lists (items != NULL) rather than a contiguous range.
-template <int PXV, int HV, bool BOUNDED, bool GATHER>
+template <int PXV, int HV, bool BOUNDED, bool GATHER, bool X2>
 __global__ __launch_bounds__(256) void k_phi_mfma(
     DevProb pr, bool neg, const float* __restrict__ bound, int n_begin, int n_count, int steps,
     const int32_t* __restrict__ items, const int32_t* __restrict__ item_count, long item_stride,
     const float* __restrict__ sbuf, long s_pstride, long s_bstride,
     float* __restrict__ phi, long phi_stride, uint64_t* __restrict__ keys, long key_stride) {
-  using Mlp = std::conditional_t<PXV == 2, MolMlp16<HV>, MolMlp<PXV, HV>>;
+  // X2: the two-term gating chain
+  using Mlp = std::conditional_t<PXV == 2, MolMlp16<HV, X2>, MolMlp<PXV, HV, X2>>;
   constexpr int RUN = Mlp::RUN, PT = Mlp::PT;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int c = lane & 15, g = lane >> 4;
@@ -180,20 +181,18 @@ __global__ __launch_bounds__(256) void k_phi_mfma(
 }
 
 bool phi_mfma_supported(const DevProb& pr) {
-  // the f16 chain only: both precision flags take the float32 kernel here
-  return !(pr.flags & (MOL_FLAG_F32_GATING | MOL_FLAG_BF16X2_GATING)) && pr.dtype == MOL_BF16 && pr.P <= 64 &&
-         pr.H <= 128;
+  return !(pr.flags & MOL_FLAG_F32_GATING) && pr.dtype == MOL_BF16 && pr.P <= 64 && pr.H <= 128;
 }
 
 // Waves of one k_phi_mfma instantiation that the device holds at once.
-template <int PXV, int HV, bool BOUNDED, bool GATHER>
+template <int PXV, int HV, bool BOUNDED, bool GATHER, bool X2>
 static long pair_resident_waves() {
   static const long waves = [] {
     int dev = 0, ncu = 0, nb = 0;
     if (hipGetDevice(&dev) != hipSuccess ||
         hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || ncu <= 0)
       ncu = 256;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, k_phi_mfma<PXV, HV, BOUNDED, GATHER>, 256, 0) !=
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, k_phi_mfma<PXV, HV, BOUNDED, GATHER, X2>, 256, 0) !=
             hipSuccess ||
         nb <= 0)
       nb = 1;
@@ -207,19 +206,36 @@ static long pair_resident_waves() {
 // kPairMinIters iterations, and about one round of resident waves for the
 // whole launch (a wave that lives longer amortises its operand set-up), but
 // no more than one workgroup of 4 waves needs for the whole range.
+template <int PXV, int HV, bool BOUNDED, bool GATHER, bool X2>
+static void launch_phi_mfma_x(long per_query, long groups, long qb, const DevProb& pr, bool neg,
+                              const float* bound, int n_begin, int n_count, const int32_t* items,
+                              const int32_t* item_count, long item_stride, const float* sbuf, long s_pstride,
+                              long s_bstride, float* phi, long phi_stride, uint64_t* keys, long key_stride,
+                              hipStream_t st) {
+  const long waves = pair_resident_waves<PXV, HV, BOUNDED, GATHER, X2>();
+  long steps = std::max<long>((kPairMinIters + qb - 1) / qb, (per_query * groups + waves - 1) / waves);
+  steps = std::max<long>(1, std::min<long>(steps, (per_query + 3) / 4));
+  const dim3 grid(static_cast<unsigned>((per_query + 4 * steps - 1) / (4 * steps)), static_cast<unsigned>(groups));
+  hipLaunchKernelGGL((k_phi_mfma<PXV, HV, BOUNDED, GATHER, X2>), grid, dim3(256), 0, st, pr, neg, bound, n_begin,
+                     n_count, static_cast<int>(steps), items, item_count, item_stride, sbuf, s_pstride, s_bstride,
+                     phi, phi_stride, keys, key_stride);
+}
+
+// the two-term chain where the problem asks for it (MOL_FLAG_BF16X2_GATING)
 template <int PXV, int HV, bool BOUNDED, bool GATHER>
 static void launch_phi_mfma_k(long per_query, long groups, long qb, const DevProb& pr, bool neg,
                               const float* bound, int n_begin, int n_count, const int32_t* items,
                               const int32_t* item_count, long item_stride, const float* sbuf, long s_pstride,
                               long s_bstride, float* phi, long phi_stride, uint64_t* keys, long key_stride,
                               hipStream_t st) {
-  const long waves = pair_resident_waves<PXV, HV, BOUNDED, GATHER>();
-  long steps = std::max<long>((kPairMinIters + qb - 1) / qb, (per_query * groups + waves - 1) / waves);
-  steps = std::max<long>(1, std::min<long>(steps, (per_query + 3) / 4));
-  const dim3 grid(static_cast<unsigned>((per_query + 4 * steps - 1) / (4 * steps)), static_cast<unsigned>(groups));
-  hipLaunchKernelGGL((k_phi_mfma<PXV, HV, BOUNDED, GATHER>), grid, dim3(256), 0, st, pr, neg, bound, n_begin,
-                     n_count, static_cast<int>(steps), items, item_count, item_stride, sbuf, s_pstride, s_bstride,
-                     phi, phi_stride, keys, key_stride);
+  if (pr.flags & MOL_FLAG_BF16X2_GATING)
+    launch_phi_mfma_x<PXV, HV, BOUNDED, GATHER, true>(per_query, groups, qb, pr, neg, bound, n_begin, n_count,
+                                                      items, item_count, item_stride, sbuf, s_pstride, s_bstride,
+                                                      phi, phi_stride, keys, key_stride, st);
+  else
+    launch_phi_mfma_x<PXV, HV, BOUNDED, GATHER, false>(per_query, groups, qb, pr, neg, bound, n_begin, n_count,
+                                                       items, item_count, item_stride, sbuf, s_pstride, s_bstride,
+                                                       phi, phi_stride, keys, key_stride, st);
 }
 
 template <int PXV, int HV, bool BOUNDED>

@@ -355,7 +355,6 @@ struct MolMlp {
   // padded hidden units give h' = 0 and the padded components' logits keep
   // their accumulator input (set to -inf by the caller: zero weight).
   __device__ void load_padded(const DevProb& pr, int c, int g) {
-    static_assert(!X2, "the padded form has no two-term variant");
     const bf16_t* W1 = static_cast<const bf16_t*>(pr.W1);
     const bf16_t* W2 = static_cast<const bf16_t*>(pr.W2);
     const int Pr = pr.P, Hr = pr.H;
@@ -366,12 +365,12 @@ struct MolMlp {
     auto w1 = [&](int j, int p) -> uint32_t {
       const bf16_t w = W1[min(j, Hr - 1) * Pr + min(p, Pr - 1)];
       const uint32_t keep = 0u - static_cast<uint32_t>((j < Hr) & (p < Pr));
-      return neg_bf16_to_f16_bits(w, kLog2e) & keep;
+      return (X2 ? static_cast<uint32_t>(w) : neg_bf16_to_f16_bits(w, kLog2e)) & keep;
     };
     auto w2 = [&](int p, int j) -> uint32_t {
       const bf16_t w = W2[min(p, Pr - 1) * Hr + min(j, Hr - 1)];
       const uint32_t keep = 0u - static_cast<uint32_t>((j < Hr) & (p < Pr));
-      return neg_bf16_to_f16_bits(w, 1.f) & keep;
+      return (X2 ? static_cast<uint32_t>(w ^ 0x8000u) : neg_bf16_to_f16_bits(w, 1.f)) & keep;
     };
 #pragma unroll
     for (int jt = 0; jt < JT; ++jt)
@@ -699,8 +698,9 @@ struct MolMlp {
 // e < 4, and GEMM3 has one output tile whose row 4 g + i is p = 4 g + i:
 // no padding of P to 32.  Same interface as MolMlp (pr.P <= 16, pr.H <= H).
 typedef _Float16 f16x4_t __attribute__((ext_vector_type(4)));
-template <int H>
-struct MolMlp16 {
+typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
+template <int H, bool X2 = false>
+struct MolMlp16 {   // X2: the two-term chain, as in MolMlp
   static constexpr int P = 16;
   static constexpr int RUN = 4;
   static constexpr int JT = H / 16;   // output tiles of GEMM2
@@ -719,12 +719,12 @@ struct MolMlp16 {
     auto w1 = [&](int j, int p) -> uint32_t {
       const bf16_t w = W1[min(j, Hr - 1) * Pr + min(p, Pr - 1)];
       const uint32_t keep = 0u - static_cast<uint32_t>((j < Hr) & (p < Pr));
-      return neg_bf16_to_f16_bits(w, kLog2e) & keep;
+      return (X2 ? static_cast<uint32_t>(w) : neg_bf16_to_f16_bits(w, kLog2e)) & keep;
     };
     auto w2 = [&](int p, int j) -> uint32_t {
       const bf16_t w = W2[min(p, Pr - 1) * Hr + min(j, Hr - 1)];
       const uint32_t keep = 0u - static_cast<uint32_t>((j < Hr) & (p < Pr));
-      return neg_bf16_to_f16_bits(w, 1.f) & keep;
+      return (X2 ? static_cast<uint32_t>(w ^ 0x8000u) : neg_bf16_to_f16_bits(w, 1.f)) & keep;
     };
     // W1' = -log2(e) W1: row j = 16 jt + c, K slot 4 g + e <-> p = 4 g + e
 #pragma unroll
@@ -756,6 +756,10 @@ struct MolMlp16 {
   }
 
   __device__ void logits(const float (&s)[RUN], const f32x4_t (&c0)[PT], f32x4_t (&lg)[PT]) const {
+    if constexpr (X2) {
+      logits_x2(s, c0, lg);
+      return;
+    }
     const uint2 sop = make_uint2(pack_f16(s[0], s[1]), pack_f16(s[2], s[3]));
     f32x4_t u[JT];
     mfma_priority_begin();
@@ -780,6 +784,48 @@ struct MolMlp16 {
     lg[0] = c0[0];
 #pragma unroll
     for (int m = 0; m < KH; ++m) lg[0] = mfma_f16(w2op[m], hop[m], lg[0]);
+    mfma_priority_end();
+  }
+
+  // The two-term chain (see MolMlp::logits_x2): GEMM2 on 16x16x16 bf16 MFMAs
+  // with the hi and the lo operand of -log2(e) s, GEMM3 with those of h'.
+  __device__ void logits_x2(const float (&s)[RUN], const f32x4_t (&c0)[PT], f32x4_t (&lg)[PT]) const {
+    uint32_t s01h, s01l, s23h, s23l;
+    split_bf16(-kLog2e * s[0], -kLog2e * s[1], s01h, s01l);
+    split_bf16(-kLog2e * s[2], -kLog2e * s[3], s23h, s23l);
+    const uint2 shi = make_uint2(s01h, s23h), slo = make_uint2(s01l, s23l);
+    f32x4_t u[JT];
+    mfma_priority_begin();
+#pragma unroll
+    for (int jt = 0; jt < JT; ++jt) {
+      u[jt] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(bf16x4_t, w1op[jt]),
+                                                       __builtin_bit_cast(bf16x4_t, shi), b1acc[jt], 0, 0, 0);
+      u[jt] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(bf16x4_t, w1op[jt]),
+                                                       __builtin_bit_cast(bf16x4_t, slo), u[jt], 0, 0, 0);
+    }
+    mfma_priority_end();
+    uint4 hhi[KH], hlo[KH];
+#pragma unroll
+    for (int m = 0; m < KH; ++m) {
+      float hv[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float x = u[2 * m + (e >> 2)][e & 3];
+        hv[e] = x * __builtin_amdgcn_rcpf(1.f + __builtin_amdgcn_exp2f(x));
+      }
+      uint32_t h[4], l[4];
+#pragma unroll
+      for (int e2 = 0; e2 < 4; ++e2) split_bf16(hv[2 * e2], hv[2 * e2 + 1], h[e2], l[e2]);
+      hhi[m] = make_uint4(h[0], h[1], h[2], h[3]);
+      hlo[m] = make_uint4(l[0], l[1], l[2], l[3]);
+    }
+    mfma_priority_begin();
+    lg[0] = c0[0];
+#pragma unroll
+    for (int m = 0; m < KH; ++m) {
+      lg[0] = mfma_bf16(w2op[m], hhi[m], lg[0]);
+      lg[0] = mfma_bf16(w2op[m], hlo[m], lg[0]);
+    }
     mfma_priority_end();
   }
 

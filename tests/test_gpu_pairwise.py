@@ -12,7 +12,7 @@ import torch
 import synth
 from oracle import mol_oracle as mo
 from paper_2407_15462_amd import mol
-from parity_helpers import check_topk_row, cuda_inputs, log, oracle_problem
+from parity_helpers import check_scores, check_topk_row, cuda_inputs, log, oracle_problem
 
 pytestmark = pytest.mark.gpu
 
@@ -150,3 +150,37 @@ def test_pairwise_softmax_redo_far_logits():
         s, i = s.cpu().numpy(), i.cpu().numpy()
         for b in range(spec.B):
             check_topk_row(phi[b], i[b], s[b], k, f"pairwise redo P={P} query {b}")
+
+
+# the two-term gating chain (MOL_FLAG_BF16X2_GATING) on the pair-wise path:
+# both MLP forms (P <= 16 and the padded 16x16x32 one), at gating weights of
+# standard deviation 1, the top of the flag's stated range
+X2_SHAPES = [s for s in SHAPES if s[0] in ("p12_h32_d64", "p16_h48_d96", "p24_h100_d128", "p48_h64_d64",
+                                           "p64_h128_d64")]
+
+
+@pytest.mark.parametrize("name,Pq,Px,d,H,side", X2_SHAPES, ids=[s[0] for s in X2_SHAPES])
+def test_pairwise_bf16x2_gating(name, Pq, Px, d, H, side):
+    spec = dataclasses.replace(_spec(Pq, Px, d, H, side), gating_std=1.0)
+    k = 50
+    log(f"[pairwise bf16x2] {name} B={spec.B} N={spec.N} P={spec.P} d={d} H={H} std={spec.gating_std}")
+    inp = cuda_inputs(spec, seed=62)
+    prob = mol.Problem.from_inputs(inp, flags=mol.MOL_FLAG_BF16X2_GATING)
+    phi = mol.score(prob)
+    s, i = mol.topk_exact(prob, k)
+    g = torch.Generator(device="cuda").manual_seed(10)
+    cand = torch.randint(0, spec.N, (spec.B, 333), device="cuda", generator=g, dtype=torch.int32)
+    rs, ri, _ = mol.rerank(prob, cand, k)
+    bs, bi = mol.topk_exact_bounded(prob, k, s[:, k - 1].contiguous())
+    torch.cuda.synchronize()
+    want = mo.mol_scores(oracle_problem(inp), list(range(spec.B)))
+    check_scores(phi.cpu().numpy(), want, what=f"pairwise_bf16x2 {name} phi")
+    s, i, rs, ri = s.cpu().numpy(), i.cpu().numpy(), rs.cpu().numpy(), ri.cpu().numpy()
+    bs, bi, cand_np = bs.cpu().numpy(), bi.cpu().numpy(), cand.cpu().numpy()
+    for b in range(spec.B):
+        check_topk_row(want[b], i[b], s[b], k, f"pairwise_bf16x2 {name} exact query {b}")
+        check_topk_row(want[b], bi[b], bs[b], k, f"pairwise_bf16x2 {name} bounded query {b}")
+        uniq = mo.union_dedup([cand_np[b]])
+        full = np.full(spec.N, -np.inf)
+        full[uniq] = want[b][uniq]
+        check_topk_row(full, ri[b], rs[b], k, f"pairwise_bf16x2 {name} rerank query {b}")
